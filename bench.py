@@ -1,0 +1,418 @@
+#!/usr/bin/env python3
+"""Benchmark of the band-attention hot path on one MI355X.
+
+One step = sa_forward + sa_backward over one batch of the SA forward+backward
+workload (B=16, T=800, H=12, d=64, Lb=64, La=8, lengths U[400, 800], bf16,
+synthetic N(0,1)/sqrt(d) inputs and N(0,1) upstream gradient). The headline
+value is valid frames per second over the whole step. Inputs are resident in
+HBM before timing; four copies of the batch are rotated so that no step finds
+its inputs in the 256 MB Infinity Cache.
+
+The same run also times, on their own workloads:
+  * llsa_forward, two-branch, same shapes (rows "llsa");
+  * sa_stream_step, 64 streams x 1000 steps, ring of 64 + 8 + 1 frames, eager
+    and replayed from a HIP graph (row "stream");
+  * masked full attention in PyTorch (dense T x T scores, band mask) as the
+    GPU baseline the paper argues against (row "masked_attention_torch");
+  * the CPU oracle on the host cores (``cpu_baseline``).
+
+Prints one JSON line. ``--gpus N`` with N > 1 is not supported (one GPU).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2302_13451_amd import accounting as acc  # noqa: E402
+from paper_2302_13451_amd import binding as bd  # noqa: E402
+from paper_2302_13451_amd.inputs import llsa_inputs, sa_inputs, stream_inputs  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
+BF16_DENSE_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, published
+
+WORKLOAD = dict(B=16, T=800, H=12, d=64, Lb=64, La=8, lengths=(400, 800), seed=3)
+STREAM = dict(S=64, H=12, d=64, Lb=64, La=8, steps=1000, seed=5)
+N_SETS = 4
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def source_sha(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2302_13451_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(profile_name, sha):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", profile_name)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha") != sha:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+class EventTimer:
+    """Accumulates the duration of one kernel launch at a time with HIP events
+    recorded on the stream the library launches on."""
+
+    def __init__(self):
+        self.pairs = []
+
+    def start(self):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def stop(self, s):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.pairs.append((s, e))
+
+    def mean_ms(self):
+        return sum(s.elapsed_time(e) for s, e in self.pairs) / max(1, len(self.pairs))
+
+    def all_ms(self):
+        return [s.elapsed_time(e) for s, e in self.pairs]
+
+
+def sa_sets(w):
+    x = sa_inputs(w["B"], w["T"], w["H"], w["d"], w["seed"], dtype="bf16",
+                  lengths=w["lengths"])
+    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v", "dout")}
+    lengths = x["lengths"].cuda()
+    sets = []
+    for i in range(N_SETS):
+        s = {n: (t if i == 0 else t.clone()) for n, t in base.items()}
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty(w["B"], w["H"], w["T"], dtype=torch.float32, device="cuda")
+        s["dq"] = torch.empty_like(s["q"])
+        s["dk"] = torch.empty_like(s["q"])
+        s["dv"] = torch.empty_like(s["q"])
+        sets.append(s)
+    return sets, lengths, x["lengths"].tolist()
+
+
+def sa_step(s, lengths, w, tf=None, tb=None):
+    e = tf.start() if tf else None
+    bd.sa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"], lse=s["lse"])
+    if tf:
+        tf.stop(e)
+    e = tb.start() if tb else None
+    bd.sa_backward(s["q"], s["k"], s["v"], s["out"], s["lse"], s["dout"], w["Lb"], w["La"],
+                   lengths, dq=s["dq"], dk=s["dk"], dv=s["dv"])
+    if tb:
+        tb.stop(e)
+
+
+def bench_sa(steps, warmup):
+    w = WORKLOAD
+    sets, lengths, host_lengths = sa_sets(w)
+    for i in range(warmup):
+        sa_step(sets[i % N_SETS], lengths, w)
+    torch.cuda.synchronize()
+    tf, tb = EventTimer(), EventTimer()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        sa_step(sets[i % N_SETS], lengths, w, tf, tb)
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    return dict(total_ms=total_ms, fwd_ms=tf.mean_ms(), bwd_ms=tb.mean_ms(),
+                lengths=host_lengths)
+
+
+def bench_llsa(steps, warmup):
+    w = WORKLOAD
+    x = llsa_inputs(w["B"], w["T"], w["H"], w["d"], 4, dtype="bf16", lengths=w["lengths"])
+    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v")}
+    lengths = x["lengths"].cuda()
+    sets = []
+    for i in range(N_SETS):
+        s = {n: (t if i == 0 else t.clone()) for n, t in base.items()}
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty(2, w["B"], w["H"], w["T"], dtype=torch.float32, device="cuda")
+        sets.append(s)
+    for i in range(warmup):
+        s = sets[i % N_SETS]
+        bd.llsa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
+                        lse=s["lse"])
+    torch.cuda.synchronize()
+    t = EventTimer()
+    for i in range(steps):
+        s = sets[i % N_SETS]
+        e = t.start()
+        bd.llsa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
+                        lse=s["lse"])
+        t.stop(e)
+    torch.cuda.synchronize()
+    L = x["lengths"].tolist()
+    ms = t.mean_ms()
+    byts = acc.llsa_forward_bytes(L, w["H"], w["d"])
+    flops = acc.llsa_forward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
+    return {
+        "workload": "LLSA forward (two-branch) bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, "
+                    "lengths U[400,800]",
+        "ms_per_call": ms,
+        "frames_per_s": sum(L) / (ms * 1e-3),
+        "useful_tflops": flops / (ms * 1e-3) / 1e12,
+        "algorithmic_gbs": byts / (ms * 1e-3) / 1e9,
+        "roofline": {"bound": "hbm", "achieved": byts / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": byts / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": load_traffic("band_fwd_llsa_traffic.json",
+                                             source_sha("band_fwd.hip"))},
+        "algorithmic_bytes": byts,
+        "useful_flops": flops,
+    }
+
+
+def bench_stream():
+    c = STREAM
+    S, H, d, Lb, La, steps = c["S"], c["H"], c["d"], c["Lb"], c["La"], c["steps"]
+    R = Lb + La + 1
+    x = stream_inputs(steps, S, H, d, c["seed"], dtype="bf16")
+    q, k, v = (x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v"))
+    st = bd.StreamState(S, H, d, Lb, La, R)
+    out = torch.empty(S, H, d, dtype=torch.bfloat16, device="cuda")
+    # eager, one launch per step, per-step latency from events
+    for u in range(20):
+        bd.sa_stream_step(st, q[u], k[u], v[u], out=out)
+    st = bd.StreamState(S, H, d, Lb, La, R)
+    torch.cuda.synchronize()
+    t = EventTimer()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for u in range(steps):
+        e = t.start()
+        bd.sa_stream_step(st, q[u], k[u], v[u], out=out)
+        t.stop(e)
+    end.record()
+    torch.cuda.synchronize()
+    eager_ms = start.elapsed_time(end)
+    lat = sorted(t.all_ms())
+    # graph: capture 100 steps, replay 10 times (the counters advance on the device)
+    n_cap = 100
+    st = bd.StreamState(S, H, d, Lb, La, R)
+    qb = torch.empty(n_cap, S, H, d, dtype=torch.bfloat16, device="cuda")
+    kb, vb = torch.empty_like(qb), torch.empty_like(qb)
+    side = bd.StreamState(S, H, d, Lb, La, R)
+    bd.sa_stream_step(side, q[0], k[0], v[0], out=out)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n_cap):
+            bd.sa_stream_step(st, qb[i], kb[i], vb[i], out=out)
+    torch.cuda.synchronize()
+    g_ms = 0.0
+    for r in range(steps // n_cap):
+        sl = slice(r * n_cap, (r + 1) * n_cap)
+        qb.copy_(q[sl])
+        kb.copy_(k[sl])
+        vb.copy_(v[sl])
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        graph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        g_ms += s0.elapsed_time(s1)
+    # steady-state step (every stream emitting over a full window)
+    widths = [Lb + La + 1] * S
+    byts = acc.stream_step_bytes(widths, S, H, d)
+    flops = acc.stream_step_flops(widths, H, d)
+    mean_step = t.mean_ms()
+    return {
+        "workload": "SA streaming step bf16, 64 streams x 1000 steps, H=12, d=64, ring 64 past + "
+                    "8 look-ahead + current",
+        "eager_steps_per_s": steps / (eager_ms * 1e-3),
+        "eager_frames_per_s": S * steps / (eager_ms * 1e-3),
+        "graph_steps_per_s": steps / (g_ms * 1e-3),
+        "graph_frames_per_s": S * steps / (g_ms * 1e-3),
+        "step_latency_ms_p50": lat[len(lat) // 2],
+        "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
+        "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
+        "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
+        "note": "ring is L2/MALL resident; the step is launch-bound",
+    }
+
+
+def bench_masked_attention(steps=5):
+    """Masked full attention (dense T x T scores + band mask) in PyTorch,
+    forward+backward, bf16 inputs with float32 softmax, same workload."""
+    w = WORKLOAD
+    x = sa_inputs(w["B"], w["T"], w["H"], w["d"], w["seed"], dtype="bf16", lengths=w["lengths"])
+    T = w["T"]
+    t = torch.arange(T, device="cuda")
+    L = x["lengths"].cuda()
+    band = (t[None, :] >= t[:, None] - w["Lb"]) & (t[None, :] <= t[:, None] + w["La"])
+    mask = band[None, None] & (t[None, None, None, :] < L[:, None, None, None])
+    rows = (t[None, :] < L[:, None])[:, None, :, None]
+    q, k, v, do = (x[n].to(torch.bfloat16).cuda().permute(0, 2, 1, 3).contiguous()
+                   for n in ("q", "k", "v", "dout"))
+
+    def step():
+        qq, kk, vv = (a.detach().requires_grad_(True) for a in (q, k, v))
+        s = torch.matmul(qq.float(), kk.float().transpose(-1, -2).contiguous()) / math.sqrt(w["d"])
+        s = s.masked_fill(~mask, float("-inf"))
+        p = torch.softmax(s, dim=-1)
+        p = torch.where(rows, p, torch.zeros_like(p))
+        o = torch.matmul(p, vv.float())
+        o.backward(do.float())
+        return o
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for _ in range(steps):
+        step()
+    s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1) / steps
+    return {"workload": "masked full attention fwd+bwd in PyTorch (float32 math on bf16 inputs), "
+                        "same batch", "ms_per_step": ms,
+            "frames_per_s": sum(x["lengths"].tolist()) / (ms * 1e-3)}
+
+
+def cpu_baseline(min_seconds=10.0):
+    """The fp64 oracle on the host cores: repeated passes of forward+backward
+    over the first sequences of the workload until ~10 s have elapsed."""
+    import oracle
+
+    w = WORKLOAD
+    x = sa_inputs(w["B"], w["T"], w["H"], w["d"], w["seed"], dtype="bf16", lengths=w["lengths"])
+    nseq = 4
+    q, k, v, do = (x[n][:nseq].double().numpy() for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"][:nseq].numpy()
+    threads = min(os.cpu_count() or 1, 16)
+    oracle._load()
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        oracle.sa_forward(q, k, v, w["Lb"], w["La"], ln, threads=threads)
+        oracle.sa_backward(q, k, v, do, w["Lb"], w["La"], ln, threads=threads)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or passes >= 50:
+            break
+    frames = int(ln.sum()) * passes
+    return {"value": frames / el, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": "%d passes of forward+backward over the first %d sequences (%d frames, all "
+                      "12 heads) of the workload, %.1f s" % (passes, nseq, int(ln.sum()), el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the SA forward+backward step")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of 512 MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: --gpus %d is not supported (the band kernels shard "
+              "over batch and heads with no communication; see the design notes)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        n = 512 << 20
+        src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n}))
+        return
+    bd.load_library()
+    log("SA forward+backward: %d warmup + %d timed steps" % (args.warmup, args.steps))
+    r = bench_sa(args.steps, args.warmup)
+    w = WORKLOAD
+    L = r["lengths"]
+    frames = sum(L)
+    step_s = r["total_ms"] * 1e-3 / args.steps
+    fwd_b = acc.sa_forward_bytes(L, w["H"], w["d"])
+    bwd_b = acc.sa_backward_bytes(L, w["H"], w["d"])
+    fwd_f = acc.sa_forward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
+    bwd_f = acc.sa_backward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
+    fwd_gbs = fwd_b / (r["fwd_ms"] * 1e-3) / 1e9
+    bwd_gbs = bwd_b / (r["bwd_ms"] * 1e-3) / 1e9
+    dominant = "sa_backward" if r["bwd_ms"] >= r["fwd_ms"] else "sa_forward"
+    dom_gbs = bwd_gbs if dominant == "sa_backward" else fwd_gbs
+    dom_sha = source_sha("band_bwd.hip") if dominant == "sa_backward" else source_sha("band_fwd.hip")
+    traffic_file = ("sa_bwd_traffic.json" if dominant == "sa_backward" else "sa_fwd_traffic.json")
+    line = {
+        "metric": "band-attention frames/s + TFLOP/s & HBM GB/s vs roofline (fwd+bwd)",
+        "value": frames / step_s,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["total_ms"] / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "SA forward+backward bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, "
+                               "lengths U[400,800] (20 ms frames)",
+                   "B": w["B"], "T": w["T"], "H": w["H"], "d": w["d"], "Lb": w["Lb"],
+                   "La": w["La"], "valid_frames": frames, "input_sets_rotated": N_SETS},
+        "roofline": {"bound": "hbm", "achieved": dom_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": dom_gbs / HBM_PEAK_GBS, "kernel": dominant,
+                     "traffic": load_traffic(traffic_file, dom_sha)},
+        "kernels": {
+            "sa_forward": {"ms": r["fwd_ms"], "algorithmic_bytes": fwd_b, "gbs": fwd_gbs,
+                           "hbm_frac": fwd_gbs / HBM_PEAK_GBS, "useful_flops": fwd_f,
+                           "tflops": fwd_f / (r["fwd_ms"] * 1e-3) / 1e12},
+            "sa_backward": {"ms": r["bwd_ms"], "algorithmic_bytes": bwd_b, "gbs": bwd_gbs,
+                            "hbm_frac": bwd_gbs / HBM_PEAK_GBS, "useful_flops": bwd_f,
+                            "tflops": bwd_f / (r["bwd_ms"] * 1e-3) / 1e12},
+        },
+        "useful_tflops_step": (fwd_f + bwd_f) / step_s / 1e12,
+        "algorithmic_gbs_step": (fwd_b + bwd_b) / step_s / 1e9,
+    }
+    if not args.no_extras:
+        log("LLSA forward")
+        line["llsa"] = bench_llsa(max(20, args.steps // 2), 5)
+        log("streaming step")
+        line["stream"] = bench_stream()
+        log("masked full attention in PyTorch")
+        try:
+            line["masked_attention_torch"] = bench_masked_attention()
+        except RuntimeError as e:  # e.g. out of memory on a smaller card
+            line["masked_attention_torch"] = {"error": str(e)[:200]}
+    if not args.no_cpu_baseline:
+        log("CPU oracle baseline")
+        line["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,349 @@
+// Band-attention forward for gfx950: SA (Eq. 4-6) and two-branch LLSA
+// (Eq. 14/15). Scores are computed directly on the band and never stored; the
+// softmax is online (running max and sum), so only the output rows and one
+// float log-sum-exp per row reach memory.
+//
+// bfloat16 path (MFMA): a workgroup of 4 waves owns 64 consecutive queries of
+// one (sequence, head); each wave owns 16 of them. The band of keys the tile
+// needs, [t0 + lo_off, t0 + 63 + hi_off] clipped to the valid frames, is
+// streamed through LDS in chunks of 64 frames: keys row-major, values
+// transposed (dimension-major), each loaded once from HBM with 16-byte
+// coalesced reads. Per 32-key block a wave computes S^T = K Q^T with
+// v_mfma_f32_16x16x32_bf16 (the 16 queries are the MFMA's N dimension, so
+// every lane owns exactly one query), updates the running max/sum with two
+// cross-lane exchanges, rounds the weights to bfloat16 and accumulates
+// O^T += V^T P^T with the same MFMA. Key rows are fed to the score MFMA in a
+// permuted order so that the score tile comes out in exactly the register
+// layout the weight operand of the PV MFMA needs: no shuffles between the two
+// products.
+//
+// float path (VALU): one thread per (query, head) walks its window with an
+// online softmax. It serves the float element type, where the band is too
+// narrow for float MFMA to pay.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace sa {
+namespace {
+
+constexpr int kTq = 64;       // queries per workgroup
+constexpr int kKC = 64;       // keys per LDS chunk
+constexpr int kThreads = 256;
+
+struct DevSeg {
+  const void* k;
+  const void* v;
+  int lo_off, hi_off;
+};
+
+struct DevJob {
+  const void* q;
+  DevSeg seg0, seg1;
+  int nseg;
+  void* out;
+  float* lse;
+};
+
+struct DevArgs {
+  DevJob job0, job1;
+  int B, T, H;
+  int ntiles;     // query tiles per (sequence, head)
+  int nlogical;   // workgroups doing work
+  const int32_t* lengths;
+  float scale_log2;  // log2(e) / sqrt(d)
+};
+
+template <int D>
+__device__ __forceinline__ void zero_rows_bf16(uint16_t* out, float* lse, int b, int h, int T,
+                                               int H, int r_begin, int r_end, int tid) {
+  constexpr int V = D / 8;
+  const int rows = r_end - r_begin;
+  for (int e = tid; e < rows * V; e += kThreads) {
+    const int r = e / V, c = e % V;
+    *reinterpret_cast<uint4*>(out + row_index(b, r_begin + r, h, T, H, D) + 8 * c) =
+        make_uint4(0, 0, 0, 0);
+  }
+  if (lse)
+    for (int r = tid; r < rows; r += kThreads)
+      lse[(static_cast<size_t>(b) * H + h) * T + r_begin + r] = kNegInf;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
+  constexpr int KS = D + 8;    // k_lds row stride (elements); 16-byte aligned rows
+  constexpr int VS = kKC + 8;  // vt_lds row stride
+  constexpr int NS = D / 32;   // MFMA k-steps over the head dim
+  constexpr int NB = D / 16;   // 16-wide blocks of the head dim in the output
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKC * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * VS];
+
+  int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
+  if (id >= a.nlogical) return;
+  const int tile = id % a.ntiles;
+  id /= a.ntiles;
+  const int h = id % a.H;
+  id /= a.H;
+  const int b = id % a.B;
+  const bool second = (id / a.B) != 0;
+  const DevJob& job = second ? a.job1 : a.job0;
+
+  const int T = a.T, H = a.H;
+  const int len = clamp_len(a.lengths, b, T);
+  const int t0 = tile * kTq;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int col = lane & 15, g = lane >> 4;
+  uint16_t* out = static_cast<uint16_t*>(job.out);
+  float* lse = job.lse;
+
+  if (t0 >= len) {  // padding tile: zeros, nothing read
+    zero_rows_bf16<D>(out, lse, b, h, T, H, t0, min(t0 + kTq, T), tid);
+    return;
+  }
+
+  const int r0 = t0 + 16 * w;   // first query of this wave
+  const int t = r0 + col;       // this lane's query
+  const bool qvalid = t < len;
+  const uint16_t* qp = static_cast<const uint16_t*>(job.q);
+
+  bf16x8 qf[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (qvalid) raw = *reinterpret_cast<const uint4*>(qp + row_index(b, t, h, T, H, D) + 32 * s + 8 * g);
+    qf[s] = __builtin_bit_cast(bf16x8, raw);
+  }
+
+  float m = kNegInf, lsum = 0.f;
+  f32x4 acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int tmax = min(t0 + kTq, len) - 1;  // last valid query of the tile
+  const int wmax = min(r0 + 15, len - 1);   // last valid query of the wave (< r0: none)
+
+  for (int si = 0; si < job.nseg; ++si) {
+    const DevSeg& sg = si ? job.seg1 : job.seg0;
+    const int klo = max(0, t0 + sg.lo_off);
+    const int khi = min(len - 1, tmax + sg.hi_off);
+    if (klo > khi) continue;  // uniform over the workgroup
+    const int wlo = max(0, r0 + sg.lo_off);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + sg.hi_off);
+    const int qlo = max(0, t + sg.lo_off);         // this lane's window in the segment
+    const int qhi = min(len - 1, t + sg.hi_off);
+    const uint16_t* kp = static_cast<const uint16_t*>(sg.k);
+    const uint16_t* vp = static_cast<const uint16_t*>(sg.v);
+
+    for (int cs = klo; cs <= khi; cs += kKC) {
+      const int cn = min(kKC, khi - cs + 1);
+      __syncthreads();  // previous chunk fully consumed
+      // keys, row-major; rows past the chunk are zero
+      for (int e = tid; e < kKC * (D / 8); e += kThreads) {
+        const int r = e / (D / 8), c = e % (D / 8);
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (r < cn) val = *reinterpret_cast<const uint4*>(kp + row_index(b, cs + r, h, T, H, D) + 8 * c);
+        *reinterpret_cast<uint4*>(k_lds + r * KS + 8 * c) = val;
+      }
+      // values, transposed two frames at a time (one 32-bit LDS word per dim)
+      for (int e = tid; e < (kKC / 2) * (D / 8); e += kThreads) {
+        const int p = e / (D / 8), c = e % (D / 8);
+        const int r = 2 * p;
+        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+        if (r < cn) v0 = *reinterpret_cast<const uint4*>(vp + row_index(b, cs + r, h, T, H, D) + 8 * c);
+        if (r + 1 < cn) v1 = *reinterpret_cast<const uint4*>(vp + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
+        const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+        const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t lo = (w0[j] & 0xffffu) | (w1[j] << 16);
+          const uint32_t hi = (w0[j] >> 16) | (w1[j] & 0xffff0000u);
+          *reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * j) * VS + r) = lo;
+          *reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * j + 1) * VS + r) = hi;
+        }
+      }
+      __syncthreads();
+      if (wlo > whi) continue;
+
+      for (int sb = 0; sb < kKC; sb += 32) {
+        const int kb = cs + sb;
+        if (sb >= cn || kb > whi || kb + 31 < wlo) continue;  // uniform over the wave
+        // score tiles: block 0 row r holds key sb + 8(r/4) + r%4, block 1 the
+        // same + 4, so lane (g, col) ends up with keys kb + 8g + 0..7
+        const int kr = sb + 8 * (col >> 2) + (col & 3);
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(k_lds + kr * KS + 32 * s + 8 * g);
+          const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(k_lds + (kr + 4) * KS + 32 * s + 8 * g);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[s], s1, 0, 0, 0);
+        }
+        float p[8];
+        float mloc = kNegInf;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = kb + 8 * g + j;
+          const float sv = (j < 4 ? s0[j] : s1[j - 4]) * a.scale_log2;
+          const bool ok = qvalid && key >= qlo && key <= qhi;
+          p[j] = ok ? sv : kNegInf;
+          mloc = fmaxf(mloc, p[j]);
+        }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float mnew = fmaxf(m, mloc);
+        const float msafe = (mnew == kNegInf) ? 0.f : mnew;
+        const float alpha = fast_exp2(m - msafe);
+        float psum = 0.f;
+        bf16x8 pf;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          p[j] = fast_exp2(p[j] - msafe);
+          psum += p[j];
+          pf[j] = static_cast<__bf16>(p[j]);
+        }
+        lsum = lsum * alpha + psum;
+        m = mnew;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          acc[i] *= alpha;
+          const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt_lds + (16 * i + col) * VS + sb + 8 * g);
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pf, acc[i], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (t < T) {
+    uint16_t* orow = out + row_index(b, t, h, T, H, D);
+    const float inv = qvalid ? 1.f / lsum : 0.f;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      uint2 pk;
+      pk.x = qvalid ? pack_bf16x2(acc[i][0] * inv, acc[i][1] * inv) : 0u;
+      pk.y = qvalid ? pack_bf16x2(acc[i][2] * inv, acc[i][3] * inv) : 0u;
+      *reinterpret_cast<uint2*>(orow + 16 * i + 4 * g) = pk;
+    }
+    if (lse && g == 0)
+      lse[(static_cast<size_t>(b) * H + h) * T + t] = qvalid ? (m + log2f(lsum)) * kLn2 : kNegInf;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void band_fwd_f32_kernel(DevArgs a, int njobs) {
+  const size_t total = static_cast<size_t>(njobs) * a.B * a.T * a.H;
+  for (size_t gid = static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x; gid < total;
+       gid += static_cast<size_t>(gridDim.x) * kThreads) {
+    size_t r = gid;
+    const int h = static_cast<int>(r % a.H);
+    r /= a.H;
+    const int t = static_cast<int>(r % a.T);
+    r /= a.T;
+    const int b = static_cast<int>(r % a.B);
+    const bool second = (r / a.B) != 0;
+    const DevJob& job = second ? a.job1 : a.job0;
+    const int T = a.T, H = a.H;
+    const int len = clamp_len(a.lengths, b, T);
+    float* orow = static_cast<float*>(job.out) + row_index(b, t, h, T, H, D);
+    float* lrow = job.lse ? job.lse + (static_cast<size_t>(b) * H + h) * T + t : nullptr;
+    if (t >= len) {
+#pragma unroll
+      for (int i = 0; i < D; i += 4) *reinterpret_cast<float4*>(orow + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (lrow) *lrow = kNegInf;
+      continue;
+    }
+    float qv[D], acc[D];
+    const float* qrow = static_cast<const float*>(job.q) + row_index(b, t, h, T, H, D);
+#pragma unroll
+    for (int i = 0; i < D; i += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(qrow + i);
+      qv[i] = x.x; qv[i + 1] = x.y; qv[i + 2] = x.z; qv[i + 3] = x.w;
+      acc[i] = acc[i + 1] = acc[i + 2] = acc[i + 3] = 0.f;
+    }
+    float m = kNegInf, l = 0.f;
+    for (int si = 0; si < job.nseg; ++si) {
+      const DevSeg& sg = si ? job.seg1 : job.seg0;
+      const int lo = max(0, t + sg.lo_off), hi = min(len - 1, t + sg.hi_off);
+      const float* kp = static_cast<const float*>(sg.k);
+      const float* vp = static_cast<const float*>(sg.v);
+      for (int key = lo; key <= hi; ++key) {
+        const float* krow = kp + row_index(b, key, h, T, H, D);
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < D; i += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(krow + i);
+          s += qv[i] * x.x + qv[i + 1] * x.y + qv[i + 2] * x.z + qv[i + 3] * x.w;
+        }
+        s *= a.scale_log2;
+        const float mnew = fmaxf(m, s);
+        const float alpha = fast_exp2(m - mnew);
+        const float pw = fast_exp2(s - mnew);
+        l = l * alpha + pw;
+        m = mnew;
+        const float* vrow = vp + row_index(b, key, h, T, H, D);
+#pragma unroll
+        for (int i = 0; i < D; i += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(vrow + i);
+          acc[i] = acc[i] * alpha + pw * x.x;
+          acc[i + 1] = acc[i + 1] * alpha + pw * x.y;
+          acc[i + 2] = acc[i + 2] * alpha + pw * x.z;
+          acc[i + 3] = acc[i + 3] * alpha + pw * x.w;
+        }
+      }
+    }
+    const float inv = 1.f / l;
+#pragma unroll
+    for (int i = 0; i < D; i += 4)
+      *reinterpret_cast<float4*>(orow + i) = make_float4(acc[i] * inv, acc[i + 1] * inv, acc[i + 2] * inv, acc[i + 3] * inv);
+    if (lrow) *lrow = (m + log2f(l)) * kLn2;
+  }
+}
+
+DevSeg to_dev(const BandSegment& s) { return DevSeg{s.k, s.v, s.lo_off, s.hi_off}; }
+
+DevJob to_dev(const BandJob& j) {
+  DevJob d;
+  d.q = j.q;
+  d.seg0 = to_dev(j.seg[0]);
+  d.seg1 = j.nseg > 1 ? to_dev(j.seg[1]) : d.seg0;
+  d.nseg = j.nseg;
+  d.out = j.out;
+  d.lse = j.lse;
+  return d;
+}
+
+}  // namespace
+
+hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_t stream) {
+  DevArgs d;
+  d.job0 = to_dev(a.job[0]);
+  d.job1 = a.njobs > 1 ? to_dev(a.job[1]) : d.job0;
+  d.B = a.B;
+  d.T = a.T;
+  d.H = a.H;
+  d.lengths = a.lengths;
+  d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
+  if (et == kBF16) {
+    d.ntiles = (a.T + kTq - 1) / kTq;
+    d.nlogical = a.njobs * a.B * a.H * d.ntiles;
+    const int grid = round_up8(d.nlogical);
+    if (a.d == 64)
+      hipLaunchKernelGGL(band_fwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
+    else
+      hipLaunchKernelGGL(band_fwd_bf16_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d);
+  } else {
+    d.ntiles = 0;
+    d.nlogical = 0;
+    const size_t total = static_cast<size_t>(a.njobs) * a.B * a.T * a.H;
+    const size_t blocks = (total + kThreads - 1) / kThreads;
+    const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
+    if (a.d == 64)
+      hipLaunchKernelGGL(band_fwd_f32_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d, a.njobs);
+    else
+      hipLaunchKernelGGL(band_fwd_f32_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d, a.njobs);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sa

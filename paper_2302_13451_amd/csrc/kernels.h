@@ -1,0 +1,64 @@
+// Host-side launchers of the band-attention kernels. Internal to libsa.so: the
+// C ABI in capi.cpp validates arguments and then calls these.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sa {
+
+enum ElemType { kF32 = 0, kBF16 = 1 };
+
+// One segment of a query's window: frames t + lo_off .. t + hi_off (clipped to
+// the valid frames), with keys and values read from k / v.
+struct BandSegment {
+  const void* k;
+  const void* v;
+  int lo_off;
+  int hi_off;
+};
+
+// One output of a band-forward launch: queries q, up to two window segments
+// that together form each query's receptive field, output rows and their
+// log-sum-exp (nullable).
+struct BandJob {
+  const void* q;
+  BandSegment seg[2];
+  int nseg;
+  void* out;
+  float* lse;
+};
+
+struct BandForwardArgs {
+  BandJob job[2];
+  int njobs;
+  int B, T, H, d;
+  const int32_t* lengths;
+};
+
+hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_t stream);
+
+struct SaBackwardArgs {
+  const void *q, *k, *v, *out, *dout;
+  const float* lse;
+  void *dq, *dk, *dv;
+  int B, T, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+hipError_t launch_sa_backward(const SaBackwardArgs& a, ElemType et, hipStream_t stream);
+
+struct StreamStepArgs {
+  const void *q, *k, *v;
+  void* out;
+  void *q_ring, *k_ring, *v_ring;
+  int R;
+  int32_t* step;
+  int32_t* emitted;
+  int S, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+hipError_t launch_stream_step(const StreamStepArgs& a, ElemType et, hipStream_t stream);
+
+}  // namespace sa
