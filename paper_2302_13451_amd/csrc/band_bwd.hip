@@ -11,9 +11,22 @@
 // recomputed from the log-sum-exp the forward stored, so nothing of size
 // T x window is ever kept.
 //
-// This file holds the vector-ALU kernel: one thread per query row computes
-// dq, one thread per key row computes dk and dv. It serves the float element
-// type.
+// bfloat16 path (MFMA): one launch, two workgroup roles per 64-frame tile of a
+// (sequence, head). The key role owns 64 keys and sweeps the queries that see
+// them, [f0 - La, f0 + 63 + Lb], accumulating dk and dv in registers; the query
+// role owns 64 queries and sweeps their keys, [f0 - Lb, f0 + 63 + La],
+// accumulating dq. Every gradient row is produced by exactly one workgroup, so
+// there are no atomics and no workspace, and the result is deterministic. The
+// two roles of a tile get adjacent logical ids and the ids are laid out
+// contiguously per XCD, so the second read of a tile's q, k, v, out and dout
+// usually hits that XCD's L2. The swept operand is staged through LDS in
+// 64-frame chunks, row-major for the score-side products and transposed for the
+// products that contract over frames; each wave keeps its own 16 rows in
+// registers as the MFMA's N operand, so every lane owns one key (key role) or
+// one query (query role) and the softmax statistics it needs are per lane.
+//
+// float path (VALU): one thread per query row computes dq, one thread per key
+// row computes dk and dv.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -166,6 +179,298 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_valu_kernel(SaBackwardArgs a)
   }
 }
 
+constexpr int kC = 64;  // frames per tile and per LDS chunk
+
+struct BwdDev {
+  const uint16_t *q, *k, *v, *o, *dout;
+  const float* lse;
+  uint16_t *dq, *dk, *dv;
+  int B, T, H, Lb, La;
+  int ntiles, nlogical;
+  const int32_t* lengths;
+  float scale, scale_log2;
+};
+
+__device__ __forceinline__ bf16x8 ld8(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+}
+
+__device__ __forceinline__ bf16x8 lds8(const uint16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+// Stage frames [cs, cs + cn) of one (sequence, head) of X into LDS: row-major
+// into rm (stride D + 8) and/or transposed into tr (stride kC + 8). Rows past
+// cn are zero. When `o` is given, X is dout and the row dots dout . out go to
+// dn together with lse2 = lse * log2(e) of each row.
+template <int D, bool ROWMAJOR, bool TRANS>
+__device__ __forceinline__ void stage_rows(const uint16_t* X, const uint16_t* o, const float* lse,
+                                           int b, int h, int T, int H, int cs, int cn,
+                                           uint16_t* rm, uint16_t* tr, float* dn, float* lse2,
+                                           int tid) {
+  constexpr int RS = D + 8, TS = kC + 8, CH = D / 8;
+  for (int e = tid; e < (kC / 2) * CH; e += kThreads) {
+    const int p = e / CH, c = e % CH;
+    const int r = 2 * p;
+    uint4 x0 = make_uint4(0, 0, 0, 0), x1 = make_uint4(0, 0, 0, 0);
+    if (r < cn) x0 = *reinterpret_cast<const uint4*>(X + row_index(b, cs + r, h, T, H, D) + 8 * c);
+    if (r + 1 < cn) x1 = *reinterpret_cast<const uint4*>(X + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
+    if (ROWMAJOR) {
+      *reinterpret_cast<uint4*>(rm + r * RS + 8 * c) = x0;
+      *reinterpret_cast<uint4*>(rm + (r + 1) * RS + 8 * c) = x1;
+    }
+    const uint32_t w0[4] = {x0.x, x0.y, x0.z, x0.w};
+    const uint32_t w1[4] = {x1.x, x1.y, x1.z, x1.w};
+    if (TRANS) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint32_t*>(tr + (8 * c + 2 * j) * TS + r) = (w0[j] & 0xffffu) | (w1[j] << 16);
+        *reinterpret_cast<uint32_t*>(tr + (8 * c + 2 * j + 1) * TS + r) = (w0[j] >> 16) | (w1[j] & 0xffff0000u);
+      }
+    }
+    if (o) {
+      uint4 y0 = make_uint4(0, 0, 0, 0), y1 = make_uint4(0, 0, 0, 0);
+      if (r < cn) y0 = *reinterpret_cast<const uint4*>(o + row_index(b, cs + r, h, T, H, D) + 8 * c);
+      if (r + 1 < cn) y1 = *reinterpret_cast<const uint4*>(o + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
+      const uint32_t z0[4] = {y0.x, y0.y, y0.z, y0.w};
+      const uint32_t z1[4] = {y1.x, y1.y, y1.z, y1.w};
+      float d0 = 0.f, d1 = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        d0 += bf2f(w0[j] & 0xffffu) * bf2f(z0[j] & 0xffffu) + bf2f(w0[j] >> 16) * bf2f(z0[j] >> 16);
+        d1 += bf2f(w1[j] & 0xffffu) * bf2f(z1[j] & 0xffffu) + bf2f(w1[j] >> 16) * bf2f(z1[j] >> 16);
+      }
+      // the CH threads of a row pair are consecutive lanes
+#pragma unroll
+      for (int m = 1; m < CH; m <<= 1) {
+        d0 += __shfl_xor(d0, m);
+        d1 += __shfl_xor(d1, m);
+      }
+      if (c == 0) {
+        dn[r] = d0;
+        dn[r + 1] = d1;
+        const float* lrow = lse + (static_cast<size_t>(b) * H + h) * T + cs;
+        lse2[r] = r < cn ? lrow[r] * kLog2e : 0.f;
+        lse2[r + 1] = r + 1 < cn ? lrow[r + 1] * kLog2e : 0.f;
+      }
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void zero_rows(uint16_t* x, uint16_t* y, int b, int h, int T, int H,
+                                          int r_begin, int r_end, int tid) {
+  constexpr int V = D / 8;
+  for (int e = tid; e < (r_end - r_begin) * V; e += kThreads) {
+    const int r = e / V, c = e % V;
+    const size_t off = row_index(b, r_begin + r, h, T, H, D) + 8 * c;
+    *reinterpret_cast<uint4*>(x + off) = make_uint4(0, 0, 0, 0);
+    if (y) *reinterpret_cast<uint4*>(y + off) = make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_rows4(uint16_t* dst, const f32x4* acc, float mul, bool valid,
+                                            int g) {
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) {
+    uint2 pk;
+    pk.x = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    pk.y = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
+    *reinterpret_cast<uint2*>(dst + 16 * i + 4 * g) = pk;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
+  constexpr int RS = D + 8, TS = kC + 8;
+  constexpr int NS = D / 32, NB = D / 16;
+  __shared__ __attribute__((aligned(16))) uint16_t rm0[kC * RS];
+  __shared__ __attribute__((aligned(16))) uint16_t rm1[kC * RS];
+  __shared__ __attribute__((aligned(16))) uint16_t tr0[D * TS];
+  __shared__ __attribute__((aligned(16))) uint16_t tr1[D * TS];
+  __shared__ __attribute__((aligned(16))) float s_dn[kC];
+  __shared__ __attribute__((aligned(16))) float s_lse2[kC];
+
+  int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
+  if (id >= a.nlogical) return;
+  const bool key_role = (id & 1) == 0;
+  id >>= 1;
+  const int tile = id % a.ntiles;
+  id /= a.ntiles;
+  const int h = id % a.H;
+  const int b = id / a.H;
+  const int T = a.T, H = a.H, Lb = a.Lb, La = a.La;
+  const int len = clamp_len(a.lengths, b, T);
+  const int f0 = tile * kC;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int col = lane & 15, g = lane >> 4;
+
+  if (f0 >= len) {  // padding tile
+    if (key_role)
+      zero_rows<D>(a.dk, a.dv, b, h, T, H, f0, min(f0 + kC, T), tid);
+    else
+      zero_rows<D>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
+    return;
+  }
+  const int r0 = f0 + 16 * w;
+  const int me = r0 + col;  // this lane's key (key role) or query (query role)
+  const bool valid = me < len;
+  const int fmax = min(f0 + kC, len) - 1;
+  const int wmax = min(r0 + 15, len - 1);
+
+  if (key_role) {
+    bf16x8 kf[NS], vf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      kf[s] = valid ? ld8(a.k + row_index(b, me, h, T, H, D) + 32 * s + 8 * g) : bf16x8{};
+      vf[s] = valid ? ld8(a.v + row_index(b, me, h, T, H, D) + 32 * s + 8 * g) : bf16x8{};
+    }
+    f32x4 adv[NB], adk[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nlo = max(0, f0 - La), nhi = min(len - 1, fmax + Lb);
+    const int wlo = max(0, r0 - La);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
+    const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
+    for (int cs = nlo; cs <= nhi; cs += kC) {
+      const int cn = min(kC, nhi - cs + 1);
+      __syncthreads();
+      stage_rows<D, true, true>(a.q, nullptr, nullptr, b, h, T, H, cs, cn, rm0, tr0, nullptr,
+                                nullptr, tid);
+      stage_rows<D, true, true>(a.dout, a.o, a.lse, b, h, T, H, cs, cn, rm1, tr1, s_dn, s_lse2,
+                                tid);
+      __syncthreads();
+      if (wlo > whi) continue;
+      for (int sb = 0; sb < kC; sb += 32) {
+        const int qb = cs + sb;
+        if (sb >= cn || qb > whi || qb + 31 < wlo) continue;
+        const int qr = sb + 8 * (col >> 2) + (col & 3);
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + qr * RS + 32 * s + 8 * g), kf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + (qr + 4) * RS + 32 * s + 8 * g), kf[s], s1, 0, 0, 0);
+          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + qr * RS + 32 * s + 8 * g), vf[s], p0, 0, 0, 0);
+          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + (qr + 4) * RS + 32 * s + 8 * g), vf[s], p1, 0, 0, 0);
+        }
+        bf16x8 pf, dsf;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int lr = sb + 8 * g + j;  // local row of query qb + 8g + j
+          const int nq = cs + lr;
+          const float sv = j < 4 ? s0[j] : s1[j - 4];
+          const float dp = j < 4 ? p0[j] : p1[j - 4];
+          const bool ok = valid && nq >= mylo && nq <= myhi;
+          const float pw = ok ? fast_exp2(sv * a.scale_log2 - s_lse2[lr]) : 0.f;
+          pf[j] = static_cast<__bf16>(pw);
+          dsf[j] = static_cast<__bf16>(pw * (dp - s_dn[lr]));
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr1 + (16 * i + col) * TS + sb + 8 * g), pf, adv[i], 0, 0, 0);
+          adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr0 + (16 * i + col) * TS + sb + 8 * g), dsf, adk[i], 0, 0, 0);
+        }
+      }
+    }
+    if (me < T) {
+      store_rows4<D>(a.dv + row_index(b, me, h, T, H, D), adv, 1.f, valid, g);
+      store_rows4<D>(a.dk + row_index(b, me, h, T, H, D), adk, a.scale, valid, g);
+    }
+  } else {
+    bf16x8 qf[NS], df[NS];
+    float dn = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const size_t off = row_index(b, me, h, T, H, D) + 32 * s + 8 * g;
+      qf[s] = valid ? ld8(a.q + off) : bf16x8{};
+      const uint4 dr = valid ? *reinterpret_cast<const uint4*>(a.dout + off) : make_uint4(0, 0, 0, 0);
+      const uint4 orw = valid ? *reinterpret_cast<const uint4*>(a.o + off) : make_uint4(0, 0, 0, 0);
+      df[s] = __builtin_bit_cast(bf16x8, dr);
+      const uint32_t x[4] = {dr.x, dr.y, dr.z, dr.w}, y[4] = {orw.x, orw.y, orw.z, orw.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        dn += bf2f(x[j] & 0xffffu) * bf2f(y[j] & 0xffffu) + bf2f(x[j] >> 16) * bf2f(y[j] >> 16);
+    }
+    dn += __shfl_xor(dn, 16);
+    dn += __shfl_xor(dn, 32);
+    const float lse2 = valid ? a.lse[(static_cast<size_t>(b) * H + h) * T + me] * kLog2e : 0.f;
+    f32x4 aq[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La);
+    const int wlo = max(0, r0 - Lb);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
+    const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
+    for (int cs = klo; cs <= khi; cs += kC) {
+      const int cn = min(kC, khi - cs + 1);
+      __syncthreads();
+      stage_rows<D, true, true>(a.k, nullptr, nullptr, b, h, T, H, cs, cn, rm0, tr0, nullptr,
+                                nullptr, tid);
+      stage_rows<D, true, false>(a.v, nullptr, nullptr, b, h, T, H, cs, cn, rm1, nullptr,
+                                 nullptr, nullptr, tid);
+      __syncthreads();
+      if (wlo > whi) continue;
+      for (int sb = 0; sb < kC; sb += 32) {
+        const int kb = cs + sb;
+        if (sb >= cn || kb > whi || kb + 31 < wlo) continue;
+        const int kr = sb + 8 * (col >> 2) + (col & 3);
+        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + kr * RS + 32 * s + 8 * g), qf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + (kr + 4) * RS + 32 * s + 8 * g), qf[s], s1, 0, 0, 0);
+          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + kr * RS + 32 * s + 8 * g), df[s], p0, 0, 0, 0);
+          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + (kr + 4) * RS + 32 * s + 8 * g), df[s], p1, 0, 0, 0);
+        }
+        bf16x8 dsf;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = kb + 8 * g + j;
+          const float sv = j < 4 ? s0[j] : s1[j - 4];
+          const float dp = j < 4 ? p0[j] : p1[j - 4];
+          const bool ok = valid && key >= mylo && key <= myhi;
+          const float pw = ok ? fast_exp2(sv * a.scale_log2 - lse2) : 0.f;
+          dsf[j] = static_cast<__bf16>(pw * (dp - dn));
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+          aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr0 + (16 * i + col) * TS + sb + 8 * g), dsf, aq[i], 0, 0, 0);
+      }
+    }
+    if (me < T) store_rows4<D>(a.dq + row_index(b, me, h, T, H, D), aq, a.scale, valid, g);
+  }
+}
+
+hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
+  BwdDev d;
+  d.q = static_cast<const uint16_t*>(a.q);
+  d.k = static_cast<const uint16_t*>(a.k);
+  d.v = static_cast<const uint16_t*>(a.v);
+  d.o = static_cast<const uint16_t*>(a.out);
+  d.dout = static_cast<const uint16_t*>(a.dout);
+  d.lse = a.lse;
+  d.dq = static_cast<uint16_t*>(a.dq);
+  d.dk = static_cast<uint16_t*>(a.dk);
+  d.dv = static_cast<uint16_t*>(a.dv);
+  d.B = a.B;
+  d.T = a.T;
+  d.H = a.H;
+  d.Lb = a.Lb;
+  d.La = a.La;
+  d.lengths = a.lengths;
+  d.scale = 1.f / sqrtf(static_cast<float>(a.d));
+  d.scale_log2 = kLog2e * d.scale;
+  d.ntiles = (a.T + kC - 1) / kC;
+  d.nlogical = 2 * a.B * a.H * d.ntiles;
+  const int grid = round_up8(d.nlogical);
+  if (a.d == 64)
+    hipLaunchKernelGGL(sa_bwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
+  else
+    hipLaunchKernelGGL(sa_bwd_bf16_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d);
+  return hipGetLastError();
+}
+
 template <typename E>
 hipError_t launch_valu(const SaBackwardArgs& a, hipStream_t stream) {
   const size_t total = 2 * static_cast<size_t>(a.B) * a.T * a.H;
@@ -181,7 +486,7 @@ hipError_t launch_valu(const SaBackwardArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_sa_backward(const SaBackwardArgs& a, ElemType et, hipStream_t stream) {
-  if (et == kBF16) return launch_valu<uint16_t>(a, stream);
+  if (et == kBF16) return launch_mfma(a, stream);
   return launch_valu<float>(a, stream);
 }
 
