@@ -26,6 +26,9 @@ HIPCC_FLAGS = [
     "-Wall",
     # keep hipcc from emitting packed float32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results and accumulators in VGPRs: the online softmax rescales the
+    # accumulators on the VALU, and AGPR round trips would double that cost
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", INCLUDE,
     "-I", CSRC,
 ]

@@ -19,11 +19,12 @@
 // there are no atomics and no workspace, and the result is deterministic. The
 // two roles of a tile get adjacent logical ids and the ids are laid out
 // contiguously per XCD, so the second read of a tile's q, k, v, out and dout
-// usually hits that XCD's L2. The swept operand is staged through LDS in
-// 64-frame chunks, row-major for the score-side products and transposed for the
-// products that contract over frames; each wave keeps its own 16 rows in
-// registers as the MFMA's N operand, so every lane owns one key (key role) or
-// one query (query role) and the softmax statistics it needs are per lane.
+// usually hits that XCD's L2. The swept operands are staged row-major through
+// LDS in 64-frame chunks (the next chunk's loads in flight while the current
+// one is computed); the products that contract over frames read them with the
+// transposing LDS read. Each wave keeps its own 16 rows in registers as the
+// MFMA's N operand, so every lane owns one key (key role) or one query (query
+// role) and the softmax statistics it needs are per lane.
 //
 // float path (VALU): one thread per query row computes dq, one thread per key
 // row computes dk and dv.
@@ -195,66 +196,13 @@ __device__ __forceinline__ bf16x8 ld8(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
 
-__device__ __forceinline__ bf16x8 lds8(const uint16_t* p) {
-  return *reinterpret_cast<const bf16x8*>(p);
-}
-
-// Stage frames [cs, cs + cn) of one (sequence, head) of X into LDS: row-major
-// into rm (stride D + 8) and/or transposed into tr (stride kC + 8). Rows past
-// cn are zero. When `o` is given, X is dout and the row dots dout . out go to
-// dn together with lse2 = lse * log2(e) of each row.
-template <int D, bool ROWMAJOR, bool TRANS>
-__device__ __forceinline__ void stage_rows(const uint16_t* X, const uint16_t* o, const float* lse,
-                                           int b, int h, int T, int H, int cs, int cn,
-                                           uint16_t* rm, uint16_t* tr, float* dn, float* lse2,
-                                           int tid) {
-  constexpr int RS = D + 8, TS = kC + 8, CH = D / 8;
-  for (int e = tid; e < (kC / 2) * CH; e += kThreads) {
-    const int p = e / CH, c = e % CH;
-    const int r = 2 * p;
-    uint4 x0 = make_uint4(0, 0, 0, 0), x1 = make_uint4(0, 0, 0, 0);
-    if (r < cn) x0 = *reinterpret_cast<const uint4*>(X + row_index(b, cs + r, h, T, H, D) + 8 * c);
-    if (r + 1 < cn) x1 = *reinterpret_cast<const uint4*>(X + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
-    if (ROWMAJOR) {
-      *reinterpret_cast<uint4*>(rm + r * RS + 8 * c) = x0;
-      *reinterpret_cast<uint4*>(rm + (r + 1) * RS + 8 * c) = x1;
-    }
-    const uint32_t w0[4] = {x0.x, x0.y, x0.z, x0.w};
-    const uint32_t w1[4] = {x1.x, x1.y, x1.z, x1.w};
-    if (TRANS) {
+__device__ __forceinline__ float dot8_bf16(const uint4& x, const uint4& y) {
+  const uint32_t a[4] = {x.x, x.y, x.z, x.w}, c[4] = {y.x, y.y, y.z, y.w};
+  float d = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint32_t*>(tr + (8 * c + 2 * j) * TS + r) = (w0[j] & 0xffffu) | (w1[j] << 16);
-        *reinterpret_cast<uint32_t*>(tr + (8 * c + 2 * j + 1) * TS + r) = (w0[j] >> 16) | (w1[j] & 0xffff0000u);
-      }
-    }
-    if (o) {
-      uint4 y0 = make_uint4(0, 0, 0, 0), y1 = make_uint4(0, 0, 0, 0);
-      if (r < cn) y0 = *reinterpret_cast<const uint4*>(o + row_index(b, cs + r, h, T, H, D) + 8 * c);
-      if (r + 1 < cn) y1 = *reinterpret_cast<const uint4*>(o + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
-      const uint32_t z0[4] = {y0.x, y0.y, y0.z, y0.w};
-      const uint32_t z1[4] = {y1.x, y1.y, y1.z, y1.w};
-      float d0 = 0.f, d1 = 0.f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        d0 += bf2f(w0[j] & 0xffffu) * bf2f(z0[j] & 0xffffu) + bf2f(w0[j] >> 16) * bf2f(z0[j] >> 16);
-        d1 += bf2f(w1[j] & 0xffffu) * bf2f(z1[j] & 0xffffu) + bf2f(w1[j] >> 16) * bf2f(z1[j] >> 16);
-      }
-      // the CH threads of a row pair are consecutive lanes
-#pragma unroll
-      for (int m = 1; m < CH; m <<= 1) {
-        d0 += __shfl_xor(d0, m);
-        d1 += __shfl_xor(d1, m);
-      }
-      if (c == 0) {
-        dn[r] = d0;
-        dn[r + 1] = d1;
-        const float* lrow = lse + (static_cast<size_t>(b) * H + h) * T + cs;
-        lse2[r] = r < cn ? lrow[r] * kLog2e : 0.f;
-        lse2[r + 1] = r + 1 < cn ? lrow[r + 1] * kLog2e : 0.f;
-      }
-    }
-  }
+  for (int j = 0; j < 4; ++j)
+    d += bf2f(a[j] & 0xffffu) * bf2f(c[j] & 0xffffu) + bf2f(a[j] >> 16) * bf2f(c[j] >> 16);
+  return d;
 }
 
 template <int D>
@@ -283,12 +231,13 @@ __device__ __forceinline__ void store_rows4(uint16_t* dst, const f32x4* acc, flo
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
-  constexpr int RS = D + 8, TS = kC + 8;
+  constexpr int RS = D + 8;                  // LDS row stride (elements)
   constexpr int NS = D / 32, NB = D / 16;
-  __shared__ __attribute__((aligned(16))) uint16_t rm0[kC * RS];
-  __shared__ __attribute__((aligned(16))) uint16_t rm1[kC * RS];
-  __shared__ __attribute__((aligned(16))) uint16_t tr0[D * TS];
-  __shared__ __attribute__((aligned(16))) uint16_t tr1[D * TS];
+  constexpr int CPR = D / 8;                 // 16-byte pieces per row
+  constexpr int CPT = kC * CPR / kThreads;   // pieces per thread per tensor per chunk
+  static_assert(CPT * kThreads == kC * CPR, "chunk must split evenly over the threads");
+  __shared__ __attribute__((aligned(16))) uint16_t rm0[kC * RS];  // key role: q   | query role: k
+  __shared__ __attribute__((aligned(16))) uint16_t rm1[kC * RS];  // key role: dout| query role: v
   __shared__ __attribute__((aligned(16))) float s_dn[kC];
   __shared__ __attribute__((aligned(16))) float s_lse2[kC];
 
@@ -318,28 +267,60 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
   const bool valid = me < len;
   const int fmax = min(f0 + kC, len) - 1;
   const int wmax = min(r0 + 15, len - 1);
+  const size_t my_off = row_index(b, me, h, T, H, D);
 
   if (key_role) {
+    // sweep the queries that see the tile's keys: [f0 - La, fmax + Lb]
+    const int nlo = max(0, f0 - La), nhi = min(len - 1, fmax + Lb);
+    const int nchunks = (nhi - nlo + kC) / kC;
+    uint4 qreg[CPT], dreg[CPT], oreg[CPT];
+    float lreg[CPT];
+    auto fetch = [&](int c) {
+      const int cs = nlo + c * kC, cn = min(kC, nhi - cs + 1);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+        qreg[i] = dreg[i] = oreg[i] = make_uint4(0, 0, 0, 0);
+        lreg[i] = 0.f;
+        if (r < cn) {
+          const size_t off = row_index(b, cs + r, h, T, H, D) + 8 * pc;
+          qreg[i] = *reinterpret_cast<const uint4*>(a.q + off);
+          dreg[i] = *reinterpret_cast<const uint4*>(a.dout + off);
+          oreg[i] = *reinterpret_cast<const uint4*>(a.o + off);
+          if (pc == 0) lreg[i] = a.lse[(static_cast<size_t>(b) * H + h) * T + cs + r];
+        }
+      }
+    };
+    fetch(0);
     bf16x8 kf[NS], vf[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kf[s] = valid ? ld8(a.k + row_index(b, me, h, T, H, D) + 32 * s + 8 * g) : bf16x8{};
-      vf[s] = valid ? ld8(a.v + row_index(b, me, h, T, H, D) + 32 * s + 8 * g) : bf16x8{};
+      kf[s] = valid ? ld8(a.k + my_off + 32 * s + 8 * g) : bf16x8{};
+      vf[s] = valid ? ld8(a.v + my_off + 32 * s + 8 * g) : bf16x8{};
     }
     f32x4 adv[NB], adk[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int nlo = max(0, f0 - La), nhi = min(len - 1, fmax + Lb);
     const int wlo = max(0, r0 - La);
     const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
     const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
-    for (int cs = nlo; cs <= nhi; cs += kC) {
-      const int cn = min(kC, nhi - cs + 1);
+    for (int c = 0; c < nchunks; ++c) {
+      const int cs = nlo + c * kC, cn = min(kC, nhi - cs + 1);
       __syncthreads();
-      stage_rows<D, true, true>(a.q, nullptr, nullptr, b, h, T, H, cs, cn, rm0, tr0, nullptr,
-                                nullptr, tid);
-      stage_rows<D, true, true>(a.dout, a.o, a.lse, b, h, T, H, cs, cn, rm1, tr1, s_dn, s_lse2,
-                                tid);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+        *reinterpret_cast<uint4*>(rm0 + r * RS + 8 * pc) = qreg[i];
+        *reinterpret_cast<uint4*>(rm1 + r * RS + 8 * pc) = dreg[i];
+        float dn = dot8_bf16(dreg[i], oreg[i]);
+#pragma unroll
+        for (int m = 1; m < CPR; m <<= 1) dn += __shfl_xor(dn, m);  // the row's pieces are adjacent lanes
+        if (pc == 0) {
+          s_dn[r] = dn;
+          s_lse2[r] = lreg[i] * kLog2e;
+        }
+      }
+      if (c + 1 < nchunks) fetch(c + 1);
       __syncthreads();
       if (wlo > whi) continue;
       for (int sb = 0; sb < kC; sb += 32) {
@@ -349,10 +330,10 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + qr * RS + 32 * s + 8 * g), kf[s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + (qr + 4) * RS + 32 * s + 8 * g), kf[s], s1, 0, 0, 0);
-          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + qr * RS + 32 * s + 8 * g), vf[s], p0, 0, 0, 0);
-          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + (qr + 4) * RS + 32 * s + 8 * g), vf[s], p1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + qr * RS + 32 * s + 8 * g), kf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (qr + 4) * RS + 32 * s + 8 * g), kf[s], s1, 0, 0, 0);
+          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + qr * RS + 32 * s + 8 * g), vf[s], p0, 0, 0, 0);
+          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (qr + 4) * RS + 32 * s + 8 * g), vf[s], p1, 0, 0, 0);
         }
         bf16x8 pf, dsf;
 #pragma unroll
@@ -366,31 +347,48 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
           pf[j] = static_cast<__bf16>(pw);
           dsf[j] = static_cast<__bf16>(pw * (dp - s_dn[lr]));
         }
+        // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-          adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr1 + (16 * i + col) * TS + sb + 8 * g), pf, adv[i], 0, 0, 0);
-          adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr0 + (16 * i + col) * TS + sb + 8 * g), dsf, adk[i], 0, 0, 0);
+          adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm1, sb, 16 * i, lane), pf, adv[i], 0, 0, 0);
+          adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm0, sb, 16 * i, lane), dsf, adk[i], 0, 0, 0);
         }
       }
     }
     if (me < T) {
-      store_rows4<D>(a.dv + row_index(b, me, h, T, H, D), adv, 1.f, valid, g);
-      store_rows4<D>(a.dk + row_index(b, me, h, T, H, D), adk, a.scale, valid, g);
+      store_rows4<D>(a.dv + my_off, adv, 1.f, valid, g);
+      store_rows4<D>(a.dk + my_off, adk, a.scale, valid, g);
     }
   } else {
+    // sweep the keys of the tile's queries: [f0 - Lb, fmax + La]
+    const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La);
+    const int nchunks = (khi - klo + kC) / kC;
+    uint4 kreg[CPT], vreg[CPT];
+    auto fetch = [&](int c) {
+      const int cs = klo + c * kC, cn = min(kC, khi - cs + 1);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+        kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
+        if (r < cn) {
+          const size_t off = row_index(b, cs + r, h, T, H, D) + 8 * pc;
+          kreg[i] = *reinterpret_cast<const uint4*>(a.k + off);
+          vreg[i] = *reinterpret_cast<const uint4*>(a.v + off);
+        }
+      }
+    };
+    fetch(0);
     bf16x8 qf[NS], df[NS];
     float dn = 0.f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const size_t off = row_index(b, me, h, T, H, D) + 32 * s + 8 * g;
-      qf[s] = valid ? ld8(a.q + off) : bf16x8{};
+      const size_t off = my_off + 32 * s + 8 * g;
+      const uint4 qr = valid ? *reinterpret_cast<const uint4*>(a.q + off) : make_uint4(0, 0, 0, 0);
       const uint4 dr = valid ? *reinterpret_cast<const uint4*>(a.dout + off) : make_uint4(0, 0, 0, 0);
       const uint4 orw = valid ? *reinterpret_cast<const uint4*>(a.o + off) : make_uint4(0, 0, 0, 0);
+      qf[s] = __builtin_bit_cast(bf16x8, qr);
       df[s] = __builtin_bit_cast(bf16x8, dr);
-      const uint32_t x[4] = {dr.x, dr.y, dr.z, dr.w}, y[4] = {orw.x, orw.y, orw.z, orw.w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        dn += bf2f(x[j] & 0xffffu) * bf2f(y[j] & 0xffffu) + bf2f(x[j] >> 16) * bf2f(y[j] >> 16);
+      dn += dot8_bf16(dr, orw);
     }
     dn += __shfl_xor(dn, 16);
     dn += __shfl_xor(dn, 32);
@@ -398,17 +396,19 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
     f32x4 aq[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La);
     const int wlo = max(0, r0 - Lb);
     const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
     const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
-    for (int cs = klo; cs <= khi; cs += kC) {
-      const int cn = min(kC, khi - cs + 1);
+    for (int c = 0; c < nchunks; ++c) {
+      const int cs = klo + c * kC, cn = min(kC, khi - cs + 1);
       __syncthreads();
-      stage_rows<D, true, true>(a.k, nullptr, nullptr, b, h, T, H, cs, cn, rm0, tr0, nullptr,
-                                nullptr, tid);
-      stage_rows<D, true, false>(a.v, nullptr, nullptr, b, h, T, H, cs, cn, rm1, nullptr,
-                                 nullptr, nullptr, tid);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+        *reinterpret_cast<uint4*>(rm0 + r * RS + 8 * pc) = kreg[i];
+        *reinterpret_cast<uint4*>(rm1 + r * RS + 8 * pc) = vreg[i];
+      }
+      if (c + 1 < nchunks) fetch(c + 1);
       __syncthreads();
       if (wlo > whi) continue;
       for (int sb = 0; sb < kC; sb += 32) {
@@ -418,10 +418,10 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + kr * RS + 32 * s + 8 * g), qf[s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm0 + (kr + 4) * RS + 32 * s + 8 * g), qf[s], s1, 0, 0, 0);
-          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + kr * RS + 32 * s + 8 * g), df[s], p0, 0, 0, 0);
-          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(rm1 + (kr + 4) * RS + 32 * s + 8 * g), df[s], p1, 0, 0, 0);
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + kr * RS + 32 * s + 8 * g), qf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (kr + 4) * RS + 32 * s + 8 * g), qf[s], s1, 0, 0, 0);
+          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + kr * RS + 32 * s + 8 * g), df[s], p0, 0, 0, 0);
+          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (kr + 4) * RS + 32 * s + 8 * g), df[s], p1, 0, 0, 0);
         }
         bf16x8 dsf;
 #pragma unroll
@@ -433,12 +433,13 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
           const float pw = ok ? fast_exp2(sv * a.scale_log2 - lse2) : 0.f;
           dsf[j] = static_cast<__bf16>(pw * (dp - dn));
         }
+        // dq^T += k^T dS^T, contracting over the 32 keys
 #pragma unroll
         for (int i = 0; i < NB; ++i)
-          aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds8(tr0 + (16 * i + col) * TS + sb + 8 * g), dsf, aq[i], 0, 0, 0);
+          aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm0, sb, 16 * i, lane), dsf, aq[i], 0, 0, 0);
       }
     }
-    if (me < T) store_rows4<D>(a.dq + row_index(b, me, h, T, H, D), aq, a.scale, valid, g);
+    if (me < T) store_rows4<D>(a.dq + my_off, aq, a.scale, valid, g);
   }
 }
 

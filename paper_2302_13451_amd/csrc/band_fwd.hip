@@ -6,10 +6,13 @@
 // bfloat16 path (MFMA): a workgroup of 4 waves owns 64 consecutive queries of
 // one (sequence, head); each wave owns 16 of them. The band of keys the tile
 // needs, [t0 + lo_off, t0 + 63 + hi_off] clipped to the valid frames, is
-// streamed through LDS in chunks of 64 frames: keys row-major, values
-// transposed (dimension-major), each loaded once from HBM with 16-byte
-// coalesced reads. Per 32-key block a wave computes S^T = K Q^T with
-// v_mfma_f32_16x16x32_bf16 (the 16 queries are the MFMA's N dimension, so
+// streamed through LDS in chunks of 64 frames, keys and values row-major, each
+// loaded once from HBM with 16-byte coalesced reads; the next chunk's loads are
+// issued before the current chunk is computed. The value operand of the PV
+// product, which contracts over frames, is read with the transposing LDS read
+// of gfx950, so no transposed copy is ever written. Per 32-key block a wave
+// computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (the 16 queries are the
+// MFMA's N dimension, so
 // every lane owns exactly one query), updates the running max/sum with two
 // cross-lane exchanges, rounds the weights to bfloat16 and accumulates
 // O^T += V^T P^T with the same MFMA. Key rows are fed to the score MFMA in a
@@ -70,12 +73,14 @@ __device__ __forceinline__ void zero_rows_bf16(uint16_t* out, float* lse, int b,
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
-  constexpr int KS = D + 8;    // k_lds row stride (elements); 16-byte aligned rows
-  constexpr int VS = kKC + 8;  // vt_lds row stride
-  constexpr int NS = D / 32;   // MFMA k-steps over the head dim
-  constexpr int NB = D / 16;   // 16-wide blocks of the head dim in the output
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKC * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * VS];
+  constexpr int RS = D + 8;                       // LDS row stride (elements), 16-byte rows
+  constexpr int NS = D / 32;                      // MFMA k-steps over the head dim
+  constexpr int NB = D / 16;                      // 16-wide blocks of the head dim
+  constexpr int CPR = D / 8;                      // 16-byte pieces per row
+  constexpr int CPT = kKC * CPR / kThreads;       // pieces per thread per tensor per chunk
+  static_assert(CPT * kThreads == kKC * CPR, "chunk must split evenly over the threads");
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKC * RS];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[kKC * RS];
 
   int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
   if (id >= a.nlogical) return;
@@ -105,8 +110,49 @@ __global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
   const int t = r0 + col;       // this lane's query
   const bool qvalid = t < len;
   const uint16_t* qp = static_cast<const uint16_t*>(job.q);
+  const int tmax = min(t0 + kTq, len) - 1;  // last valid query of the tile
+  const int wmax = min(r0 + 15, len - 1);   // last valid query of the wave (< r0: none)
+
+  // The chunks of every segment's band, [t0 + lo_off, tmax + hi_off] clipped,
+  // are visited as one sequence so the next chunk is always in flight.
+  int klo[2], nch[2];
+#pragma unroll
+  for (int si = 0; si < 2; ++si) {
+    const DevSeg& sg = si ? job.seg1 : job.seg0;
+    klo[si] = max(0, t0 + sg.lo_off);
+    const int khi = min(len - 1, tmax + sg.hi_off);
+    nch[si] = (si < job.nseg && klo[si] <= khi) ? (khi - klo[si] + kKC) / kKC : 0;
+  }
+  const int nchunks = nch[0] + nch[1];
+  auto chunk_seg = [&](int c) { return c < nch[0] ? 0 : 1; };
+  auto chunk_start = [&](int c) { return c < nch[0] ? klo[0] + c * kKC : klo[1] + (c - nch[0]) * kKC; };
+  auto chunk_rows = [&](int c) {
+    const int si = chunk_seg(c);
+    const DevSeg& sg = si ? job.seg1 : job.seg0;
+    return min(kKC, min(len - 1, tmax + sg.hi_off) - chunk_start(c) + 1);
+  };
+
+  uint4 kreg[CPT], vreg[CPT];
+  auto fetch = [&](int c) {
+    const int si = chunk_seg(c);
+    const DevSeg& sg = si ? job.seg1 : job.seg0;
+    const uint16_t* kp = static_cast<const uint16_t*>(sg.k);
+    const uint16_t* vp = static_cast<const uint16_t*>(sg.v);
+    const int cs = chunk_start(c), cn = chunk_rows(c);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+      kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
+      if (r < cn) {
+        const size_t off = row_index(b, cs + r, h, T, H, D) + 8 * pc;
+        kreg[i] = *reinterpret_cast<const uint4*>(kp + off);
+        vreg[i] = *reinterpret_cast<const uint4*>(vp + off);
+      }
+    }
+  };
 
   bf16x8 qf[NS];
+  if (nchunks > 0) fetch(0);
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     uint4 raw = make_uint4(0, 0, 0, 0);
@@ -119,97 +165,84 @@ __global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
 #pragma unroll
   for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int tmax = min(t0 + kTq, len) - 1;  // last valid query of the tile
-  const int wmax = min(r0 + 15, len - 1);   // last valid query of the wave (< r0: none)
+  for (int c = 0; c < nchunks; ++c) {
+    __syncthreads();  // previous chunk fully consumed
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
+      *reinterpret_cast<uint4*>(k_lds + r * RS + 8 * pc) = kreg[i];
+      *reinterpret_cast<uint4*>(v_lds + r * RS + 8 * pc) = vreg[i];
+    }
+    const int si = chunk_seg(c);
+    const int cs = chunk_start(c), cn = chunk_rows(c);
+    if (c + 1 < nchunks) fetch(c + 1);  // in flight while this chunk is computed
+    __syncthreads();
 
-  for (int si = 0; si < job.nseg; ++si) {
     const DevSeg& sg = si ? job.seg1 : job.seg0;
-    const int klo = max(0, t0 + sg.lo_off);
-    const int khi = min(len - 1, tmax + sg.hi_off);
-    if (klo > khi) continue;  // uniform over the workgroup
     const int wlo = max(0, r0 + sg.lo_off);
     const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + sg.hi_off);
-    const int qlo = max(0, t + sg.lo_off);         // this lane's window in the segment
+    if (wlo > whi) continue;
+    // this lane's window in the segment as (start, width): key is inside iff
+    // (unsigned)(key - qlo) <= width; an empty window never matches
+    const int qlo = qvalid ? max(0, t + sg.lo_off) : 0x7fffffff;
     const int qhi = min(len - 1, t + sg.hi_off);
-    const uint16_t* kp = static_cast<const uint16_t*>(sg.k);
-    const uint16_t* vp = static_cast<const uint16_t*>(sg.v);
+    const uint32_t qwidth = (qvalid && qhi >= qlo) ? static_cast<uint32_t>(qhi - qlo) : 0u;
+    const int qlo_l = (qvalid && qhi >= qlo) ? qlo : 0x7fffffff;
+    // keys inside the window of every valid query of the wave
+    const int ilo = max(0, wmax + sg.lo_off), ihi = min(len - 1, r0 + sg.hi_off);
 
-    for (int cs = klo; cs <= khi; cs += kKC) {
-      const int cn = min(kKC, khi - cs + 1);
-      __syncthreads();  // previous chunk fully consumed
-      // keys, row-major; rows past the chunk are zero
-      for (int e = tid; e < kKC * (D / 8); e += kThreads) {
-        const int r = e / (D / 8), c = e % (D / 8);
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (r < cn) val = *reinterpret_cast<const uint4*>(kp + row_index(b, cs + r, h, T, H, D) + 8 * c);
-        *reinterpret_cast<uint4*>(k_lds + r * KS + 8 * c) = val;
+    for (int sb = 0; sb < kKC; sb += 32) {
+      const int kb = cs + sb;
+      if (sb >= cn || kb > whi || kb + 31 < wlo) continue;  // uniform over the wave
+      // score tiles: block 0 row r holds key sb + 8(r/4) + r%4, block 1 the
+      // same + 4, so lane (g, col) ends up with keys kb + 8g + 0..7
+      const int kr = sb + 8 * (col >> 2) + (col & 3);
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(k_lds + kr * RS + 32 * s + 8 * g), qf[s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(k_lds + (kr + 4) * RS + 32 * s + 8 * g), qf[s], s1, 0, 0, 0);
       }
-      // values, transposed two frames at a time (one 32-bit LDS word per dim)
-      for (int e = tid; e < (kKC / 2) * (D / 8); e += kThreads) {
-        const int p = e / (D / 8), c = e % (D / 8);
-        const int r = 2 * p;
-        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-        if (r < cn) v0 = *reinterpret_cast<const uint4*>(vp + row_index(b, cs + r, h, T, H, D) + 8 * c);
-        if (r + 1 < cn) v1 = *reinterpret_cast<const uint4*>(vp + row_index(b, cs + r + 1, h, T, H, D) + 8 * c);
-        const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
-        const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
+      float z[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+      if (!(kb >= ilo && kb + 31 <= ihi)) {  // block crosses a window edge: mask
+        const int base = kb + 8 * g - qlo_l;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t lo = (w0[j] & 0xffffu) | (w1[j] << 16);
-          const uint32_t hi = (w0[j] >> 16) | (w1[j] & 0xffff0000u);
-          *reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * j) * VS + r) = lo;
-          *reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * j + 1) * VS + r) = hi;
-        }
+        for (int j = 0; j < 8; ++j)
+          z[j] = static_cast<uint32_t>(base + j) <= qwidth ? z[j] : kNegInf;
       }
-      __syncthreads();
-      if (wlo > whi) continue;
-
-      for (int sb = 0; sb < kKC; sb += 32) {
-        const int kb = cs + sb;
-        if (sb >= cn || kb > whi || kb + 31 < wlo) continue;  // uniform over the wave
-        // score tiles: block 0 row r holds key sb + 8(r/4) + r%4, block 1 the
-        // same + 4, so lane (g, col) ends up with keys kb + 8g + 0..7
-        const int kr = sb + 8 * (col >> 2) + (col & 3);
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      float zmax = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])),
+                         fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
+      zmax = fmaxf(zmax, __shfl_xor(zmax, 16));
+      zmax = fmaxf(zmax, __shfl_xor(zmax, 32));
+      const float mblk = zmax * a.scale_log2;
+      // Lazy rescaling: a row's exponent offset m only moves when its maximum
+      // grows by more than 2^8, so the weights stay below 256 and the
+      // accumulators are rarely touched. The decision is per row (the four
+      // lanes of a row hold the same mblk and m), so each output depends on
+      // its own window only, bit for bit.
+      const bool grow = mblk > m + 8.f;
+      if (__any(grow)) {
+        const float mnew = grow ? mblk : m;
+        const float alpha = grow ? fast_exp2(m - mnew) : 1.f;  // 0 on a row's first block
+        lsum *= alpha;
 #pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(k_lds + kr * KS + 32 * s + 8 * g);
-          const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(k_lds + (kr + 4) * KS + 32 * s + 8 * g);
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[s], s1, 0, 0, 0);
-        }
-        float p[8];
-        float mloc = kNegInf;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int key = kb + 8 * g + j;
-          const float sv = (j < 4 ? s0[j] : s1[j - 4]) * a.scale_log2;
-          const bool ok = qvalid && key >= qlo && key <= qhi;
-          p[j] = ok ? sv : kNegInf;
-          mloc = fmaxf(mloc, p[j]);
-        }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-        const float mnew = fmaxf(m, mloc);
-        const float msafe = (mnew == kNegInf) ? 0.f : mnew;
-        const float alpha = fast_exp2(m - msafe);
-        float psum = 0.f;
-        bf16x8 pf;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          p[j] = fast_exp2(p[j] - msafe);
-          psum += p[j];
-          pf[j] = static_cast<__bf16>(p[j]);
-        }
-        lsum = lsum * alpha + psum;
+        for (int i = 0; i < NB; ++i) acc[i] *= alpha;
         m = mnew;
-#pragma unroll
-        for (int i = 0; i < NB; ++i) {
-          acc[i] *= alpha;
-          const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt_lds + (16 * i + col) * VS + sb + 8 * g);
-          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pf, acc[i], 0, 0, 0);
-        }
       }
+      const float msafe = (m == kNegInf) ? 0.f : m;
+      float psum = 0.f;
+      bf16x8 pf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float pw = fast_exp2(__builtin_fmaf(z[j], a.scale_log2, -msafe));
+        psum += pw;
+        pf[j] = static_cast<__bf16>(pw);
+      }
+      lsum += psum;
+      // O^T += V^T P^T: lane (g, col) needs V[kb + 8g + j][16i + col]
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(v_lds, sb, 16 * i, lane), pf, acc[i], 0, 0, 0);
     }
   }
 

@@ -29,6 +29,30 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// MFMA operand of a product that contracts over frames, read from a row-major
+// LDS tile X (row stride RS elements) with two transposing reads
+// (ds_read_b64_tr_b16): lane (g = lane/16, c = lane%16) receives
+// X[r0 + 8g + j][c0 + c] for j = 0..7. Within each 16-lane group the 4 values
+// lane 4j+q loads become element j of lanes 4q..4q+3, so lane L of the group
+// points at row r0 + 8g + L/4 (then 4 rows further), columns c0 + 4(L%4).
+template <int RS>
+__device__ __forceinline__ bf16x8 lds_col8(const uint16_t* X, int r0, int c0, int lane) {
+  const int g = lane >> 4, L = lane & 15;
+  const uint16_t* p = X + (r0 + 8 * g + (L >> 2)) * RS + c0 + 4 * (L & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * RS));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// MFMA operand of a product that contracts over the head dim: 8 consecutive
+// elements of one LDS row.
+__device__ __forceinline__ bf16x8 lds_row8(const uint16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2). Remap so that every XCD walks one contiguous range of logical tiles:
 // neighbouring tiles of a sequence, which share their band halo, then run on
