@@ -51,8 +51,10 @@ def log(msg):
 
 
 def source_sha(*names):
+    """Hash of the kernel sources a counter summary was taken on (the shared
+    device header included)."""
     h = hashlib.sha256()
-    for n in names:
+    for n in names + ("device_common.h",):
         with open(os.path.join(ROOT, "paper_2302_13451_amd", "csrc", n), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
