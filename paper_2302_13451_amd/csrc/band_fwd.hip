@@ -50,6 +50,7 @@ struct DevJob {
 struct DevArgs {
   DevJob job0, job1;
   int B, T, H;
+  int njobs;      // outputs per launch (1: SA, 2: LLSA)
   int ntiles;     // query tiles per (sequence, head)
   int nlogical;   // workgroups doing work
   const int32_t* lengths;
@@ -84,12 +85,14 @@ __global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
 
   int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
   if (id >= a.nlogical) return;
+  // the outputs of a tile are adjacent ids: they read the same K/V band, which
+  // the second one then finds in the XCD's L2
+  const bool second = a.njobs > 1 && (id & 1);
+  id = a.njobs > 1 ? id >> 1 : id;
   const int tile = id % a.ntiles;
   id /= a.ntiles;
   const int h = id % a.H;
-  id /= a.H;
-  const int b = id % a.B;
-  const bool second = (id / a.B) != 0;
+  const int b = id / a.H;
   const DevJob& job = second ? a.job1 : a.job0;
 
   const int T = a.T, H = a.H;
@@ -352,6 +355,7 @@ hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_
   DevArgs d;
   d.job0 = to_dev(a.job[0]);
   d.job1 = a.njobs > 1 ? to_dev(a.job[1]) : d.job0;
+  d.njobs = a.njobs;
   d.B = a.B;
   d.T = a.T;
   d.H = a.H;

@@ -4,12 +4,15 @@
 // Lb + La + 1 keys: a matrix-vector shape, so it runs on the vector ALUs. One
 // workgroup serves one stream (the stream's step counter is read by every wave
 // and advanced once, after a workgroup barrier, so no other workgroup can see
-// it half-way); its waves take the heads in turn. Per head a wave
+// it half-way); each wave takes one head (more in turn when H > 16). Per head a
+// wave
 //   1. stores the new frame in the rings (slot u mod (La+1) for the query,
-//      u mod R for key and value);
-//   2. if frame t = u - La is due, scores its window with one key per lane,
-//      reduces max and sum across the wave, and accumulates the output with
-//      one head dimension per lane (each key row read as one coalesced line).
+//      u mod R for key and value), one 16-byte chunk per lane;
+//   2. if frame t = u - La is due, scores its window with one key per lane
+//      (whole 16-byte chunks of the key row), reduces max and sum across the
+//      wave, and accumulates the output with each lane owning one 16-byte
+//      chunk of the head dim for every 64/chunks-th key, followed by a short
+//      cross-lane sum.
 // The just-arrived frame u is taken from the input rather than from the ring
 // slot written in this same launch, so the kernel never reads its own stores.
 #include "device_common.h"
@@ -20,14 +23,37 @@
 namespace sa {
 namespace {
 
-constexpr int kMaxWaves = 8;
+constexpr int kMaxWaves = 16;
 
 template <typename E>
-__device__ __forceinline__ float ld(const E* p);
+__device__ __forceinline__ void unpack16(const uint4& x, float* f);
 template <>
-__device__ __forceinline__ float ld<float>(const float* p) { return *p; }
+__device__ __forceinline__ void unpack16<float>(const uint4& x, float* f) {
+  f[0] = __uint_as_float(x.x); f[1] = __uint_as_float(x.y);
+  f[2] = __uint_as_float(x.z); f[3] = __uint_as_float(x.w);
+}
 template <>
-__device__ __forceinline__ float ld<uint16_t>(const uint16_t* p) { return bf2f(*p); }
+__device__ __forceinline__ void unpack16<uint16_t>(const uint4& x, float* f) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+template <typename E>
+__device__ __forceinline__ uint4 pack16(const float* f, float mul);
+template <>
+__device__ __forceinline__ uint4 pack16<float>(const float* f, float mul) {
+  return make_uint4(__float_as_uint(f[0] * mul), __float_as_uint(f[1] * mul),
+                    __float_as_uint(f[2] * mul), __float_as_uint(f[3] * mul));
+}
+template <>
+__device__ __forceinline__ uint4 pack16<uint16_t>(const float* f, float mul) {
+  return make_uint4(pack_bf16x2(f[0] * mul, f[1] * mul), pack_bf16x2(f[2] * mul, f[3] * mul),
+                    pack_bf16x2(f[4] * mul, f[5] * mul), pack_bf16x2(f[6] * mul, f[7] * mul));
+}
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
@@ -49,16 +75,22 @@ struct DevStream {
   int32_t* step;
   int32_t* emitted;
   int S, H, Lb, La;
+  int wmax;  // Lb + La + 1: score slots per wave
   const int32_t* lengths;
   float scale_log2;
 };
 
 template <typename E, int D>
 __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a) {
-  __shared__ float wts[kMaxWaves][SA_STREAM_MAX_WINDOW];
+  constexpr int EPC = 16 / sizeof(E);   // elements per 16-byte chunk
+  constexpr int CH = D / EPC;           // chunks per row
+  constexpr int NKG = 64 / CH;          // key groups in the weighted sum
+  static_assert(CH * EPC == D && NKG * CH == 64, "row must split into 16-byte chunks");
+  extern __shared__ float wts_all[];
   const int s = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
+  float* wts = wts_all + w * a.wmax;
   const int H = a.H, La = a.La, R = a.R;
   const int QR = La + 1;
   const size_t HD = static_cast<size_t>(H) * D;
@@ -78,65 +110,80 @@ __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a
   E* qring = static_cast<E*>(a.q_ring) + static_cast<size_t>(s) * QR * HD;
   E* kring = static_cast<E*>(a.k_ring) + static_cast<size_t>(s) * R * HD;
   E* vring = static_cast<E*>(a.v_ring) + static_cast<size_t>(s) * R * HD;
+  auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
 
   for (int h = w; h < H; h += nw) {
     const size_t ho = static_cast<size_t>(h) * D;
-    if (append) {
-      const size_t qs = static_cast<size_t>(u % QR) * HD + ho;
-      const size_t ks = static_cast<size_t>(u % R) * HD + ho;
-      for (int i = lane; i < D; i += 64) {
-        qring[qs + i] = qin[ho + i];
-        kring[ks + i] = kin[ho + i];
-        vring[ks + i] = vin[ho + i];
-      }
+    if (append && lane < 3 * CH) {  // store the new frame: one 16-byte chunk per lane
+      const int which = lane / CH, c = lane % CH;
+      const E* src = which == 0 ? qin : (which == 1 ? kin : vin);
+      E* dst = which == 0 ? qring + static_cast<size_t>(u % QR) * HD
+                          : (which == 1 ? kring : vring) + static_cast<size_t>(u % R) * HD;
+      *reinterpret_cast<uint4*>(dst + ho + c * EPC) = chunk(src + ho, c);
     }
     if (!emit) {
-      for (int i = lane; i < D; i += 64) out[ho + i] = E(0);
+      if (lane < CH) *reinterpret_cast<uint4*>(out + ho + lane * EPC) = make_uint4(0, 0, 0, 0);
       continue;
     }
     const int lo = max(0, t - a.Lb);
     const int hi = min(len - 1, u);
     const int W = hi - lo + 1;
-    // the query of frame t: still in the input when La == 0, else in its ring slot
-    const E* qrow = (La == 0) ? qin + ho : qring + static_cast<size_t>(t % QR) * HD + ho;
+    // frame tau's row: the just-arrived frame u is still in the input
+    auto krow = [&](int tau) { return (tau == u ? kin : kring + static_cast<size_t>(tau % R) * HD) + ho; };
+    auto vrow = [&](int tau) { return (tau == u ? vin : vring + static_cast<size_t>(tau % R) * HD) + ho; };
+    const E* qrow = (La == 0 ? qin : qring + static_cast<size_t>(t % QR) * HD) + ho;
     float qv[D];
 #pragma unroll
-    for (int i = 0; i < D; ++i) qv[i] = ld<E>(qrow + i);
+    for (int c = 0; c < CH; ++c) unpack16<E>(chunk(qrow, c), qv + c * EPC);
 
+    // scores: one key per lane
     float mloc = kNegInf;
     for (int j = lane; j < W; j += 64) {
-      const int tau = lo + j;
-      const E* krow = (tau == u) ? kin + ho : kring + static_cast<size_t>(tau % R) * HD + ho;
+      const E* kr = krow(lo + j);
       float z = 0.f;
 #pragma unroll
-      for (int i = 0; i < D; ++i) z += qv[i] * ld<E>(krow + i);
+      for (int c = 0; c < CH; ++c) {
+        float kf[EPC];
+        unpack16<E>(chunk(kr, c), kf);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) z += qv[c * EPC + e] * kf[e];
+      }
       z *= a.scale_log2;
-      wts[w][j] = z;
+      wts[j] = z;
       mloc = fmaxf(mloc, z);
     }
     const float m = wave_max(mloc);
     float lpart = 0.f;
     for (int j = lane; j < W; j += 64) {
-      const float pw = fast_exp2(wts[w][j] - m);
-      wts[w][j] = pw;
+      const float pw = fast_exp2(wts[j] - m);
+      wts[j] = pw;
       lpart += pw;
     }
     const float inv = 1.f / wave_sum(lpart);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int i = lane; i < D; i += 64) {
-      float acc = 0.f;
-      for (int j = 0; j < W; ++j) {
-        const int tau = lo + j;
-        const E* vrow = (tau == u) ? vin + ho : vring + static_cast<size_t>(tau % R) * HD + ho;
-        acc += wts[w][j] * ld<E>(vrow + i);
-      }
-      if constexpr (sizeof(E) == 2)
-        out[ho + i] = f2bf(acc * inv);
-      else
-        out[ho + i] = acc * inv;
+    // weighted sum: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
+    const int dc = lane % CH, kg = lane / CH;
+    float acc[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+    for (int j = kg; j < W; j += NKG) {
+      float vf[EPC];
+      unpack16<E>(chunk(vrow(lo + j), dc), vf);
+      const float pw = wts[j];
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[e] += pw * vf[e];
     }
+#pragma unroll
+    for (int o = CH; o < 64; o <<= 1)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[e] += __shfl_xor(acc[e], o);
+    if (kg == 0) *reinterpret_cast<uint4*>(out + ho + dc * EPC) = pack16<E>(acc, inv);
+    // the next head reuses wts: finish these reads first
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   if (threadIdx.x == 0 && a.emitted) a.emitted[s] = emit ? t : -1;
   __syncthreads();  // every wave has read step[s]
@@ -162,19 +209,21 @@ hipError_t launch_stream_step(const StreamStepArgs& a, ElemType et, hipStream_t 
   d.Lb = a.Lb;
   d.La = a.La;
   d.lengths = a.lengths;
+  d.wmax = a.Lb + a.La + 1;
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
   const int nw = a.H < kMaxWaves ? a.H : kMaxWaves;
   const dim3 grid(a.S), block(64 * nw);
+  const size_t lds = static_cast<size_t>(nw) * d.wmax * sizeof(float);
   if (et == kBF16) {
     if (a.d == 64)
-      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 64>), grid, block, 0, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 64>), grid, block, lds, stream, d);
     else
-      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 32>), grid, block, 0, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 32>), grid, block, lds, stream, d);
   } else {
     if (a.d == 64)
-      hipLaunchKernelGGL((stream_step_kernel<float, 64>), grid, block, 0, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<float, 64>), grid, block, lds, stream, d);
     else
-      hipLaunchKernelGGL((stream_step_kernel<float, 32>), grid, block, 0, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<float, 32>), grid, block, lds, stream, d);
   }
   return hipGetLastError();
 }
