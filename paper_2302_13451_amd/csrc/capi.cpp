@@ -39,10 +39,14 @@ int check_shape(const char* fn, int B, int T, int H, int d, int Lb, int La, int 
     return fail(SA_ERR_UNSUPPORTED, "%s: unsupported dtype %d", fn, dtype);
   if (d != 32 && d != 64) return fail(SA_ERR_UNSUPPORTED, "%s: unsupported head dim %d", fn, d);
   if (T > (1 << 30)) return fail(SA_ERR_INVALID, "%s: T = %d exceeds 2^30", fn, T);
-  // every frame index and every (batch, head, tile) index must fit in int
+  // every frame index and every (batch, head, tile) index must fit in int, and
+  // so must element offsets within one sequence
   const long long rows = static_cast<long long>(B) * T * H;
   if (rows > (1LL << 31) - 1)
     return fail(SA_ERR_INVALID, "%s: B*T*H = %lld exceeds 2^31-1", fn, rows);
+  if (static_cast<long long>(T) * H * d > (1LL << 31) - 1)
+    return fail(SA_ERR_INVALID, "%s: T*H*d = %lld exceeds 2^31-1", fn,
+                static_cast<long long>(T) * H * d);
   return SA_OK;
 }
 

@@ -8,6 +8,15 @@ namespace sa {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+// 16 bytes as a native vector: copies of HIP's uint4 (a struct) become
+// aggregate memcpys that the compiler may leave in scratch memory
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ void st8(void* p, u32x2 v) { *reinterpret_cast<u32x2*>(p) = v; }
+constexpr u32x4 kZero16 = {0u, 0u, 0u, 0u};
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -67,6 +76,17 @@ __host__ __device__ __forceinline__ int round_up8(int x) { return (x + 7) & ~7; 
 __device__ __forceinline__ int clamp_len(const int32_t* lengths, int b, int T) {
   if (!lengths) return T;
   int L = lengths[b];
+  L = L < 0 ? 0 : L;
+  return L > T ? T : L;
+}
+
+// Length of sequence b for a uniform b, read through the constant address space
+// (lengths are never written by a kernel), so that it is a scalar load that
+// does not wait on vector memory operations still in flight.
+__device__ __forceinline__ int clamp_len_uniform(const int32_t* lengths, int b, int T) {
+  if (!lengths) return T;
+  typedef __attribute__((address_space(4))) const int32_t cint32;
+  int L = reinterpret_cast<cint32*>(reinterpret_cast<uintptr_t>(lengths))[b];
   L = L < 0 ? 0 : L;
   return L > T ? T : L;
 }
