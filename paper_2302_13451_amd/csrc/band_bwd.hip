@@ -180,28 +180,32 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_valu_kernel(SaBackwardArgs a)
   }
 }
 
-constexpr int kC = 64;  // frames per tile and per LDS chunk
+constexpr int kC = 64;    // frames per tile
+constexpr int kSub = 32;  // frames per sub-block: the contraction length of one MFMA
+// Frames of the swept band staged in LDS at once (two tensors of SEG rows each).
+// With 4 workgroups per CU this keeps every band of the Lb = 64, La = 8 case in
+// one segment; wider bands are swept in several segments.
+template <int D>
+struct Seg {
+  static constexpr int kRows = 144 * 64 / D;
+  static constexpr int kStat = (kRows + kSub - 1) / kSub * kSub;  // rows of D_n and lse
+};
 
 struct BwdDev {
   const uint16_t *q, *k, *v, *o, *dout;
   const float* lse;
   uint16_t *dq, *dk, *dv;
   int B, T, H, Lb, La;
-  int ntiles, nlogical;
+  int ntiles;
   const int32_t* lengths;
   float scale, scale_log2;
 };
 
-__device__ __forceinline__ bf16x8 ld8(const uint16_t* p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
-}
-
-__device__ __forceinline__ float dot8_bf16(const uint4& x, const uint4& y) {
-  const uint32_t a[4] = {x.x, x.y, x.z, x.w}, c[4] = {y.x, y.y, y.z, y.w};
+__device__ __forceinline__ float dot8_bf16(u32x4 x, u32x4 y) {
   float d = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    d += bf2f(a[j] & 0xffffu) * bf2f(c[j] & 0xffffu) + bf2f(a[j] >> 16) * bf2f(c[j] >> 16);
+    d += bf2f(x[j] & 0xffffu) * bf2f(y[j] & 0xffffu) + bf2f(x[j] >> 16) * bf2f(y[j] >> 16);
   return d;
 }
 
@@ -212,47 +216,46 @@ __device__ __forceinline__ void zero_rows(uint16_t* x, uint16_t* y, int b, int h
   for (int e = tid; e < (r_end - r_begin) * V; e += kThreads) {
     const int r = e / V, c = e % V;
     const size_t off = row_index(b, r_begin + r, h, T, H, D) + 8 * c;
-    *reinterpret_cast<uint4*>(x + off) = make_uint4(0, 0, 0, 0);
-    if (y) *reinterpret_cast<uint4*>(y + off) = make_uint4(0, 0, 0, 0);
+    st16(x + off, kZero16);
+    if (y) st16(y + off, kZero16);
   }
 }
 
 template <int D>
-__device__ __forceinline__ void store_rows4(uint16_t* dst, const f32x4* acc, float mul, bool valid,
-                                            int g) {
+__device__ __forceinline__ void store_rows4(uint16_t* dst, int off, const f32x4* acc, float mul,
+                                            bool valid, int g) {
 #pragma unroll
   for (int i = 0; i < D / 16; ++i) {
-    uint2 pk;
-    pk.x = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
-    pk.y = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
-    *reinterpret_cast<uint2*>(dst + 16 * i + 4 * g) = pk;
+    u32x2 pk;
+    pk[0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    pk[1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
+    st8(dst + (off + 16 * i + 4 * g), pk);
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
-  constexpr int RS = D + 8;                  // LDS row stride (elements)
-  constexpr int NS = D / 32, NB = D / 16;
-  constexpr int CPR = D / 8;                 // 16-byte pieces per row
-  constexpr int CPT = kC * CPR / kThreads;   // pieces per thread per tensor per chunk
-  static_assert(CPT * kThreads == kC * CPR, "chunk must split evenly over the threads");
-  __shared__ __attribute__((aligned(16))) uint16_t rm0[kC * RS];  // key role: q   | query role: k
-  __shared__ __attribute__((aligned(16))) uint16_t rm1[kC * RS];  // key role: dout| query role: v
-  __shared__ __attribute__((aligned(16))) float s_dn[kC];
-  __shared__ __attribute__((aligned(16))) float s_lse2[kC];
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void sa_bwd_bf16_kernel(BwdDev a) {
+  constexpr int SEG = Seg<D>::kRows, NST = Seg<D>::kStat;
+  constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
+  constexpr int NDI = (NST * CPR + kThreads - 1) / kThreads;  // D_n pieces per thread
+  __shared__ __attribute__((aligned(16))) uint16_t rm0[SEG * D];  // key role: q    | query role: k
+  __shared__ __attribute__((aligned(16))) uint16_t rm1[SEG * D];  // key role: dout | query role: v
+  __shared__ __attribute__((aligned(16))) float s_dn[NST];
+  __shared__ __attribute__((aligned(16))) float s_lse2[NST];
 
-  int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
-  if (id >= a.nlogical) return;
-  const bool key_role = (id & 1) == 0;
-  id >>= 1;
-  const int tile = id % a.ntiles;
-  id /= a.ntiles;
-  const int h = id % a.H;
-  const int b = id / a.H;
+  // items of a slice: the key and query roles of tile 0, of tile 1, ...; the
+  // second role of a tile finds the tile's rows in the XCD's L2
+  int bh, item;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, 2 * a.ntiles, bh, item)) return;
+  const bool key_role = (item & 1) == 0;
+  const int tile = item >> 1;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
   const int T = a.T, H = a.H, Lb = a.Lb, La = a.La;
-  const int len = clamp_len(a.lengths, b, T);
+  const int len = clamp_len_uniform(a.lengths, b, T);
   const int f0 = tile * kC;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15, g = lane >> 4;
 
   if (f0 >= len) {  // padding tile
@@ -267,36 +270,31 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
   const bool valid = me < len;
   const int fmax = min(f0 + kC, len) - 1;
   const int wmax = min(r0 + 15, len - 1);
-  const size_t my_off = row_index(b, me, h, T, H, D);
+  // Uniform pointers to frame 0 of the (sequence, head) slice; within a slice
+  // every offset fits in int (T * H * d < 2^31 is checked by the caller).
+  const size_t slice = row_index(b, 0, h, T, H, D);
+  const int fs = H * D;  // elements from one frame to the next
+  const uint16_t *q = a.q + slice, *k = a.k + slice, *v = a.v + slice;
+  const uint16_t *o = a.o + slice, *dout = a.dout + slice;
+  const float* lse_bh = a.lse + (static_cast<size_t>(b) * H + h) * T;
+  const int my_off = me * fs;
+  // own-row reads come from a valid frame (lanes past the end read the last one
+  // and discard it), so that the loads need no branch
+  const int rd_off = min(me, len - 1) * fs;
 
   if (key_role) {
     // sweep the queries that see the tile's keys: [f0 - La, fmax + Lb]
-    const int nlo = max(0, f0 - La), nhi = min(len - 1, fmax + Lb);
-    const int nchunks = (nhi - nlo + kC) / kC;
-    uint4 qreg[CPT], dreg[CPT], oreg[CPT];
-    float lreg[CPT];
-    auto fetch = [&](int c) {
-      const int cs = nlo + c * kC, cn = min(kC, nhi - cs + 1);
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
-        qreg[i] = dreg[i] = oreg[i] = make_uint4(0, 0, 0, 0);
-        lreg[i] = 0.f;
-        if (r < cn) {
-          const size_t off = row_index(b, cs + r, h, T, H, D) + 8 * pc;
-          qreg[i] = *reinterpret_cast<const uint4*>(a.q + off);
-          dreg[i] = *reinterpret_cast<const uint4*>(a.dout + off);
-          oreg[i] = *reinterpret_cast<const uint4*>(a.o + off);
-          if (pc == 0) lreg[i] = a.lse[(static_cast<size_t>(b) * H + h) * T + cs + r];
-        }
-      }
-    };
-    fetch(0);
+    const int lo = max(0, f0 - La), hi = min(len - 1, fmax + Lb);
+    int s0 = lo, nv = min(SEG, hi - lo + 1);
+    seg_issue<D>(rm0, q + s0 * fs, fs, nv, w, lane);
+    seg_issue<D>(rm1, dout + s0 * fs, fs, nv, w, lane);
+    // own key and value rows, the N operand of every product (lanes past the
+    // end of the sequence hold the last frame's and are masked out)
     bf16x8 kf[NS], vf[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kf[s] = valid ? ld8(a.k + my_off + 32 * s + 8 * g) : bf16x8{};
-      vf[s] = valid ? ld8(a.v + my_off + 32 * s + 8 * g) : bf16x8{};
+      kf[s] = __builtin_bit_cast(bf16x8, ld16(k + (rd_off + 32 * s + 8 * g)));
+      vf[s] = __builtin_bit_cast(bf16x8, ld16(v + (rd_off + 32 * s + 8 * g)));
     }
     f32x4 adv[NB], adk[NB];
 #pragma unroll
@@ -304,142 +302,159 @@ __global__ __launch_bounds__(kThreads) void sa_bwd_bf16_kernel(BwdDev a) {
     const int wlo = max(0, r0 - La);
     const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
     const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
-    for (int c = 0; c < nchunks; ++c) {
-      const int cs = nlo + c * kC, cn = min(kC, nhi - cs + 1);
+    // lanes past the end of the sequence see no query
+    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+    const int mylo_v = valid ? mylo : 1 << 30;
+    const SubBlockOffsets<D> so(lane);
+    for (;;) {
+      // out rows and lse of the segment's queries, for D_n = dout_n . out_n;
+      // unconditional loads from a clamped row, so that no lane overwrites a
+      // register with a load still in flight
+      u32x4 ov[NDI];
+      float lv[NDI];
+#pragma unroll
+      for (int i = 0; i < NDI; ++i) {
+        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR, rc = min(r, nv - 1);
+        ov[i] = ld16(o + ((s0 + rc) * fs + 8 * pc));
+        lv[i] = lse_bh[s0 + rc];
+      }
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
 #pragma unroll
-      for (int i = 0; i < CPT; ++i) {
+      for (int i = 0; i < NDI; ++i) {
         const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
-        *reinterpret_cast<uint4*>(rm0 + r * RS + 8 * pc) = qreg[i];
-        *reinterpret_cast<uint4*>(rm1 + r * RS + 8 * pc) = dreg[i];
-        float dn = dot8_bf16(dreg[i], oreg[i]);
+        float dn = r < nv ? dot8_bf16(ld16(rm1 + seg_off<D>(r, 8 * pc)), ov[i]) : 0.f;
+        const float l2 = r < nv ? lv[i] * kLog2e : 0.f;
 #pragma unroll
         for (int m = 1; m < CPR; m <<= 1) dn += __shfl_xor(dn, m);  // the row's pieces are adjacent lanes
-        if (pc == 0) {
+        if (pc == 0 && r < NST) {
           s_dn[r] = dn;
-          s_lse2[r] = lreg[i] * kLog2e;
+          s_lse2[r] = l2;
         }
       }
-      if (c + 1 < nchunks) fetch(c + 1);
       __syncthreads();
-      if (wlo > whi) continue;
-      for (int sb = 0; sb < kC; sb += 32) {
-        const int qb = cs + sb;
-        if (sb >= cn || qb > whi || qb + 31 < wlo) continue;
-        const int qr = sb + 8 * (col >> 2) + (col & 3);
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
+      const int rl = nv - 1;
+      for (int sb = 0; sb < nv && wlo <= whi; sb += kSub) {
+        const int qb = s0 + sb;
+        if (qb > whi || qb + kSub - 1 < wlo) continue;
+        int oa, oc, ota, otc;
+        so.at(sb, rl, oa, oc, ota, otc);
+        f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + qr * RS + 32 * s + 8 * g), kf[s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (qr + 4) * RS + 32 * s + 8 * g), kf[s], s1, 0, 0, 0);
-          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + qr * RS + 32 * s + 8 * g), vf[s], p0, 0, 0, 0);
-          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (qr + 4) * RS + 32 * s + 8 * g), vf[s], p1, 0, 0, 0);
+          sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
+          sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (oc ^ (32 * s))), kf[s], sc1, 0, 0, 0);
+          dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
+          dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
         }
+        // statistics of the 8 queries this lane holds: rows sb + 8g .. +7
+        const f32x4 l0 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g);
+        const f32x4 l1 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g + 4);
+        const f32x4 n0 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g);
+        const f32x4 n1 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g + 4);
+        const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
         bf16x8 pf, dsf;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const int lr = sb + 8 * g + j;  // local row of query qb + 8g + j
-          const int nq = cs + lr;
-          const float sv = j < 4 ? s0[j] : s1[j - 4];
-          const float dp = j < 4 ? p0[j] : p1[j - 4];
-          const bool ok = valid && nq >= mylo && nq <= myhi;
-          const float pw = ok ? fast_exp2(sv * a.scale_log2 - s_lse2[lr]) : 0.f;
-          pf[j] = static_cast<__bf16>(pw);
-          dsf[j] = static_cast<__bf16>(pw * (dp - s_dn[lr]));
+          const float sv = j < 4 ? sc0[j] : sc1[j - 4];
+          const float dp = j < 4 ? dp0[j] : dp1[j - 4];
+          const float l2 = j < 4 ? l0[j] : l1[j - 4];
+          const float dnq = j < 4 ? n0[j] : n1[j - 4];
+          const bool ok = static_cast<unsigned>(d0 + j) <= span;
+          const float pw = fast_exp2(sv * a.scale_log2 - l2);
+          pf[j] = static_cast<__bf16>(ok ? pw : 0.f);
+          dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dnq) : 0.f);
         }
         // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-          adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm1, sb, 16 * i, lane), pf, adv[i], 0, 0, 0);
-          adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm0, sb, 16 * i, lane), dsf, adk[i], 0, 0, 0);
+          adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(rm1, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
+          adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(rm0, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
         }
       }
+      s0 += SEG;
+      if (s0 > hi) break;
+      nv = min(SEG, hi - s0 + 1);
+      __syncthreads();  // every wave is done with this segment
+      seg_issue<D>(rm0, q + s0 * fs, fs, nv, w, lane);
+      seg_issue<D>(rm1, dout + s0 * fs, fs, nv, w, lane);
     }
     if (me < T) {
-      store_rows4<D>(a.dv + my_off, adv, 1.f, valid, g);
-      store_rows4<D>(a.dk + my_off, adk, a.scale, valid, g);
+      store_rows4<D>(a.dv + slice, my_off, adv, 1.f, valid, g);
+      store_rows4<D>(a.dk + slice, my_off, adk, a.scale, valid, g);
     }
   } else {
     // sweep the keys of the tile's queries: [f0 - Lb, fmax + La]
-    const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La);
-    const int nchunks = (khi - klo + kC) / kC;
-    uint4 kreg[CPT], vreg[CPT];
-    auto fetch = [&](int c) {
-      const int cs = klo + c * kC, cn = min(kC, khi - cs + 1);
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
-        kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
-        if (r < cn) {
-          const size_t off = row_index(b, cs + r, h, T, H, D) + 8 * pc;
-          kreg[i] = *reinterpret_cast<const uint4*>(a.k + off);
-          vreg[i] = *reinterpret_cast<const uint4*>(a.v + off);
-        }
-      }
-    };
-    fetch(0);
+    const int lo = max(0, f0 - Lb), hi = min(len - 1, fmax + La);
+    int s0 = lo, nv = min(SEG, hi - lo + 1);
+    seg_issue<D>(rm0, k + s0 * fs, fs, nv, w, lane);
+    seg_issue<D>(rm1, v + s0 * fs, fs, nv, w, lane);
+    // own query and output-gradient rows, the N operand of every product, and
+    // D = dout . out of the own query (lanes past the end of the sequence hold
+    // the last frame's and are masked out)
     bf16x8 qf[NS], df[NS];
     float dn = 0.f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const size_t off = my_off + 32 * s + 8 * g;
-      const uint4 qr = valid ? *reinterpret_cast<const uint4*>(a.q + off) : make_uint4(0, 0, 0, 0);
-      const uint4 dr = valid ? *reinterpret_cast<const uint4*>(a.dout + off) : make_uint4(0, 0, 0, 0);
-      const uint4 orw = valid ? *reinterpret_cast<const uint4*>(a.o + off) : make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8, qr);
+      const int off = rd_off + 32 * s + 8 * g;
+      const u32x4 dr = ld16(dout + off);
+      qf[s] = __builtin_bit_cast(bf16x8, ld16(q + off));
       df[s] = __builtin_bit_cast(bf16x8, dr);
-      dn += dot8_bf16(dr, orw);
+      dn += dot8_bf16(dr, ld16(o + off));
     }
     dn += __shfl_xor(dn, 16);
     dn += __shfl_xor(dn, 32);
-    const float lse2 = valid ? a.lse[(static_cast<size_t>(b) * H + h) * T + me] * kLog2e : 0.f;
+    const float lse2 = lse_bh[min(me, len - 1)] * kLog2e;
     f32x4 aq[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int wlo = max(0, r0 - Lb);
     const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
     const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
-    for (int c = 0; c < nchunks; ++c) {
-      const int cs = klo + c * kC, cn = min(kC, khi - cs + 1);
+    // lanes past the end of the sequence have an empty window
+    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+    const int mylo_v = valid ? mylo : 1 << 30;
+    const SubBlockOffsets<D> so(lane);
+    for (;;) {
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const int e = tid + i * kThreads, r = e / CPR, pc = e % CPR;
-        *reinterpret_cast<uint4*>(rm0 + r * RS + 8 * pc) = kreg[i];
-        *reinterpret_cast<uint4*>(rm1 + r * RS + 8 * pc) = vreg[i];
-      }
-      if (c + 1 < nchunks) fetch(c + 1);
-      __syncthreads();
-      if (wlo > whi) continue;
-      for (int sb = 0; sb < kC; sb += 32) {
-        const int kb = cs + sb;
-        if (sb >= cn || kb > whi || kb + 31 < wlo) continue;
-        const int kr = sb + 8 * (col >> 2) + (col & 3);
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0, p0 = s0, p1 = s0;
+      const int rl = nv - 1;
+      for (int sb = 0; sb < nv && wlo <= whi; sb += kSub) {
+        const int kb = s0 + sb;
+        if (kb > whi || kb + kSub - 1 < wlo) continue;
+        int oa, oc, ota, otc;
+        so.at(sb, rl, oa, oc, ota, otc);
+        f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + kr * RS + 32 * s + 8 * g), qf[s], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (kr + 4) * RS + 32 * s + 8 * g), qf[s], s1, 0, 0, 0);
-          p0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + kr * RS + 32 * s + 8 * g), df[s], p0, 0, 0, 0);
-          p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (kr + 4) * RS + 32 * s + 8 * g), df[s], p1, 0, 0, 0);
+          sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
+          sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm0 + (oc ^ (32 * s))), qf[s], sc1, 0, 0, 0);
+          dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
+          dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(rm1 + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
         }
+        const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
         bf16x8 dsf;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const int key = kb + 8 * g + j;
-          const float sv = j < 4 ? s0[j] : s1[j - 4];
-          const float dp = j < 4 ? p0[j] : p1[j - 4];
-          const bool ok = valid && key >= mylo && key <= myhi;
-          const float pw = ok ? fast_exp2(sv * a.scale_log2 - lse2) : 0.f;
-          dsf[j] = static_cast<__bf16>(pw * (dp - dn));
+          const float sv = j < 4 ? sc0[j] : sc1[j - 4];
+          const float dp = j < 4 ? dp0[j] : dp1[j - 4];
+          const bool ok = static_cast<unsigned>(d0 + j) <= span;
+          const float pw = fast_exp2(sv * a.scale_log2 - lse2);
+          dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dn) : 0.f);
         }
         // dq^T += k^T dS^T, contracting over the 32 keys
 #pragma unroll
         for (int i = 0; i < NB; ++i)
-          aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_col8<RS>(rm0, sb, 16 * i, lane), dsf, aq[i], 0, 0, 0);
+          aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(rm0, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
       }
+      s0 += SEG;
+      if (s0 > hi) break;
+      nv = min(SEG, hi - s0 + 1);
+      __syncthreads();  // every wave is done with this segment
+      seg_issue<D>(rm0, k + s0 * fs, fs, nv, w, lane);
+      seg_issue<D>(rm1, v + s0 * fs, fs, nv, w, lane);
     }
-    if (me < T) store_rows4<D>(a.dq + my_off, aq, a.scale, valid, g);
+    if (me < T) store_rows4<D>(a.dq + slice, my_off, aq, a.scale, valid, g);
   }
 }
 
@@ -463,8 +478,7 @@ hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   d.scale = 1.f / sqrtf(static_cast<float>(a.d));
   d.scale_log2 = kLog2e * d.scale;
   d.ntiles = (a.T + kC - 1) / kC;
-  d.nlogical = 2 * a.B * a.H * d.ntiles;
-  const int grid = round_up8(d.nlogical);
+  const int grid = xcd_slice_grid(a.B * a.H, 2 * d.ntiles);
   if (a.d == 64)
     hipLaunchKernelGGL(sa_bwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
   else

@@ -52,7 +52,6 @@ struct DevArgs {
   int B, T, H;
   int njobs;      // outputs per launch (1: SA, 2: LLSA)
   int ntiles;     // query tiles per (sequence, head)
-  int nlogical;   // workgroups doing work
   const int32_t* lengths;
   float scale_log2;  // log2(e) / sqrt(d)
 };
@@ -83,16 +82,14 @@ __global__ __launch_bounds__(kThreads) void band_fwd_bf16_kernel(DevArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKC * RS];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kKC * RS];
 
-  int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
-  if (id >= a.nlogical) return;
-  // the outputs of a tile are adjacent ids: they read the same K/V band, which
-  // the second one then finds in the XCD's L2
-  const bool second = a.njobs > 1 && (id & 1);
-  id = a.njobs > 1 ? id >> 1 : id;
-  const int tile = id % a.ntiles;
-  id /= a.ntiles;
-  const int h = id % a.H;
-  const int b = id / a.H;
+  // items of a slice: the outputs of tile 0, of tile 1, ...; the outputs of a
+  // tile read the same K/V band, which the second one finds in the XCD's L2
+  int bh, item;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.njobs * a.ntiles, bh, item)) return;
+  const bool second = a.njobs > 1 && (item & 1);
+  const int tile = a.njobs > 1 ? item >> 1 : item;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
   const DevJob& job = second ? a.job1 : a.job0;
 
   const int T = a.T, H = a.H;
@@ -363,15 +360,13 @@ hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
   if (et == kBF16) {
     d.ntiles = (a.T + kTq - 1) / kTq;
-    d.nlogical = a.njobs * a.B * a.H * d.ntiles;
-    const int grid = round_up8(d.nlogical);
+    const int grid = xcd_slice_grid(a.B * a.H, a.njobs * d.ntiles);
     if (a.d == 64)
       hipLaunchKernelGGL(band_fwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
     else
       hipLaunchKernelGGL(band_fwd_bf16_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d);
   } else {
     d.ntiles = 0;
-    d.nlogical = 0;
     const size_t total = static_cast<size_t>(a.njobs) * a.B * a.T * a.H;
     const size_t blocks = (total + kThreads - 1) / kThreads;
     const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);

@@ -62,13 +62,147 @@ __device__ __forceinline__ bf16x8 lds_row8(const uint16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
 }
 
+// Band segments staged in LDS by direct global->LDS copies. One copy
+// instruction moves 16 bytes per lane and fills 1 KiB of LDS contiguously
+// (lane L at byte 16 L), so a segment is row-major with unpadded D-element
+// rows. The 16-byte pieces of row r are permuted by XOR with seg_swizzle(r) so
+// that both read patterns of the MFMA operands stay free of bank conflicts:
+// eight lanes reading one piece from rows {0..3, 8..11} (+4, +16) of a 32-row
+// block, and sixteen lanes reading 32 bytes from each of four consecutive rows
+// (the transposing read).
+template <int D>
+__device__ __forceinline__ int seg_swizzle(int r);
+template <>
+__device__ __forceinline__ int seg_swizzle<64>(int r) {
+  return (((r >> 3) ^ (r >> 4)) & 1) | (((r ^ (r >> 3)) & 1) << 1) | ((r & 2) << 1);
+}
+template <>
+__device__ __forceinline__ int seg_swizzle<32>(int r) {
+  return ((r >> 1) & 1) | ((r >> 2) & 2);
+}
+
+// Element offset of (row r, column c) in a swizzled segment.
+template <int D>
+__device__ __forceinline__ int seg_off(int r, int c) {
+  return r * D + ((((c >> 3) ^ seg_swizzle<D>(r)) << 3) | (c & 7));
+}
+
+// Issue the direct copies that fill rows [0, nrows) of segment X from
+// src[r * rstride + 0 .. D-1] (src is uniform: the (sequence, head) slice at
+// the segment's first frame). Wave w (uniform) issues copies w, w + 4, ...;
+// copy I fills LDS bytes [1024 I, 1024 I + 1024). Rows at and beyond nrows are
+// left untouched. The caller waits (vmcnt) and barriers before reading X.
+template <int D>
+__device__ __forceinline__ void seg_issue(uint16_t* X, const uint16_t* src, int rstride, int nrows,
+                                          int w, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR;
+  const int rl = lane / CPR, pp = lane % CPR;
+  for (int I = w; I * RPI < nrows; I += 4) {
+    const int r = I * RPI + rl;
+    if (r < nrows) {
+      const int p = pp ^ seg_swizzle<D>(r);
+      __builtin_amdgcn_global_load_lds(src + (r * rstride + 8 * p), X + I * 512, 16, 0, 0);
+    }
+  }
+}
+
+// Row read from a swizzled segment: 8 consecutive elements of row r starting at
+// column c (c a multiple of 8).
+template <int D>
+__device__ __forceinline__ bf16x8 seg_row8(const uint16_t* X, int r, int c) {
+  return *reinterpret_cast<const bf16x8*>(X + seg_off<D>(r, c));
+}
+
+// Transposed MFMA operand from a swizzled segment (the lds_col8 pattern): lane
+// (g, c) receives X[min(r0 + 8g + j, rlast)][c0 + c] for j = 0..7. Rows past
+// rlast are replaced by row rlast, so no read leaves the filled rows; the
+// caller multiplies them by zero weights.
+template <int D>
+__device__ __forceinline__ bf16x8 seg_col8(const uint16_t* X, int r0, int c0, int lane, int rlast) {
+  const int g = lane >> 4, L = lane & 15;
+  const int ra = r0 + 8 * g + (L >> 2);
+  const int rlo = ra < rlast ? ra : rlast, rhi = ra + 4 < rlast ? ra + 4 : rlast;
+  const int c = c0 + 4 * (L & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(X + seg_off<D>(rlo, c)));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(X + seg_off<D>(rhi, c)));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Element offsets of the two MFMA operand reads from a swizzled segment.
+// Row read: the 16-byte piece g of row r (the piece 4s + g is this offset XOR
+// 32 s). Transposing read of row r by lane L of a 16-lane group: columns
+// 4 (L % 4) .. +3 of the first 16 (the block of columns 16 i is this offset
+// XOR 16 i).
+template <int D>
+__device__ __forceinline__ int seg_row_off(int r, int g) {
+  return r * D + ((g ^ seg_swizzle<D>(r)) << 3);
+}
+template <int D>
+__device__ __forceinline__ int seg_tr_off(int r, int L) {
+  return r * D + (((((L >> 1) & 1) ^ seg_swizzle<D>(r)) << 3) | ((L & 1) << 2));
+}
+
+__device__ __forceinline__ bf16x8 lds_tr8(const uint16_t* X, int off_lo, int off_hi) {
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(X + off_lo));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(X + off_hi));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Per-lane offsets of every MFMA operand read of the 32-row sub-block that
+// starts at segment row sb (a multiple of 32). The swizzle only depends on the
+// low five bits of the row, so away from the segment's end the offsets are the
+// first sub-block's plus sb * D; in the last, partial sub-block rows past rlast
+// read row rlast instead (their weights are zero).
+template <int D>
+struct SubBlockOffsets {
+  int xa, xt;              // the lane's rows inside a sub-block: row read, transposing read
+  int ra, rc, ta, tc;      // offsets in sub-block 0: rows xa, xa + 4, xt, xt + 4
+  int g, L;
+  __device__ __forceinline__ SubBlockOffsets(int lane) {
+    const int col = lane & 15;
+    g = lane >> 4;
+    L = col;
+    xa = 8 * (col >> 2) + (col & 3);
+    xt = 8 * g + (col >> 2);
+    ra = seg_row_off<D>(xa, g);
+    rc = seg_row_off<D>(xa + 4, g);
+    ta = seg_tr_off<D>(xt, L);
+    tc = seg_tr_off<D>(xt + 4, L);
+  }
+  // offsets for the sub-block at sb: {row xa, row xa + 4, tr row xt, tr row xt + 4}
+  __device__ __forceinline__ void at(int sb, int rlast, int& oa, int& oc, int& ota, int& otc) const {
+    if (sb + 31 <= rlast) {
+      const int d = sb * D;
+      oa = ra + d; oc = rc + d; ota = ta + d; otc = tc + d;
+    } else {
+      const int r1 = sb + xa, r2 = sb + xt;
+      oa = seg_row_off<D>(r1 < rlast ? r1 : rlast, g);
+      oc = seg_row_off<D>(r1 + 4 < rlast ? r1 + 4 : rlast, g);
+      ota = seg_tr_off<D>(r2 < rlast ? r2 : rlast, L);
+      otc = seg_tr_off<D>(r2 + 4 < rlast ? r2 + 4 : rlast, L);
+    }
+  }
+};
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
-// L2). Remap so that every XCD walks one contiguous range of logical tiles:
-// neighbouring tiles of a sequence, which share their band halo, then run on
-// the same XCD close together in time. `nblocks` must be a multiple of 8.
-__device__ __forceinline__ int xcd_contiguous_id(int bid, int nblocks) {
-  const int per = nblocks >> 3;
-  return (bid & 7) * per + (bid >> 3);
+// L2): block bid runs on XCD bid % 8. XCD x walks the (sequence, head) slices
+// x, x + 8, x + 16, ... and, within a slice, its per_slice work items in
+// order. Neighbouring tiles of a slice, which share their band halo, so run on
+// one XCD close together in time, and the heads of every sequence (sequences
+// differ in length) are spread over all XCDs, which balances their work. The
+// grid is xcd_slice_grid(nslices, per_slice) blocks; blocks past the last
+// slice get false.
+__device__ __forceinline__ bool xcd_slice_item(int bid, int nslices, int per_slice, int& slice,
+                                               int& item) {
+  const int j = bid >> 3;
+  const int k = j / per_slice;
+  item = j - k * per_slice;
+  slice = (bid & 7) + 8 * k;
+  return slice < nslices;
+}
+
+inline int xcd_slice_grid(int nslices, int per_slice) {
+  return (nslices + 7) / 8 * 8 * per_slice;
 }
 
 __host__ __device__ __forceinline__ int round_up8(int x) { return (x + 7) & ~7; }
