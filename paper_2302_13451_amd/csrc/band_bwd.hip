@@ -189,6 +189,9 @@ template <int D>
 struct Seg {
   static constexpr int kRows = 144 * 64 / D;
   static constexpr int kStat = (kRows + kSub - 1) / kSub * kSub;  // rows of D_n and lse
+  // A sweep that does not fit one segment advances by whole sub-blocks; the
+  // rows a segment holds past kStep are processed again by the next one.
+  static constexpr int kStep = kRows / kSub * kSub;
 };
 
 struct BwdDev {
@@ -209,11 +212,11 @@ __device__ __forceinline__ float dot8_bf16(u32x4 x, u32x4 y) {
   return d;
 }
 
-template <int D>
+template <int D, int NT = kThreads>
 __device__ __forceinline__ void zero_rows(uint16_t* x, uint16_t* y, int b, int h, int T, int H,
                                           int r_begin, int r_end, int tid) {
   constexpr int V = D / 8;
-  for (int e = tid; e < (r_end - r_begin) * V; e += kThreads) {
+  for (int e = tid; e < (r_end - r_begin) * V; e += NT) {
     const int r = e / V, c = e % V;
     const size_t off = row_index(b, r_begin + r, h, T, H, D) + 8 * c;
     st16(x + off, kZero16);
@@ -235,7 +238,7 @@ __device__ __forceinline__ void store_rows4(uint16_t* dst, int off, const f32x4*
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void sa_bwd_bf16_kernel(BwdDev a) {
-  constexpr int SEG = Seg<D>::kRows, NST = Seg<D>::kStat;
+  constexpr int SEG = Seg<D>::kRows, NST = Seg<D>::kStat, STEP = Seg<D>::kStep;
   constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
   constexpr int NDI = (NST * CPR + kThreads - 1) / kThreads;  // D_n pieces per thread
   __shared__ __attribute__((aligned(16))) uint16_t rm0[SEG * D];  // key role: q    | query role: k
@@ -307,6 +310,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const int mylo_v = valid ? mylo : 1 << 30;
     const SubBlockOffsets<D> so(lane);
     for (;;) {
+      const bool last = hi - s0 + 1 <= SEG;  // nv rows, all of them swept here
+      const int nsw = last ? nv : STEP;      // rows whose sub-blocks are swept here
       // out rows and lse of the segment's queries, for D_n = dout_n . out_n;
       // unconditional loads from a clamped row, so that no lane overwrites a
       // register with a load still in flight
@@ -334,7 +339,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
       }
       __syncthreads();
       const int rl = nv - 1;
-      for (int sb = 0; sb < nv && wlo <= whi; sb += kSub) {
+      for (int sb = 0; sb < nsw && wlo <= whi; sb += kSub) {
         const int qb = s0 + sb;
         if (qb > whi || qb + kSub - 1 < wlo) continue;
         int oa, oc, ota, otc;
@@ -372,8 +377,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
           adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(rm0, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
         }
       }
-      s0 += SEG;
-      if (s0 > hi) break;
+      if (last) break;
+      s0 += STEP;
       nv = min(SEG, hi - s0 + 1);
       __syncthreads();  // every wave is done with this segment
       seg_issue<D>(rm0, q + s0 * fs, fs, nv, w, lane);
@@ -416,10 +421,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const int mylo_v = valid ? mylo : 1 << 30;
     const SubBlockOffsets<D> so(lane);
     for (;;) {
+      const bool last = hi - s0 + 1 <= SEG;  // nv rows, all of them swept here
+      const int nsw = last ? nv : STEP;      // rows whose sub-blocks are swept here
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       const int rl = nv - 1;
-      for (int sb = 0; sb < nv && wlo <= whi; sb += kSub) {
+      for (int sb = 0; sb < nsw && wlo <= whi; sb += kSub) {
         const int kb = s0 + sb;
         if (kb > whi || kb + kSub - 1 < wlo) continue;
         int oa, oc, ota, otc;
@@ -447,8 +454,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         for (int i = 0; i < NB; ++i)
           aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(rm0, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
       }
-      s0 += SEG;
-      if (s0 > hi) break;
+      if (last) break;
+      s0 += STEP;
       nv = min(SEG, hi - s0 + 1);
       __syncthreads();  // every wave is done with this segment
       seg_issue<D>(rm0, k + s0 * fs, fs, nv, w, lane);
@@ -457,6 +464,198 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     if (me < T) store_rows4<D>(a.dq + slice, my_off, aq, a.scale, valid, g);
   }
 }
+
+// Both roles of one 64-frame tile in one workgroup of 8 waves, for windows
+// whose sweeps fit one LDS segment (64 + Lb + La <= Seg<D>::kRows): waves 0-3
+// take the key role and waves 4-7 the query role. The query band
+// [f0 - La, fmax + Lb] of q and dout and the key band [f0 - Lb, fmax + La] of
+// k and v are staged once; each role finds its own rows inside the other
+// role's band, and D_n and lse of the query band are computed once for both.
+template <int D>
+__global__ __launch_bounds__(2 * kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void sa_bwd_tile_kernel(BwdDev a) {
+  constexpr int NT = 2 * kThreads;
+  constexpr int SEG = Seg<D>::kRows, NST = Seg<D>::kStat;
+  constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
+  constexpr int NDI = (NST * CPR + NT - 1) / NT;  // out pieces per thread for D_n
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[SEG * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_do[SEG * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[SEG * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[SEG * D];
+  __shared__ __attribute__((aligned(16))) float s_dn[NST];
+  __shared__ __attribute__((aligned(16))) float s_lse2[NST];
+
+  int bh, tile;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int T = a.T, H = a.H, Lb = a.Lb, La = a.La;
+  const int len = clamp_len_uniform(a.lengths, b, T);
+  const int f0 = tile * kC;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, g = lane >> 4;
+
+  if (f0 >= len) {  // padding tile
+    zero_rows<D, NT>(a.dk, a.dv, b, h, T, H, f0, min(f0 + kC, T), tid);
+    zero_rows<D, NT>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
+    return;
+  }
+  const int fmax = min(f0 + kC, len) - 1;
+  const int qlo = max(0, f0 - La), qhi = min(len - 1, fmax + Lb), nq = qhi - qlo + 1;
+  const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La), nk = khi - klo + 1;
+  const size_t slice = row_index(b, 0, h, T, H, D);
+  const int fs = H * D;  // elements from one frame to the next
+  const uint16_t *q = a.q + slice, *k = a.k + slice, *v = a.v + slice;
+  const uint16_t *o = a.o + slice, *dout = a.dout + slice;
+  const float* lse_bh = a.lse + (static_cast<size_t>(b) * H + h) * T;
+
+  seg_issue<D, 8>(s_q, q + qlo * fs, fs, nq, w, lane);
+  seg_issue<D, 8>(s_do, dout + qlo * fs, fs, nq, w, lane);
+  seg_issue<D, 8>(s_k, k + klo * fs, fs, nk, w, lane);
+  seg_issue<D, 8>(s_v, v + klo * fs, fs, nk, w, lane);
+  // out rows and lse of the query band, for D_n = dout_n . out_n; a wave skips
+  // the pieces past the band as a whole, and loads the rest unconditionally
+  // (rows clamped), so that no lane overwrites a register with a load in flight
+  u32x4 ov[NDI];
+#pragma unroll
+  for (int i = 0; i < NDI; ++i) {
+    ov[i] = kZero16;
+    if ((i * NT + w * 64) / CPR < nq) {
+      const int e = tid + i * NT, r = e / CPR, pc = e % CPR;
+      ov[i] = ld16(o + ((qlo + min(r, nq - 1)) * fs + 8 * pc));
+    }
+  }
+  float lsev = 0.f;
+  if (w * 64 < NST) lsev = lse_bh[qlo + min(tid, nq - 1)];
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NDI; ++i) {
+    if ((i * NT + w * 64) / CPR < NST) {
+      const int e = tid + i * NT, r = e / CPR, pc = e % CPR;
+      float dn = r < nq ? dot8_bf16(ld16(s_do + seg_off<D>(r, 8 * pc)), ov[i]) : 0.f;
+#pragma unroll
+      for (int m = 1; m < CPR; m <<= 1) dn += __shfl_xor(dn, m);  // the row's pieces are adjacent lanes
+      if (pc == 0 && r < NST) s_dn[r] = dn;
+    }
+  }
+  if (tid < NST) s_lse2[tid] = tid < nq ? lsev * kLog2e : 0.f;
+  __syncthreads();
+
+  const int r0 = f0 + 16 * (w & 3);
+  const int me = r0 + col;  // this lane's key (waves 0-3) or query (waves 4-7)
+  const bool valid = me < len;
+  const int mec = min(me, len - 1);  // lanes past the end read the last frame's rows, masked out
+  const int wmax = min(r0 + 15, len - 1);
+  const int my_off = me * fs;
+  const SubBlockOffsets<D> so(lane);
+  if (w < 4) {
+    // key role: keys r0 .. r0 + 15 against the query band
+    bf16x8 kf[NS], vf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      kf[s] = seg_row8<D>(s_k, mec - klo, 32 * s + 8 * g);
+      vf[s] = seg_row8<D>(s_v, mec - klo, 32 * s + 8 * g);
+    }
+    f32x4 adv[NB], adk[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int wlo = max(0, r0 - La);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
+    const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
+    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+    const int mylo_v = valid ? mylo : 1 << 30;
+    const int rl = nq - 1;
+    for (int sb = 0; sb < nq && wlo <= whi; sb += kSub) {
+      const int qb = qlo + sb;
+      if (qb > whi || qb + kSub - 1 < wlo) continue;
+      int oa, oc, ota, otc;
+      so.at(sb, rl, oa, oc, ota, otc);
+      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_q + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
+        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_q + (oc ^ (32 * s))), kf[s], sc1, 0, 0, 0);
+        dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
+        dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
+      }
+      const f32x4 l0 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g);
+      const f32x4 l1 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g + 4);
+      const f32x4 n0 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g);
+      const f32x4 n1 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g + 4);
+      const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
+      bf16x8 pf, dsf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float sv = j < 4 ? sc0[j] : sc1[j - 4];
+        const float dp = j < 4 ? dp0[j] : dp1[j - 4];
+        const float l2 = j < 4 ? l0[j] : l1[j - 4];
+        const float dnq = j < 4 ? n0[j] : n1[j - 4];
+        const bool ok = static_cast<unsigned>(d0 + j) <= span;
+        const float pw = fast_exp2(sv * a.scale_log2 - l2);
+        pf[j] = static_cast<__bf16>(ok ? pw : 0.f);
+        dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dnq) : 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_do, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
+        adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_q, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
+      }
+    }
+    if (me < T) {
+      store_rows4<D>(a.dv + slice, my_off, adv, 1.f, valid, g);
+      store_rows4<D>(a.dk + slice, my_off, adk, a.scale, valid, g);
+    }
+  } else {
+    // query role: queries r0 .. r0 + 15 against the key band
+    bf16x8 qf[NS], df[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      qf[s] = seg_row8<D>(s_q, mec - qlo, 32 * s + 8 * g);
+      df[s] = seg_row8<D>(s_do, mec - qlo, 32 * s + 8 * g);
+    }
+    const float dn = s_dn[mec - qlo], lse2 = s_lse2[mec - qlo];
+    f32x4 aq[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int wlo = max(0, r0 - Lb);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
+    const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
+    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+    const int mylo_v = valid ? mylo : 1 << 30;
+    const int rl = nk - 1;
+    for (int sb = 0; sb < nk && wlo <= whi; sb += kSub) {
+      const int kb = klo + sb;
+      if (kb > whi || kb + kSub - 1 < wlo) continue;
+      int oa, oc, ota, otc;
+      so.at(sb, rl, oa, oc, ota, otc);
+      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_k + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
+        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_k + (oc ^ (32 * s))), qf[s], sc1, 0, 0, 0);
+        dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
+        dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
+      }
+      const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
+      bf16x8 dsf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float sv = j < 4 ? sc0[j] : sc1[j - 4];
+        const float dp = j < 4 ? dp0[j] : dp1[j - 4];
+        const bool ok = static_cast<unsigned>(d0 + j) <= span;
+        const float pw = fast_exp2(sv * a.scale_log2 - lse2);
+        dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dn) : 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_k, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
+    }
+    if (me < T) store_rows4<D>(a.dq + slice, my_off, aq, a.scale, valid, g);
+  }
+}
+
 
 hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   BwdDev d;
@@ -478,11 +677,21 @@ hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   d.scale = 1.f / sqrtf(static_cast<float>(a.d));
   d.scale_log2 = kLog2e * d.scale;
   d.ntiles = (a.T + kC - 1) / kC;
-  const int grid = xcd_slice_grid(a.B * a.H, 2 * d.ntiles);
-  if (a.d == 64)
-    hipLaunchKernelGGL(sa_bwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
-  else
-    hipLaunchKernelGGL(sa_bwd_bf16_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d);
+  const int seg_rows = a.d == 64 ? Seg<64>::kRows : Seg<32>::kRows;
+  if (kC + a.Lb + a.La <= seg_rows) {
+    // both sweeps fit one segment: one workgroup per tile
+    const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
+    if (a.d == 64)
+      hipLaunchKernelGGL(sa_bwd_tile_kernel<64>, dim3(grid), dim3(2 * kThreads), 0, stream, d);
+    else
+      hipLaunchKernelGGL(sa_bwd_tile_kernel<32>, dim3(grid), dim3(2 * kThreads), 0, stream, d);
+  } else {
+    const int grid = xcd_slice_grid(a.B * a.H, 2 * d.ntiles);
+    if (a.d == 64)
+      hipLaunchKernelGGL(sa_bwd_bf16_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, d);
+    else
+      hipLaunchKernelGGL(sa_bwd_bf16_kernel<32>, dim3(grid), dim3(kThreads), 0, stream, d);
+  }
   return hipGetLastError();
 }
 

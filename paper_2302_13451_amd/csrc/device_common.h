@@ -89,15 +89,15 @@ __device__ __forceinline__ int seg_off(int r, int c) {
 
 // Issue the direct copies that fill rows [0, nrows) of segment X from
 // src[r * rstride + 0 .. D-1] (src is uniform: the (sequence, head) slice at
-// the segment's first frame). Wave w (uniform) issues copies w, w + 4, ...;
+// the segment's first frame). Wave w (uniform) of NW issues copies w, w + NW, ...;
 // copy I fills LDS bytes [1024 I, 1024 I + 1024). Rows at and beyond nrows are
 // left untouched. The caller waits (vmcnt) and barriers before reading X.
-template <int D>
+template <int D, int NW = 4>
 __device__ __forceinline__ void seg_issue(uint16_t* X, const uint16_t* src, int rstride, int nrows,
                                           int w, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR;
   const int rl = lane / CPR, pp = lane % CPR;
-  for (int I = w; I * RPI < nrows; I += 4) {
+  for (int I = w; I * RPI < nrows; I += NW) {
     const int r = I * RPI + rl;
     if (r < nrows) {
       const int p = pp ^ seg_swizzle<D>(r);

@@ -48,6 +48,11 @@ def test_config1_shape_float32(oracle_mod):
     (2, 190, 1, 64, 70, 0, (64, 190)),
     (2, 97, 2, 32, 200, 200, (30, 97)),
     (1, 40, 2, 64, 0, 0, "full"),
+    # a window that just fills one staged segment of 144 frames (64 + Lb + La),
+    # and one that needs the multi-segment sweep
+    (2, 260, 2, 64, 72, 8, (70, 260)),
+    (2, 300, 2, 64, 100, 20, (50, 300)),
+    (1, 600, 2, 32, 250, 60, (300, 600)),
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_backward_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):
