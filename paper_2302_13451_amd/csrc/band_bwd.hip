@@ -466,24 +466,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 }
 
 // Both roles of one 64-frame tile in one workgroup of 8 waves, for windows
-// whose sweeps fit one LDS segment (64 + Lb + La <= Seg<D>::kRows): waves 0-3
-// take the key role and waves 4-7 the query role. The query band
-// [f0 - La, fmax + Lb] of q and dout and the key band [f0 - Lb, fmax + La] of
-// k and v are staged once; each role finds its own rows inside the other
-// role's band, and D_n and lse of the query band are computed once for both.
+// with 48 + 32 ceil((16 + Lb + La) / 32) <= Seg<D>::kRows: waves 0-3 take the
+// key role and waves 4-7 the query role. The query band of q and dout starts
+// at frame f0 - La and the key band of k and v at f0 - Lb; each band stages
+// Seg<D>::kRows frames (frames outside the sequence are zero-filled), and each
+// role finds its own rows inside the other role's band. The 16 keys (queries)
+// of wave w sweep the band rows 16 (w % 4) + 32 m, m = 0, 1, ...: every
+// sub-block of a wave starts at the same offset from the wave's window, so a
+// window of 16 + Lb + La frames takes ceil((16 + Lb + La) / 32) sub-blocks.
+//
+// D_n = dout_n . out_n of the query band is the diagonal of one 16 x 16 MFMA
+// product per 16 rows (dout rows from LDS times out rows loaded straight into
+// the operand registers). It is stored negated, so that the products
+// dP = dout V^T start from -D and give dP - D directly. Query rows outside
+// the sequence get lse = +inf, so their weights are exactly zero without a
+// window test; the window test is only made in sub-blocks that cross a window
+// edge or the sequence's ends.
 template <int D>
 __global__ __launch_bounds__(2 * kThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void sa_bwd_tile_kernel(BwdDev a) {
   constexpr int NT = 2 * kThreads;
-  constexpr int SEG = Seg<D>::kRows, NST = Seg<D>::kStat;
-  constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
-  constexpr int NDI = (NST * CPR + NT - 1) / NT;  // out pieces per thread for D_n
-  __shared__ __attribute__((aligned(16))) uint16_t s_q[SEG * D];
-  __shared__ __attribute__((aligned(16))) uint16_t s_do[SEG * D];
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[SEG * D];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[SEG * D];
-  __shared__ __attribute__((aligned(16))) float s_dn[NST];
-  __shared__ __attribute__((aligned(16))) float s_lse2[NST];
+  constexpr int SEG = Seg<D>::kRows;
+  constexpr int NS = D / 32, NB = D / 16;
+  constexpr int NB16 = SEG / 16;           // 16-row blocks of the D product
+  constexpr int BPW = (NB16 + 7) / 8;      // ... per wave
+  static_assert(SEG % 16 == 0, "the D product covers the band in 16-row blocks");
+  // the four bands; once every wave is done with them, the first part holds
+  // each wave's output rows on their way to memory
+  __shared__ __attribute__((aligned(16))) uint16_t s_band[4 * SEG * D];
+  static_assert(8 * 2 * stage_elems<D>() <= 4 * SEG * D, "staging must fit in the bands");
+  uint16_t* const s_q = s_band;
+  uint16_t* const s_do = s_band + SEG * D;
+  uint16_t* const s_k = s_band + 2 * SEG * D;
+  uint16_t* const s_v = s_band + 3 * SEG * D;
+  __shared__ __attribute__((aligned(16))) float s_ndn[SEG];   // -D_n of the query band
+  __shared__ __attribute__((aligned(16))) float s_lse2[SEG];  // lse_n * log2(e); +inf outside the sequence
 
   int bh, tile;
   if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
@@ -501,46 +518,65 @@ void sa_bwd_tile_kernel(BwdDev a) {
     zero_rows<D, NT>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
     return;
   }
-  const int fmax = min(f0 + kC, len) - 1;
-  const int qlo = max(0, f0 - La), qhi = min(len - 1, fmax + Lb), nq = qhi - qlo + 1;
-  const int klo = max(0, f0 - Lb), khi = min(len - 1, fmax + La), nk = khi - klo + 1;
+  const int qbase = f0 - La, kbase = f0 - Lb;  // frames of band row 0 (may be negative)
+  // band rows that hold frames of the sequence; the others are zero-filled
+  const int qlo = max(0, -qbase), qhi = min(SEG, len - qbase);
+  const int klo = max(0, -kbase), khi = min(SEG, len - kbase);
   const size_t slice = row_index(b, 0, h, T, H, D);
   const int fs = H * D;  // elements from one frame to the next
   const uint16_t *q = a.q + slice, *k = a.k + slice, *v = a.v + slice;
   const uint16_t *o = a.o + slice, *dout = a.dout + slice;
   const float* lse_bh = a.lse + (static_cast<size_t>(b) * H + h) * T;
 
-  seg_issue<D, 8>(s_q, q + qlo * fs, fs, nq, w, lane);
-  seg_issue<D, 8>(s_do, dout + qlo * fs, fs, nq, w, lane);
-  seg_issue<D, 8>(s_k, k + klo * fs, fs, nk, w, lane);
-  seg_issue<D, 8>(s_v, v + klo * fs, fs, nk, w, lane);
-  // out rows and lse of the query band, for D_n = dout_n . out_n; a wave skips
-  // the pieces past the band as a whole, and loads the rest unconditionally
-  // (rows clamped), so that no lane overwrites a register with a load in flight
-  u32x4 ov[NDI];
+  seg_issue_rows<D, 8>(s_q, q, fs, qbase, qlo, qhi, w, lane);
+  seg_issue_rows<D, 8>(s_do, dout, fs, qbase, qlo, qhi, w, lane);
+  seg_issue_rows<D, 8>(s_k, k, fs, kbase, klo, khi, w, lane);
+  seg_issue_rows<D, 8>(s_v, v, fs, kbase, klo, khi, w, lane);
+  // out rows of the query band as the B operand of the D product (zero outside
+  // the sequence): wave w takes the 16-row blocks w, w + 8, ...
+  bf16x8 of[BPW][NS];
 #pragma unroll
-  for (int i = 0; i < NDI; ++i) {
-    ov[i] = kZero16;
-    if ((i * NT + w * 64) / CPR < nq) {
-      const int e = tid + i * NT, r = e / CPR, pc = e % CPR;
-      ov[i] = ld16(o + ((qlo + min(r, nq - 1)) * fs + 8 * pc));
+  for (int j = 0; j < BPW; ++j) {
+    const int fr = qbase + 16 * (w + 8 * j) + col;
+    const bool in = w + 8 * j < NB16 && fr >= 0 && fr < len;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      of[j][s] = bf16x8{};
+      if (in) of[j][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
     }
   }
   float lsev = 0.f;
-  if (w * 64 < NST) lsev = lse_bh[qlo + min(tid, nq - 1)];
+  const int lfr = qbase + tid;
+  if (tid < SEG && lfr >= 0 && lfr < len) lsev = lse_bh[lfr];
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (qlo > 0 || qhi < SEG || klo > 0 || khi < SEG) {  // the tile touches an end of the sequence
+    seg_zero_rows<D, NT>(s_q, 0, qlo, tid);
+    seg_zero_rows<D, NT>(s_q, qhi, SEG, tid);
+    seg_zero_rows<D, NT>(s_do, 0, qlo, tid);
+    seg_zero_rows<D, NT>(s_do, qhi, SEG, tid);
+    seg_zero_rows<D, NT>(s_k, 0, klo, tid);
+    seg_zero_rows<D, NT>(s_k, khi, SEG, tid);
+    seg_zero_rows<D, NT>(s_v, 0, klo, tid);
+    seg_zero_rows<D, NT>(s_v, khi, SEG, tid);
+    __syncthreads();
+  }
+  if (tid < SEG) s_lse2[tid] = (lfr >= 0 && lfr < len) ? lsev * kLog2e : __builtin_huge_valf();
 #pragma unroll
-  for (int i = 0; i < NDI; ++i) {
-    if ((i * NT + w * 64) / CPR < NST) {
-      const int e = tid + i * NT, r = e / CPR, pc = e % CPR;
-      float dn = r < nq ? dot8_bf16(ld16(s_do + seg_off<D>(r, 8 * pc)), ov[i]) : 0.f;
+  for (int j = 0; j < BPW; ++j) {
+    const int blk = w + 8 * j;
+    if (blk < NB16) {
+      f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int m = 1; m < CPR; m <<= 1) dn += __shfl_xor(dn, m);  // the row's pieces are adjacent lanes
-      if (pc == 0 && r < NST) s_dn[r] = dn;
+      for (int s = 0; s < NS; ++s)
+        dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(seg_row8<D>(s_do, 16 * blk + col, 32 * s + 8 * g), of[j][s], dd, 0, 0, 0);
+      // lane (g, col) holds rows 4g .. 4g + 3 of column col: the diagonal entry
+      // of row 16 blk + col sits in lane g = col / 4, element col % 4
+      const int e = col & 3;
+      const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
+      if ((col >> 2) == g) s_ndn[16 * blk + col] = -dg;
     }
   }
-  if (tid < NST) s_lse2[tid] = tid < nq ? lsev * kLog2e : 0.f;
   __syncthreads();
 
   const int r0 = f0 + 16 * (w & 3);
@@ -548,15 +584,17 @@ void sa_bwd_tile_kernel(BwdDev a) {
   const bool valid = me < len;
   const int mec = min(me, len - 1);  // lanes past the end read the last frame's rows, masked out
   const int wmax = min(r0 + 15, len - 1);
-  const int my_off = me * fs;
-  const SubBlockOffsets<D> so(lane);
+  const float c2 = a.scale_log2;
+  const int nblk = (16 + Lb + La + kSub - 1) / kSub;  // sub-blocks per wave
+  const int sb0 = 16 * (w & 3);                        // first sub-block of the wave
+  const BlockOffsets<D> bo(lane, 16 * (w & 1));
   if (w < 4) {
     // key role: keys r0 .. r0 + 15 against the query band
     bf16x8 kf[NS], vf[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kf[s] = seg_row8<D>(s_k, mec - klo, 32 * s + 8 * g);
-      vf[s] = seg_row8<D>(s_v, mec - klo, 32 * s + 8 * g);
+      kf[s] = seg_row8<D>(s_k, mec - kbase, 32 * s + 8 * g);
+      vf[s] = seg_row8<D>(s_v, mec - kbase, 32 * s + 8 * g);
     }
     f32x4 adv[NB], adk[NB];
 #pragma unroll
@@ -566,13 +604,17 @@ void sa_bwd_tile_kernel(BwdDev a) {
     const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
     const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
     const int mylo_v = valid ? mylo : 1 << 30;
-    const int rl = nq - 1;
-    for (int sb = 0; sb < nq && wlo <= whi; sb += kSub) {
-      const int qb = qlo + sb;
+    // a sub-block needs no window test when every valid key of the wave sees
+    // every query of it (queries outside the sequence weigh zero anyway)
+    const int ilo = wmax - La, ihi = r0 + Lb;
+    for (int m = 0; m < nblk; ++m) {
+      const int sb = sb0 + kSub * m, qb = qbase + sb;
       if (qb > whi || qb + kSub - 1 < wlo) continue;
       int oa, oc, ota, otc;
-      so.at(sb, rl, oa, oc, ota, otc);
-      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
+      bo.at(sb, oa, oc, ota, otc);
+      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
+      f32x4 dp0 = *reinterpret_cast<const f32x4*>(s_ndn + sb + 8 * g);
+      f32x4 dp1 = *reinterpret_cast<const f32x4*>(s_ndn + sb + 8 * g + 4);
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_q + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
@@ -580,42 +622,49 @@ void sa_bwd_tile_kernel(BwdDev a) {
         dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
         dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
       }
+      // statistics of the 8 queries this lane holds: rows sb + 8g .. +7
       const f32x4 l0 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g);
       const f32x4 l1 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g + 4);
-      const f32x4 n0 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g);
-      const f32x4 n1 = *reinterpret_cast<const f32x4*>(s_dn + sb + 8 * g + 4);
-      const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
-      bf16x8 pf, dsf;
+      f32x8 x;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = __builtin_fmaf(sc0[j], c2, -l0[j]);
+        x[j + 4] = __builtin_fmaf(sc1[j], c2, -l1[j]);
+      }
+      if (!(qb >= ilo && qb + kSub - 1 <= ihi)) {
+        const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
+      }
+      f32x8 ds;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float sv = j < 4 ? sc0[j] : sc1[j - 4];
-        const float dp = j < 4 ? dp0[j] : dp1[j - 4];
-        const float l2 = j < 4 ? l0[j] : l1[j - 4];
-        const float dnq = j < 4 ? n0[j] : n1[j - 4];
-        const bool ok = static_cast<unsigned>(d0 + j) <= span;
-        const float pw = fast_exp2(sv * a.scale_log2 - l2);
-        pf[j] = static_cast<__bf16>(ok ? pw : 0.f);
-        dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dnq) : 0.f);
+        x[j] = fast_exp2(x[j]);
+        ds[j] = x[j] * (j < 4 ? dp0[j] : dp1[j - 4]);
       }
+      const bf16x8 pf = __builtin_convertvector(x, bf16x8);
+      const bf16x8 dsf = __builtin_convertvector(ds, bf16x8);
+      // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
         adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_do, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
         adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_q, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
       }
     }
-    if (me < T) {
-      store_rows4<D>(a.dv + slice, my_off, adv, 1.f, valid, g);
-      store_rows4<D>(a.dk + slice, my_off, adk, a.scale, valid, g);
-    }
+    __syncthreads();  // every wave is done with the bands
+    uint16_t* stage = s_band + w * 2 * stage_elems<D>();
+    const int nrows = min(16, T - r0);
+    store_tile_rows<D>(stage, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+    store_tile_rows<D>(stage + stage_elems<D>(), a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   } else {
     // query role: queries r0 .. r0 + 15 against the key band
     bf16x8 qf[NS], df[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      qf[s] = seg_row8<D>(s_q, mec - qlo, 32 * s + 8 * g);
-      df[s] = seg_row8<D>(s_do, mec - qlo, 32 * s + 8 * g);
+      qf[s] = seg_row8<D>(s_q, mec - qbase, 32 * s + 8 * g);
+      df[s] = seg_row8<D>(s_do, mec - qbase, 32 * s + 8 * g);
     }
-    const float dn = s_dn[mec - qlo], lse2 = s_lse2[mec - qlo];
+    const float ndn = s_ndn[mec - qbase], lse2 = s_lse2[mec - qbase];
     f32x4 aq[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -624,13 +673,16 @@ void sa_bwd_tile_kernel(BwdDev a) {
     const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
     const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
     const int mylo_v = valid ? mylo : 1 << 30;
-    const int rl = nk - 1;
-    for (int sb = 0; sb < nk && wlo <= whi; sb += kSub) {
-      const int kb = klo + sb;
+    // a sub-block needs no window test when it lies in the window of every
+    // valid query of the wave (and so inside the sequence)
+    const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
+    for (int m = 0; m < nblk; ++m) {
+      const int sb = sb0 + kSub * m, kb = kbase + sb;
       if (kb > whi || kb + kSub - 1 < wlo) continue;
       int oa, oc, ota, otc;
-      so.at(sb, rl, oa, oc, ota, otc);
-      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0, dp0 = sc0, dp1 = sc0;
+      bo.at(sb, oa, oc, ota, otc);
+      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
+      f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_k + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
@@ -638,21 +690,28 @@ void sa_bwd_tile_kernel(BwdDev a) {
         dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
         dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
       }
-      const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
-      bf16x8 dsf;
+      f32x8 x;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float sv = j < 4 ? sc0[j] : sc1[j - 4];
-        const float dp = j < 4 ? dp0[j] : dp1[j - 4];
-        const bool ok = static_cast<unsigned>(d0 + j) <= span;
-        const float pw = fast_exp2(sv * a.scale_log2 - lse2);
-        dsf[j] = static_cast<__bf16>(ok ? pw * (dp - dn) : 0.f);
+      for (int j = 0; j < 4; ++j) {
+        x[j] = __builtin_fmaf(sc0[j], c2, -lse2);
+        x[j + 4] = __builtin_fmaf(sc1[j], c2, -lse2);
       }
+      if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {
+        const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = fast_exp2(x[j]) * (j < 4 ? dp0[j] : dp1[j - 4]);
+      const bf16x8 dsf = __builtin_convertvector(x, bf16x8);
+      // dq^T += k^T dS^T, contracting over the 32 keys
 #pragma unroll
       for (int i = 0; i < NB; ++i)
         aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_k, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
     }
-    if (me < T) store_rows4<D>(a.dq + slice, my_off, aq, a.scale, valid, g);
+    __syncthreads();  // every wave is done with the bands
+    store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, min(16, T - r0), aq,
+                       a.scale, valid, lane);
   }
 }
 
@@ -678,7 +737,8 @@ hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   d.scale_log2 = kLog2e * d.scale;
   d.ntiles = (a.T + kC - 1) / kC;
   const int seg_rows = a.d == 64 ? Seg<64>::kRows : Seg<32>::kRows;
-  if (kC + a.Lb + a.La <= seg_rows) {
+  const long long nblk = (16LL + a.Lb + a.La + kSub - 1) / kSub;
+  if (48 + kSub * nblk <= seg_rows) {
     // both sweeps fit one segment: one workgroup per tile
     const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
     if (a.d == 64)

@@ -32,6 +32,7 @@ namespace {
 constexpr int kTq = 64;       // queries per workgroup
 constexpr int kKC = 64;       // keys per LDS chunk
 constexpr int kThreads = 256;
+constexpr int kSub = 32;      // keys per MFMA sub-block of the tile kernel
 
 struct DevSeg {
   const void* k;
@@ -333,6 +334,231 @@ __global__ __launch_bounds__(kThreads) void band_fwd_f32_kernel(DevArgs a, int n
   }
 }
 
+// ---------------------------------------------------------------------------
+// bfloat16 tile kernel for windows whose bands fit in LDS. A workgroup owns
+// the 64 queries of one tile of one (sequence, head) for NJOB outputs (SA: one
+// output, 4 waves; LLSA: both outputs, 8 waves, waves 4j .. 4j + 3 for output
+// j). Each band (a pair of key and value tensors) is staged once, in one go,
+// with direct global->LDS copies: band b holds the frames f0 + base_b ..
+// f0 + base_b + rows_b - 1 (frames outside the sequence zero-filled). The 16
+// queries of wave w of an output sweep band b in 32-key sub-blocks starting at
+// row 16 (w % 4) + shift, so all four waves of an output see their window at
+// the same offset inside their sub-blocks and a window of 16 + hi - lo frames
+// takes ceil((16 + hi - lo) / 32) of them. Per sub-block: S^T = K Q^T on the
+// MFMA (queries are the N dimension: a lane owns one query), the window test
+// only in sub-blocks crossing a window edge or an end of the sequence, the
+// running maximum over the four lanes of a query with two lane-swap
+// instructions, weights rounded to bfloat16 and O^T += V^T P^T on the MFMA.
+// The row sums are kept in float per lane and summed over the column's lanes
+// at the end, so the log-sum-exp is that of the unrounded weights.
+struct TileBand {
+  const void* k;
+  const void* v;
+  int base;  // frame of band row 0, relative to the tile's first query
+};
+struct TileSeg {
+  int lo, hi;   // the window's frames t + lo .. t + hi come from this band
+  int shift;    // band row of frame f0 + lo (= lo - base)
+  int nblk;     // sub-blocks per wave
+};
+struct TileJob {
+  const void* q;
+  void* out;
+  float* lse;
+  TileSeg seg[2];
+};
+struct TileArgs {
+  TileBand band[2];
+  TileJob job[2];
+  int nband;
+  int B, T, H, ntiles;
+  const int32_t* lengths;
+  float scale_log2;
+};
+
+// Maximum and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 of a query
+// column, with the lane-swap instructions of gfx950 (each swap leaves x[l]
+// and x[l ^ 16] (x[l ^ 32]) in the two results of every lane, so every lane
+// gets the same value).
+__device__ __forceinline__ float max_over_column(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_over_column(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D, int NJOB, int SEG0, int SEG1>
+__global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
+  constexpr int NT = 256 * NJOB, NW = 4 * NJOB;
+  constexpr int NS = D / 32, NB = D / 16;
+  constexpr int CPR = D / 8;
+  __shared__ __attribute__((aligned(16))) uint16_t s_kv[2 * (SEG0 + SEG1) * D];
+  static_assert(NW * stage_elems<D>() <= 2 * (SEG0 + SEG1) * D, "staging must fit in the bands");
+  uint16_t* const bk[2] = {s_kv, s_kv + 2 * SEG0 * D};
+  uint16_t* const bv[2] = {s_kv + SEG0 * D, s_kv + (2 * SEG0 + SEG1) * D};
+  constexpr int brows[2] = {SEG0, SEG1};
+
+  int bh, tile;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
+  const int h = bh % a.H, b = bh / a.H;
+  const int T = a.T, H = a.H;
+  const int len = clamp_len_uniform(a.lengths, b, T);
+  const int f0 = tile * kTq;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, g = lane >> 4;
+  const size_t slice = row_index(b, 0, h, T, H, D);
+  const int fs = H * D;
+  float* lse_bh[NJOB];
+#pragma unroll
+  for (int j = 0; j < NJOB; ++j)
+    lse_bh[j] = a.job[j].lse ? a.job[j].lse + (static_cast<size_t>(b) * H + h) * T : nullptr;
+
+  if (f0 >= len) {  // padding tile: zeros, nothing read
+    const int r1 = min(f0 + kTq, T);
+#pragma unroll
+    for (int j = 0; j < NJOB; ++j) {
+      uint16_t* out = static_cast<uint16_t*>(a.job[j].out) + slice;
+      for (int e = tid; e < (r1 - f0) * CPR; e += NT) st16(out + (f0 + e / CPR) * fs + 8 * (e % CPR), kZero16);
+      if (lse_bh[j])
+        for (int r = f0 + tid; r < r1; r += NT) lse_bh[j][r] = kNegInf;
+    }
+    return;
+  }
+
+  // stage the bands; rows outside the sequence are zero-filled below
+  int blo[2], bhi[2];
+  bool edge = false;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi) {
+    if (bi >= a.nband) break;
+    const int bbase = f0 + a.band[bi].base;
+    blo[bi] = max(0, -bbase);
+    bhi[bi] = min(brows[bi], len - bbase);
+    edge |= blo[bi] > 0 || bhi[bi] < brows[bi];
+    seg_issue_rows<D, NW>(bk[bi], static_cast<const uint16_t*>(a.band[bi].k) + slice, fs, bbase, blo[bi], bhi[bi], w, lane);
+    seg_issue_rows<D, NW>(bv[bi], static_cast<const uint16_t*>(a.band[bi].v) + slice, fs, bbase, blo[bi], bhi[bi], w, lane);
+  }
+  const int jb = NJOB > 1 ? (w >> 2) : 0;
+  const TileJob& job = a.job[jb];
+  const int r0 = f0 + 16 * (w & 3);
+  const int t = r0 + col;  // this lane's query
+  const bool valid = t < len;
+  const int wmax = min(r0 + 15, len - 1);  // last valid query of the wave (< r0: none)
+  bf16x8 qf[NS];
+  {
+    const uint16_t* qp = static_cast<const uint16_t*>(job.q) + slice;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      qf[s] = bf16x8{};
+      if (valid) qf[s] = __builtin_bit_cast(bf16x8, ld16(qp + (t * fs + 32 * s + 8 * g)));
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (edge) {  // the tile touches an end of the sequence
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+      if (bi >= a.nband) break;
+      seg_zero_rows<D, NT>(bk[bi], 0, blo[bi], tid);
+      seg_zero_rows<D, NT>(bk[bi], bhi[bi], brows[bi], tid);
+      seg_zero_rows<D, NT>(bv[bi], 0, blo[bi], tid);
+      seg_zero_rows<D, NT>(bv[bi], bhi[bi], brows[bi], tid);
+    }
+    __syncthreads();
+  }
+
+  const float c2 = a.scale_log2;
+  float m = kNegInf, lsum = 0.f;
+  f32x4 acc[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi) {
+    if (bi >= a.nband) break;
+    const TileSeg sg = job.seg[bi];
+    if (sg.lo > sg.hi) continue;  // empty segment (no look-ahead)
+    const int bbase = f0 + a.band[bi].base;
+    const int wlo = max(0, r0 + sg.lo);
+    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + sg.hi);
+    // this lane's window in the band as (start, width): key inside iff
+    // (unsigned)(key - qlo) <= width; an empty window never matches
+    const int qlo = max(0, t + sg.lo), qhi = min(len - 1, t + sg.hi);
+    const unsigned qwidth = (valid && qhi >= qlo) ? static_cast<unsigned>(qhi - qlo) : 0u;
+    const int qlo_l = (valid && qhi >= qlo) ? qlo : 1 << 30;
+    // keys inside the window of every valid query of the wave
+    const int ilo = max(0, wmax + sg.lo), ihi = min(len - 1, r0 + sg.hi);
+    const int sb0 = 16 * (w & 3) + sg.shift;
+    const BlockOffsets<D> bo(lane, sb0);
+    const uint16_t* Xk = bk[bi];
+    const uint16_t* Xv = bv[bi];
+    for (int mm = 0; mm < sg.nblk; ++mm) {
+      const int sb = sb0 + kSub * mm, kb = bbase + sb;
+      if (kb > whi || kb + kSub - 1 < wlo) continue;  // uniform over the wave
+      int oa, oc, ota, otc;
+      bo.at(sb, oa, oc, ota, otc);
+      // score tiles: block 0 row r holds key sb + 8(r/4) + r%4, block 1 the
+      // same + 4, so lane (g, col) ends up with keys kb + 8g + 0..7
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(Xk + (oa ^ (32 * s))), qf[s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(Xk + (oc ^ (32 * s))), qf[s], s1, 0, 0, 0);
+      }
+      f32x8 z;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        z[j] = s0[j];
+        z[j + 4] = s1[j];
+      }
+      if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {  // crosses a window edge or an end: mask
+        const int base = kb + 8 * g - qlo_l;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) z[j] = static_cast<unsigned>(base + j) <= qwidth ? z[j] : kNegInf;
+      }
+      float zmax = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])),
+                         fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
+      const float mblk = max_over_column(zmax) * c2;
+      // Lazy rescaling: a row's exponent offset m only moves when its maximum
+      // grows by more than 2^8, so the weights stay below 256 and the
+      // accumulators are rarely touched. The decision is per row (the four
+      // lanes of a row hold the same mblk and m), so each output depends on
+      // its own window only, bit for bit.
+      const bool grow = mblk > m + 8.f;
+      if (__any(grow)) {
+        const float mnew = grow ? mblk : m;
+        const float alpha = grow ? fast_exp2(m - mnew) : 1.f;  // 0 on a row's first block
+        lsum *= alpha;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) acc[i] *= alpha;
+        m = mnew;
+      }
+      const float msafe = (m == kNegInf) ? 0.f : m;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) z[j] = fast_exp2(__builtin_fmaf(z[j], c2, -msafe));
+      lsum += ((z[0] + z[1]) + (z[2] + z[3])) + ((z[4] + z[5]) + (z[6] + z[7]));
+      const bf16x8 pf = __builtin_convertvector(z, bf16x8);
+      // O^T += V^T P^T: lane (g, col) needs V[kb + 8g + j][16i + col]
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(Xv, ota ^ (16 * i), otc ^ (16 * i)), pf, acc[i], 0, 0, 0);
+    }
+  }
+
+  lsum = sum_over_column(lsum);
+  __syncthreads();  // every wave is done with the bands
+  store_tile_rows<D>(s_kv + w * stage_elems<D>(), static_cast<uint16_t*>(job.out) + slice, fs, r0,
+                     min(16, T - r0), acc, valid ? 1.f / lsum : 0.f, valid, lane);
+  if (lse_bh[jb] && g == 0 && t < T)
+    lse_bh[jb][t] = valid ? (m + log2f(lsum)) * kLn2 : kNegInf;
+}
+
 DevSeg to_dev(const BandSegment& s) { return DevSeg{s.k, s.v, s.lo_off, s.hi_off}; }
 
 DevJob to_dev(const BandJob& j) {
@@ -346,9 +572,77 @@ DevJob to_dev(const BandJob& j) {
   return d;
 }
 
+
+// Rows staged per band by the tile kernel (for d = 64; twice as many for
+// d = 32, whose rows are half as long).
+constexpr int kSaRows = 144;                     // SA: 48 + 32 * 3 (Lb + La <= 80)
+constexpr int kLlsaRows0 = 152, kLlsaRows1 = 88;  // LLSA: both outputs, Lb = 64, La = 8 and smaller
+
+// Lays the jobs' window segments onto tile-kernel bands (segment i of every job
+// reads band i). Returns false when a band would need more than its rows.
+bool plan_tile(const BandForwardArgs& a, int rows0, int rows1, TileArgs& d) {
+  const int nseg = a.job[0].nseg;
+  for (int j = 1; j < a.njobs; ++j)
+    if (a.job[j].nseg != nseg) return false;
+  d.nband = nseg;
+  for (int i = 0; i < nseg; ++i) {
+    const int rows = i == 0 ? rows0 : rows1;
+    int base = 1 << 30;
+    for (int j = 0; j < a.njobs; ++j) {
+      const BandSegment& sg = a.job[j].seg[i];
+      if (sg.k != a.job[0].seg[i].k || sg.v != a.job[0].seg[i].v) return false;
+      if (sg.lo_off <= sg.hi_off) base = base < sg.lo_off ? base : sg.lo_off;
+    }
+    if (base == (1 << 30)) base = 0;  // every job's segment is empty
+    d.band[i] = TileBand{a.job[0].seg[i].k, a.job[0].seg[i].v, base};
+    for (int j = 0; j < a.njobs; ++j) {
+      const BandSegment& sg = a.job[j].seg[i];
+      TileSeg& ts = d.job[j].seg[i];
+      ts.lo = sg.lo_off;
+      ts.hi = sg.hi_off;
+      ts.shift = sg.lo_off - base;
+      ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + kSub) / kSub : 0;
+      if (ts.nblk > 0 && static_cast<long long>(ts.shift) + 48 + kSub * ts.nblk > rows) return false;
+    }
+  }
+  for (int j = 0; j < a.njobs; ++j) {
+    d.job[j].q = a.job[j].q;
+    d.job[j].out = a.job[j].out;
+    d.job[j].lse = a.job[j].lse;
+  }
+  return true;
+}
+
+template <int D>
+bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
+  TileArgs d{};
+  d.B = a.B;
+  d.T = a.T;
+  d.H = a.H;
+  d.ntiles = (a.T + kTq - 1) / kTq;
+  d.lengths = a.lengths;
+  d.scale_log2 = kLog2e / sqrtf(static_cast<float>(D));
+  constexpr int X = 64 / D;
+  const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
+  if (a.njobs == 1 && a.job[0].nseg == 1) {
+    if (!plan_tile(a, X * kSaRows, 0, d)) return false;
+    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 1, X * kSaRows, 0>), dim3(grid), dim3(256), 0, stream, d);
+    return true;
+  }
+  if (a.njobs == 2 && a.job[0].nseg == 2) {
+    if (!plan_tile(a, X * kLlsaRows0, X * kLlsaRows1, d)) return false;
+    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 2, X * kLlsaRows0, X * kLlsaRows1>), dim3(grid), dim3(512), 0,
+                       stream, d);
+    return true;
+  }
+  return false;
+}
+
 }  // namespace
 
 hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_t stream) {
+  if (et == kBF16 && (a.d == 64 ? launch_tile<64>(a, stream) : launch_tile<32>(a, stream)))
+    return hipGetLastError();
   DevArgs d;
   d.job0 = to_dev(a.job[0]);
   d.job1 = a.njobs > 1 ? to_dev(a.job[1]) : d.job0;
@@ -359,6 +653,7 @@ hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_
   d.lengths = a.lengths;
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
   if (et == kBF16) {
+    // windows too wide for the tile kernel's bands: chunked sweep
     d.ntiles = (a.T + kTq - 1) / kTq;
     const int grid = xcd_slice_grid(a.B * a.H, a.njobs * d.ntiles);
     if (a.d == 64)

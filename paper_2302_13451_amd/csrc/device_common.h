@@ -8,6 +8,9 @@ namespace sa {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+// eight floats; __builtin_convertvector of one to bf16x8 rounds to nearest even
+// with four paired conversions (v_cvt_pk_bf16_f32)
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 // 16 bytes as a native vector: copies of HIP's uint4 (a struct) become
 // aggregate memcpys that the compiler may leave in scratch memory
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -183,6 +186,92 @@ struct SubBlockOffsets {
     }
   }
 };
+
+// Per-lane offsets of the MFMA operand reads of 32-row sub-blocks that start
+// at segment rows sb = b0 + 32 m (b0 = 0 or 16): the swizzle only depends on
+// the low five bits of the row, so the offsets of every such sub-block are
+// those of the one at b0 plus (sb - b0) * D. Every row a sub-block touches
+// must hold finite data (loaded or zero-filled).
+template <int D>
+struct BlockOffsets {
+  int ra, rc, ta, tc;  // offsets in the sub-block at b0: rows xa, xa + 4 (row reads), xt, xt + 4 (transposing)
+  int b0;
+  __device__ __forceinline__ BlockOffsets(int lane, int base) : b0(base) {
+    const int col = lane & 15, g = lane >> 4;
+    const int xa = b0 + 8 * (col >> 2) + (col & 3);
+    const int xt = b0 + 8 * g + (col >> 2);
+    ra = seg_row_off<D>(xa, g);
+    rc = seg_row_off<D>(xa + 4, g);
+    ta = seg_tr_off<D>(xt, col);
+    tc = seg_tr_off<D>(xt + 4, col);
+  }
+  __device__ __forceinline__ void at(int sb, int& oa, int& oc, int& ota, int& otc) const {
+    const int d = (sb - b0) * D;
+    oa = ra + d; oc = rc + d; ota = ta + d; otc = tc + d;
+  }
+};
+
+// Issue the direct copies that fill segment rows [lo, hi) of X with frames
+// base + lo .. base + hi - 1 of src (src: the (sequence, head) slice at frame
+// 0, row stride rstride elements; base may be negative, frames base + r for
+// r in [lo, hi) must exist). Copy I fills rows RPI I .. RPI I + RPI - 1; lanes of
+// rows outside [lo, hi) are inactive and leave their bytes untouched. Wave w
+// (uniform) of NW issues copies w, w + NW, ... The caller waits (vmcnt) and
+// barriers before reading X.
+template <int D, int NW>
+__device__ __forceinline__ void seg_issue_rows(uint16_t* X, const uint16_t* src, int rstride, int base, int lo,
+                                               int hi, int w, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR;
+  const int rl = lane / CPR, pp = lane % CPR;
+  for (int I = lo / RPI + w; I * RPI < hi; I += NW) {
+    const int r = I * RPI + rl;
+    if (r >= lo && r < hi) {
+      const int p = pp ^ seg_swizzle<D>(r);
+      __builtin_amdgcn_global_load_lds(src + ((base + r) * rstride + 8 * p), X + I * 512, 16, 0, 0);
+    }
+  }
+}
+
+// Zero segment rows [lo, hi) of X (NT threads, thread tid).
+template <int D, int NT>
+__device__ __forceinline__ void seg_zero_rows(uint16_t* X, int lo, int hi, int tid) {
+  constexpr int CPR = D / 8;
+  for (int e = lo * CPR + tid; e < hi * CPR; e += NT) st16(X + 8 * e, kZero16);
+}
+
+// Number of elements a wave's staging area for one 16-row output tile takes
+// (rows of D elements padded to D + 8, so every row starts 16-byte aligned).
+template <int D>
+__host__ __device__ constexpr int stage_elems() { return 16 * (D + 8); }
+
+// Stores the 16 rows of one wave's output tile, held as MFMA accumulators
+// (lane (g, col) holds columns 16 i + 4 g .. + 3 of row col, i < D / 16), as
+// whole rows: the wave writes the rows, scaled by mul and rounded to bfloat16,
+// to its own LDS staging area, reads them back 16 bytes per lane and writes
+// every row of D elements with D / 8 adjacent lanes of one instruction. A
+// store that covers each 128-byte row in quarters is several times slower on
+// HBM. Rows of lanes with !valid are written as zeros; rows r0 + nrows and
+// beyond are not written. The staging area is private to the wave, so no
+// barrier is needed between the write and the read.
+template <int D>
+__device__ __forceinline__ void store_tile_rows(uint16_t* stage, uint16_t* dst, int fs, int r0, int nrows,
+                                                const f32x4* acc, float mul, bool valid, int lane) {
+  constexpr int SS = D + 8, CPR = D / 8, RPI = 64 / CPR;
+  const int g = lane >> 4, col = lane & 15;
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) {
+    u32x2 pk;
+    pk[0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    pk[1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
+    st8(stage + col * SS + 16 * i + 4 * g, pk);
+  }
+#pragma unroll
+  for (int h = 0; h < 16 / RPI; ++h) {
+    const int rr = h * RPI + lane / CPR, c = lane % CPR;
+    const u32x4 v = ld16(stage + rr * SS + 8 * c);
+    if (rr < nrows) st16(dst + (r0 + rr) * fs + 8 * c, v);
+  }
+}
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2): block bid runs on XCD bid % 8. XCD x walks the (sequence, head) slices
