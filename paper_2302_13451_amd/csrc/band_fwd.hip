@@ -393,7 +393,113 @@ __device__ __forceinline__ float sum_over_column(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int NJOB, int SEG0, int SEG1>
+// A wave's window segment inside a staged band: its 16 queries r0 .. r0 + 15
+// (this lane's: t) see frames t + lo .. t + hi, held by band rows from sb0 on.
+template <int D>
+struct WaveSeg {
+  const uint16_t* Xk;
+  const uint16_t* Xv;
+  BlockOffsets<D> bo;  // operand offsets of the sub-blocks at sb0 + 32 m
+  int sb0;             // band row of the wave's first sub-block
+  int kb0;             // its frame
+  int nblk;            // sub-blocks of the wave's window
+  int wlo, whi;        // frames of the wave's window (whi < wlo: empty)
+  int qlo_l;           // this lane's first frame (1 << 30: empty window)
+  unsigned qwidth;     // ... and the width of its window
+  int ilo, ihi;        // frames inside the window of every valid query of the wave
+  __device__ __forceinline__ WaveSeg(const uint16_t* k, const uint16_t* v, int lane, int bbase, int shift, int nb,
+                                     int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq)
+      : Xk(k), Xv(v), bo(lane, 16 * wq + shift) {
+    sb0 = 16 * wq + shift;
+    kb0 = bbase + sb0;
+    nblk = lo <= hi ? nb : 0;
+    wlo = max(0, r0 + lo);
+    whi = (wmax < r0) ? -1 : min(len - 1, wmax + hi);
+    const int qlo = max(0, t + lo), qhi = min(len - 1, t + hi);
+    const bool any = valid && qhi >= qlo;
+    qwidth = any ? static_cast<unsigned>(qhi - qlo) : 0u;
+    qlo_l = any ? qlo : 1 << 30;
+    ilo = max(0, wmax + lo);
+    ihi = min(len - 1, r0 + hi);
+  }
+};
+
+// First pass over a segment: the scaled scores y = (q . k) log2(e) / sqrt(d)
+// of the wave's NBM sub-blocks (lane (g, col): keys kb + 8g + 0..7 of query
+// col; the score tiles take the key rows in the order 8(r/4) + r%4 and + 4,
+// which puts them straight into the weight operand layout of the PV product),
+// -inf outside the lane's window. All NBM sub-blocks are computed without
+// branches, so the LDS reads and MFMAs of different sub-blocks overlap: the
+// band must hold finite data in every row they touch (rows outside the
+// sequence, or past the window, are masked). Returns the lane's maximum.
+template <int D, int NBM>
+__device__ __forceinline__ float seg_scores(const WaveSeg<D>& s, const bf16x8* qf, float c2, int lane, f32x8* y) {
+  constexpr int NS = D / 32;
+  const int g = lane >> 4;
+  bf16x8 ka[NBM][2 * NS];
+#pragma unroll
+  for (int m = 0; m < NBM; ++m) {
+    int oa, oc, ota, otc;
+    s.bo.at(s.sb0 + kSub * m, oa, oc, ota, otc);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      ka[m][2 * k] = lds_row8(s.Xk + (oa ^ (32 * k)));
+      ka[m][2 * k + 1] = lds_row8(s.Xk + (oc ^ (32 * k)));
+    }
+  }
+  float ymax = kNegInf;
+#pragma unroll
+  for (int m = 0; m < NBM; ++m) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][2 * k], qf[k], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][2 * k + 1], qf[k], s1, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      y[m][j] = s0[j] * c2;
+      y[m][j + 4] = s1[j] * c2;
+    }
+    const int kb = s.kb0 + kSub * m;
+    if (!(m < s.nblk && kb >= s.ilo && kb + kSub - 1 <= s.ihi)) {  // not inside every window: mask
+      const int base = kb + 8 * g - s.qlo_l;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[m][j] = static_cast<unsigned>(base + j) <= s.qwidth ? y[m][j] : kNegInf;
+    }
+    ymax = fmaxf(ymax, fmaxf(fmaxf(fmaxf(y[m][0], y[m][1]), fmaxf(y[m][2], y[m][3])),
+                             fmaxf(fmaxf(y[m][4], y[m][5]), fmaxf(y[m][6], y[m][7]))));
+  }
+  return ymax;
+}
+
+// Second pass: weights p = 2^(y - mx), their float sum, and O^T += V^T P^T
+// with the weights rounded to bfloat16 (lane (g, col) needs
+// V[kb + 8g + j][16 i + col], the transposing LDS read).
+template <int D, int NBM>
+__device__ __forceinline__ void seg_weights_pv(const WaveSeg<D>& s, const f32x8* y, float mx, f32x4* acc,
+                                               float& lsum) {
+  constexpr int NB = D / 16;
+  bf16x8 pf[NBM];
+#pragma unroll
+  for (int m = 0; m < NBM; ++m) {
+    f32x8 p;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) p[j] = fast_exp2(y[m][j] - mx);
+    lsum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+    pf[m] = __builtin_convertvector(p, bf16x8);
+  }
+#pragma unroll
+  for (int m = 0; m < NBM; ++m) {
+    int oa, oc, ota, otc;
+    s.bo.at(s.sb0 + kSub * m, oa, oc, ota, otc);
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s.Xv, ota ^ (16 * i), otc ^ (16 * i)), pf[m], acc[i], 0, 0, 0);
+  }
+}
+
+template <int D, int NJOB, int SEG0, int SEG1, int NB0, int NB1>
 __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
   constexpr int NT = 256 * NJOB, NW = 4 * NJOB;
   constexpr int NS = D / 32, NB = D / 16;
@@ -475,81 +581,35 @@ __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
   }
 
   const float c2 = a.scale_log2;
-  float m = kNegInf, lsum = 0.f;
+  float lsum = 0.f;
   f32x4 acc[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi) {
-    if (bi >= a.nband) break;
-    const TileSeg sg = job.seg[bi];
-    if (sg.lo > sg.hi) continue;  // empty segment (no look-ahead)
-    const int bbase = f0 + a.band[bi].base;
-    const int wlo = max(0, r0 + sg.lo);
-    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + sg.hi);
-    // this lane's window in the band as (start, width): key inside iff
-    // (unsigned)(key - qlo) <= width; an empty window never matches
-    const int qlo = max(0, t + sg.lo), qhi = min(len - 1, t + sg.hi);
-    const unsigned qwidth = (valid && qhi >= qlo) ? static_cast<unsigned>(qhi - qlo) : 0u;
-    const int qlo_l = (valid && qhi >= qlo) ? qlo : 1 << 30;
-    // keys inside the window of every valid query of the wave
-    const int ilo = max(0, wmax + sg.lo), ihi = min(len - 1, r0 + sg.hi);
-    const int sb0 = 16 * (w & 3) + sg.shift;
-    const BlockOffsets<D> bo(lane, sb0);
-    const uint16_t* Xk = bk[bi];
-    const uint16_t* Xv = bv[bi];
-    for (int mm = 0; mm < sg.nblk; ++mm) {
-      const int sb = sb0 + kSub * mm, kb = bbase + sb;
-      if (kb > whi || kb + kSub - 1 < wlo) continue;  // uniform over the wave
-      int oa, oc, ota, otc;
-      bo.at(sb, oa, oc, ota, otc);
-      // score tiles: block 0 row r holds key sb + 8(r/4) + r%4, block 1 the
-      // same + 4, so lane (g, col) ends up with keys kb + 8g + 0..7
-      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(Xk + (oa ^ (32 * s))), qf[s], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(Xk + (oc ^ (32 * s))), qf[s], s1, 0, 0, 0);
-      }
-      f32x8 z;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        z[j] = s0[j];
-        z[j + 4] = s1[j];
-      }
-      if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {  // crosses a window edge or an end: mask
-        const int base = kb + 8 * g - qlo_l;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) z[j] = static_cast<unsigned>(base + j) <= qwidth ? z[j] : kNegInf;
-      }
-      float zmax = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])),
-                         fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
-      const float mblk = max_over_column(zmax) * c2;
-      // Lazy rescaling: a row's exponent offset m only moves when its maximum
-      // grows by more than 2^8, so the weights stay below 256 and the
-      // accumulators are rarely touched. The decision is per row (the four
-      // lanes of a row hold the same mblk and m), so each output depends on
-      // its own window only, bit for bit.
-      const bool grow = mblk > m + 8.f;
-      if (__any(grow)) {
-        const float mnew = grow ? mblk : m;
-        const float alpha = grow ? fast_exp2(m - mnew) : 1.f;  // 0 on a row's first block
-        lsum *= alpha;
-#pragma unroll
-        for (int i = 0; i < NB; ++i) acc[i] *= alpha;
-        m = mnew;
-      }
-      const float msafe = (m == kNegInf) ? 0.f : m;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) z[j] = fast_exp2(__builtin_fmaf(z[j], c2, -msafe));
-      lsum += ((z[0] + z[1]) + (z[2] + z[3])) + ((z[4] + z[5]) + (z[6] + z[7]));
-      const bf16x8 pf = __builtin_convertvector(z, bf16x8);
-      // O^T += V^T P^T: lane (g, col) needs V[kb + 8g + j][16i + col]
-#pragma unroll
-      for (int i = 0; i < NB; ++i)
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(Xv, ota ^ (16 * i), otc ^ (16 * i)), pf, acc[i], 0, 0, 0);
-    }
+  // two passes over the window, which a wave holds in registers whole: the
+  // scores of every sub-block and their maximum, then the weights and PV
+  const TileSeg sg0 = job.seg[0];
+  const WaveSeg<D> ws0(bk[0], bv[0], lane, f0 + a.band[0].base, sg0.shift, sg0.nblk, sg0.lo, sg0.hi, r0, wmax, t,
+                       valid, len, w & 3);
+  f32x8 y0[NB0];
+  float ymax = seg_scores<D, NB0>(ws0, qf, c2, lane, y0);
+  if constexpr (NB1 > 0) {
+    const TileSeg sg1 = job.seg[1];
+    const WaveSeg<D> ws1(bk[1], bv[1], lane, f0 + a.band[1].base, sg1.shift, sg1.nblk, sg1.lo, sg1.hi, r0, wmax,
+                         t, valid, len, w & 3);
+    f32x8 y1[NB1];
+    ymax = fmaxf(ymax, seg_scores<D, NB1>(ws1, qf, c2, lane, y1));
+    float mx = max_over_column(ymax);
+    mx = mx == kNegInf ? 0.f : mx;  // no key in the window (past the sequence's end)
+    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
+    seg_weights_pv<D, NB1>(ws1, y1, mx, acc, lsum);
+    ymax = mx;
+  } else {
+    float mx = max_over_column(ymax);
+    mx = mx == kNegInf ? 0.f : mx;
+    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
+    ymax = mx;
   }
+  const float m = ymax;
 
   lsum = sum_over_column(lsum);
   __syncthreads();  // every wave is done with the bands
@@ -577,6 +637,8 @@ DevJob to_dev(const BandJob& j) {
 // d = 32, whose rows are half as long).
 constexpr int kSaRows = 144;                     // SA: 48 + 32 * 3 (Lb + La <= 80)
 constexpr int kLlsaRows0 = 152, kLlsaRows1 = 88;  // LLSA: both outputs, Lb = 64, La = 8 and smaller
+// Sub-blocks a wave holds in registers per band (the window of one band).
+constexpr int kMaxBlocks0 = 3, kMaxBlocks1 = 1;
 
 // Lays the jobs' window segments onto tile-kernel bands (segment i of every job
 // reads band i). Returns false when a band would need more than its rows.
@@ -602,7 +664,10 @@ bool plan_tile(const BandForwardArgs& a, int rows0, int rows1, TileArgs& d) {
       ts.hi = sg.hi_off;
       ts.shift = sg.lo_off - base;
       ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + kSub) / kSub : 0;
-      if (ts.nblk > 0 && static_cast<long long>(ts.shift) + 48 + kSub * ts.nblk > rows) return false;
+      // every wave computes all of the kernel's sub-blocks of a band, the
+      // last of them starting at row shift + 48 + 32 (blocks - 1)
+      const int blocks = i == 0 ? kMaxBlocks0 : kMaxBlocks1;
+      if (ts.nblk > blocks || static_cast<long long>(ts.shift) + 48 + kSub * blocks > rows) return false;
     }
   }
   for (int j = 0; j < a.njobs; ++j) {
@@ -626,12 +691,12 @@ bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
   const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
   if (a.njobs == 1 && a.job[0].nseg == 1) {
     if (!plan_tile(a, X * kSaRows, 0, d)) return false;
-    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 1, X * kSaRows, 0>), dim3(grid), dim3(256), 0, stream, d);
+    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 1, X * kSaRows, 0, 3, 0>), dim3(grid), dim3(256), 0, stream, d);
     return true;
   }
   if (a.njobs == 2 && a.job[0].nseg == 2) {
     if (!plan_tile(a, X * kLlsaRows0, X * kLlsaRows1, d)) return false;
-    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 2, X * kLlsaRows0, X * kLlsaRows1>), dim3(grid), dim3(512), 0,
+    hipLaunchKernelGGL((band_fwd_tile_kernel<D, 2, X * kLlsaRows0, X * kLlsaRows1, 3, 1>), dim3(grid), dim3(512), 0,
                        stream, d);
     return true;
   }

@@ -273,6 +273,17 @@ __device__ __forceinline__ void store_tile_rows(uint16_t* stage, uint16_t* dst, 
   }
 }
 
+// Workgroup barrier that orders LDS accesses only. __syncthreads() also waits
+// for every global load and store of the wave to complete (vmcnt(0)), which
+// would make a wave that has just stored its outputs wait for the stores'
+// acknowledgement. Data that direct global->LDS copies bring in must be
+// waited for (vmcnt) by the issuing wave before this barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2): block bid runs on XCD bid % 8. XCD x walks the (sequence, head) slices
 // x, x + 8, x + 16, ... and, within a slice, its per_slice work items in
