@@ -465,6 +465,196 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
 }
 
+// The staged bands of one 64-frame tile of a (sequence, head) as the two
+// backward roles see them: the query band (q, dout, -D_n, lse_n log2 e) from
+// frame qbase = f0 - La and the key band (k, v) from kbase = f0 - Lb, every
+// row a sub-block touches holding finite data. Query rows outside the
+// sequence carry lse = +inf, so their weights are exactly zero. Band row r
+// sits in LDS row (slot0 + r) mod RR of each band array (RR rows, a multiple
+// of 32; slot0 a multiple of 16), rows in the swizzled layout of their LDS
+// row, so the bands can live in a ring that later tiles extend.
+template <int D, int RR>
+struct BwdBands {
+  const uint16_t *q, *dout, *k, *v;
+  const float *ndn, *lse2;
+  int qbase, kbase, slot0;
+  // LDS row of band row r (0 <= r < RR)
+  __device__ __forceinline__ int row(int r) const {
+    const int x = slot0 + r;
+    return x >= RR ? x - RR : x;
+  }
+};
+
+// Element offset o of an LDS row taken modulo RR rows (o < 2 RR D).
+template <int D, int RR>
+__device__ __forceinline__ int ring_wrap(int o) {
+  const unsigned u = static_cast<unsigned>(o), w = u - static_cast<unsigned>(RR * D);
+  return static_cast<int>(u < w ? u : w);
+}
+
+// Per-lane operand offsets of the wave's sub-blocks in the bands: the
+// sub-block at band row sb (sb = 16 wq + 32 m) sits at LDS rows slot0 + sb ..,
+// whose swizzle pattern repeats every 32 rows.
+template <int D, int RR>
+struct RingOffsets {
+  BlockOffsets<D> bo;
+  int s0;
+  __device__ __forceinline__ RingOffsets(int lane, int slot0, int wq)
+      : bo(lane, 16 * (((slot0 >> 4) + wq) & 1)), s0(slot0) {}
+  __device__ __forceinline__ void at(int sb, int& oa, int& oc, int& ota, int& otc) const {
+    bo.at(s0 + sb, oa, oc, ota, otc);
+    oa = ring_wrap<D, RR>(oa);
+    oc = ring_wrap<D, RR>(oc);
+    ota = ring_wrap<D, RR>(ota);
+    otc = ring_wrap<D, RR>(otc);
+  }
+};
+
+// Key role of one wave: keys r0 .. r0 + 15 against the query band. Each of the
+// wave's nblk sub-blocks starts at band row 16 wq + 32 m, so the wave's window
+// [r0 - La, r0 + 15 + Lb] starts at the same place in the first one; window
+// tests are made only in sub-blocks that cross a window edge. Accumulates
+// dv^T and (dk sqrt d)^T.
+template <int D, int RR>
+__device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
+                                             int nblk, float c2, int lane, f32x4* adv, f32x4* adk) {
+  constexpr int NS = D / 32, NB = D / 16;
+  const int col = lane & 15, g = lane >> 4;
+  const int me = r0 + col;
+  const bool valid = me < len;
+  const int mec = min(me, len - 1);  // lanes past the end read the last frame's rows, masked out
+  const int wmax = min(r0 + 15, len - 1);
+  bf16x8 kf[NS], vf[NS];
+  const int kr = bd.row(mec - bd.kbase);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    kf[s] = seg_row8<D>(bd.k, kr, 32 * s + 8 * g);
+    vf[s] = seg_row8<D>(bd.v, kr, 32 * s + 8 * g);
+  }
+#pragma unroll
+  for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int wlo = max(0, r0 - La);
+  const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
+  const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
+  const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+  const int mylo_v = valid ? mylo : 1 << 30;
+  // a sub-block needs no window test when every valid key of the wave sees
+  // every query of it (queries outside the sequence weigh zero anyway)
+  const int ilo = wmax - La, ihi = r0 + Lb;
+  const int sb0 = 16 * wq;
+  const RingOffsets<D, RR> ro(lane, bd.slot0, wq);
+  for (int m = 0; m < nblk; ++m) {
+    const int sb = sb0 + kSub * m, qb = bd.qbase + sb;
+    if (qb > whi || qb + kSub - 1 < wlo) continue;
+    int oa, oc, ota, otc;
+    ro.at(sb, oa, oc, ota, otc);
+    const int st = bd.row(sb + 8 * g);  // statistics of rows sb + 8g .. + 7 (never split by the wrap)
+    f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
+    f32x4 dp0 = *reinterpret_cast<const f32x4*>(bd.ndn + st);
+    f32x4 dp1 = *reinterpret_cast<const f32x4*>(bd.ndn + st + 4);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.q + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.q + (oc ^ (32 * s))), kf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.dout + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.dout + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
+    }
+    const f32x4 l0 = *reinterpret_cast<const f32x4*>(bd.lse2 + st);
+    const f32x4 l1 = *reinterpret_cast<const f32x4*>(bd.lse2 + st + 4);
+    f32x8 x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = __builtin_fmaf(sc0[j], c2, -l0[j]);
+      x[j + 4] = __builtin_fmaf(sc1[j], c2, -l1[j]);
+    }
+    if (!(qb >= ilo && qb + kSub - 1 <= ihi)) {
+      const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
+    }
+    f32x8 ds;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      x[j] = fast_exp2(x[j]);
+      ds[j] = x[j] * (j < 4 ? dp0[j] : dp1[j - 4]);
+    }
+    const bf16x8 pf = __builtin_convertvector(x, bf16x8);
+    const bf16x8 dsf = __builtin_convertvector(ds, bf16x8);
+    // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.dout, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
+      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.q, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
+    }
+  }
+}
+
+// Query role of one wave: queries r0 .. r0 + 15 against the key band, in the
+// same sub-block arrangement. Accumulates (dq sqrt d)^T.
+template <int D, int RR>
+__device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
+                                               int nblk, float c2, int lane, f32x4* aq) {
+  constexpr int NS = D / 32, NB = D / 16;
+  const int col = lane & 15, g = lane >> 4;
+  const int me = r0 + col;
+  const bool valid = me < len;
+  const int mec = min(me, len - 1);
+  const int wmax = min(r0 + 15, len - 1);
+  bf16x8 qf[NS], df[NS];
+  const int qr = bd.row(mec - bd.qbase);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    qf[s] = seg_row8<D>(bd.q, qr, 32 * s + 8 * g);
+    df[s] = seg_row8<D>(bd.dout, qr, 32 * s + 8 * g);
+  }
+  const float ndn = bd.ndn[qr], lse2 = bd.lse2[qr];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int wlo = max(0, r0 - Lb);
+  const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
+  const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
+  const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
+  const int mylo_v = valid ? mylo : 1 << 30;
+  // a sub-block needs no window test when it lies in the window of every
+  // valid query of the wave (and so inside the sequence)
+  const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
+  const int sb0 = 16 * wq;
+  const RingOffsets<D, RR> ro(lane, bd.slot0, wq);
+  for (int m = 0; m < nblk; ++m) {
+    const int sb = sb0 + kSub * m, kb = bd.kbase + sb;
+    if (kb > whi || kb + kSub - 1 < wlo) continue;
+    int oa, oc, ota, otc;
+    ro.at(sb, oa, oc, ota, otc);
+    f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
+    f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.k + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.k + (oc ^ (32 * s))), qf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.v + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.v + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
+    }
+    f32x8 x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = __builtin_fmaf(sc0[j], c2, -lse2);
+      x[j + 4] = __builtin_fmaf(sc1[j], c2, -lse2);
+    }
+    if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {
+      const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = fast_exp2(x[j]) * (j < 4 ? dp0[j] : dp1[j - 4]);
+    const bf16x8 dsf = __builtin_convertvector(x, bf16x8);
+    // dq^T += k^T dS^T, contracting over the 32 keys
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.k, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
+  }
+}
+
 // Both roles of one 64-frame tile in one workgroup of 8 waves, for windows
 // with 48 + 32 ceil((16 + Lb + La) / 32) <= Seg<D>::kRows: waves 0-3 take the
 // key role and waves 4-7 the query role. The query band of q and dout starts
@@ -580,141 +770,266 @@ void sa_bwd_tile_kernel(BwdDev a) {
   __syncthreads();
 
   const int r0 = f0 + 16 * (w & 3);
-  const int me = r0 + col;  // this lane's key (waves 0-3) or query (waves 4-7)
-  const bool valid = me < len;
-  const int mec = min(me, len - 1);  // lanes past the end read the last frame's rows, masked out
-  const int wmax = min(r0 + 15, len - 1);
-  const float c2 = a.scale_log2;
+  const bool valid = r0 + col < len;
   const int nblk = (16 + Lb + La + kSub - 1) / kSub;  // sub-blocks per wave
-  const int sb0 = 16 * (w & 3);                        // first sub-block of the wave
-  const BlockOffsets<D> bo(lane, 16 * (w & 1));
+  const BwdBands<D, SEG> bands{s_q, s_do, s_k, s_v, s_ndn, s_lse2, qbase, kbase, 0};
+  const int nrows = min(16, T - r0);
   if (w < 4) {
-    // key role: keys r0 .. r0 + 15 against the query band
-    bf16x8 kf[NS], vf[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      kf[s] = seg_row8<D>(s_k, mec - kbase, 32 * s + 8 * g);
-      vf[s] = seg_row8<D>(s_v, mec - kbase, 32 * s + 8 * g);
-    }
     f32x4 adv[NB], adk[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int wlo = max(0, r0 - La);
-    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
-    const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
-    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
-    const int mylo_v = valid ? mylo : 1 << 30;
-    // a sub-block needs no window test when every valid key of the wave sees
-    // every query of it (queries outside the sequence weigh zero anyway)
-    const int ilo = wmax - La, ihi = r0 + Lb;
-    for (int m = 0; m < nblk; ++m) {
-      const int sb = sb0 + kSub * m, qb = qbase + sb;
-      if (qb > whi || qb + kSub - 1 < wlo) continue;
-      int oa, oc, ota, otc;
-      bo.at(sb, oa, oc, ota, otc);
-      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
-      f32x4 dp0 = *reinterpret_cast<const f32x4*>(s_ndn + sb + 8 * g);
-      f32x4 dp1 = *reinterpret_cast<const f32x4*>(s_ndn + sb + 8 * g + 4);
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_q + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
-        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_q + (oc ^ (32 * s))), kf[s], sc1, 0, 0, 0);
-        dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
-        dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_do + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
-      }
-      // statistics of the 8 queries this lane holds: rows sb + 8g .. +7
-      const f32x4 l0 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g);
-      const f32x4 l1 = *reinterpret_cast<const f32x4*>(s_lse2 + sb + 8 * g + 4);
-      f32x8 x;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[j] = __builtin_fmaf(sc0[j], c2, -l0[j]);
-        x[j + 4] = __builtin_fmaf(sc1[j], c2, -l1[j]);
-      }
-      if (!(qb >= ilo && qb + kSub - 1 <= ihi)) {
-        const int d0 = qb + 8 * g - mylo_v;  // query qb + 8g + j sees me iff 0 <= d0 + j <= span
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
-      }
-      f32x8 ds;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        x[j] = fast_exp2(x[j]);
-        ds[j] = x[j] * (j < 4 ? dp0[j] : dp1[j - 4]);
-      }
-      const bf16x8 pf = __builtin_convertvector(x, bf16x8);
-      const bf16x8 dsf = __builtin_convertvector(ds, bf16x8);
-      // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_do, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
-        adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_q, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
-      }
-    }
+    bwd_key_role<D, SEG>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
     __syncthreads();  // every wave is done with the bands
     uint16_t* stage = s_band + w * 2 * stage_elems<D>();
-    const int nrows = min(16, T - r0);
     store_tile_rows<D>(stage, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
     store_tile_rows<D>(stage + stage_elems<D>(), a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   } else {
-    // query role: queries r0 .. r0 + 15 against the key band
-    bf16x8 qf[NS], df[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      qf[s] = seg_row8<D>(s_q, mec - qbase, 32 * s + 8 * g);
-      df[s] = seg_row8<D>(s_do, mec - qbase, 32 * s + 8 * g);
-    }
-    const float ndn = s_ndn[mec - qbase], lse2 = s_lse2[mec - qbase];
     f32x4 aq[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int wlo = max(0, r0 - Lb);
-    const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
-    const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
-    const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
-    const int mylo_v = valid ? mylo : 1 << 30;
-    // a sub-block needs no window test when it lies in the window of every
-    // valid query of the wave (and so inside the sequence)
-    const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
-    for (int m = 0; m < nblk; ++m) {
-      const int sb = sb0 + kSub * m, kb = kbase + sb;
-      if (kb > whi || kb + kSub - 1 < wlo) continue;
-      int oa, oc, ota, otc;
-      bo.at(sb, oa, oc, ota, otc);
-      f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
-      f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_k + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
-        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_k + (oc ^ (32 * s))), qf[s], sc1, 0, 0, 0);
-        dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
-        dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(s_v + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
-      }
-      f32x8 x;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[j] = __builtin_fmaf(sc0[j], c2, -lse2);
-        x[j + 4] = __builtin_fmaf(sc1[j], c2, -lse2);
-      }
-      if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {
-        const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = static_cast<unsigned>(d0 + j) <= span ? x[j] : kNegInf;
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = fast_exp2(x[j]) * (j < 4 ? dp0[j] : dp1[j - 4]);
-      const bf16x8 dsf = __builtin_convertvector(x, bf16x8);
-      // dq^T += k^T dS^T, contracting over the 32 keys
-#pragma unroll
-      for (int i = 0; i < NB; ++i)
-        aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s_k, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
-    }
+    bwd_query_role<D, SEG>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, aq);
     __syncthreads();  // every wave is done with the bands
-    store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, min(16, T - r0), aq,
-                       a.scale, valid, lane);
+    store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
   }
 }
 
+
+// Persistent backward for sequences that fit the lanes of a wave (B <= 64):
+// one workgroup per compute unit walks a contiguous share of the (sequence,
+// head, tile) list, whose consecutive tiles of a (sequence, head) share all but
+// 64 rows of their bands. The bands live in LDS rings of RR = 2 SEG rows: a
+// tile that continues the previous one copies only its 64 new rows, a tile
+// that starts a (sequence, head) copies its whole band behind the previous
+// one. Four loader waves copy the next tile while eight compute waves work on
+// the current one, so the compute waves never wait on memory: they read LDS
+// and store.
+// The loaders also form D = rowsum(dout * out) of the new query rows (the
+// softmax backward, Sec. 3) with the MFMA diagonal, and their lse statistics.
+// Band rows outside the sequence hold copies of its first or last frame
+// (finite data) and are masked: query rows by lse = +inf, key rows by the
+// window test.
+constexpr int kPersistMaxB = 64;
+
+template <int D, int SEG>
+struct RingRegs {
+  static constexpr int NS = D / 32, BPL = (SEG / 16 + 3) / 4;
+  bf16x8 of[BPL][NS], df[BPL][NS];  // out and dout rows of the loader's new 16-row blocks
+  float lse[BPL];
+};
+
+// The band rows [rlo, bl) of tile cur go to ring rows (slot + r) mod 2 SEG, in
+// 16-row blocks (slot, rlo and bl are multiples of 16, so no block is split by
+// the wrap); loader lw takes blocks lw, lw + 4, ... Frames are clamped into the
+// sequence.
+template <int D, int SEG>
+__device__ __forceinline__ void ring_copy(const BwdDev& a, const TileCursor<1>& cur, uint16_t* ring, int slot, int rlo,
+                                          int bl, int lw, int lane) {
+  constexpr int RR = 2 * SEG, CPR = D / 8, RPI = 64 / CPR, IPB = 16 / RPI;
+  const int rl = lane / CPR, pp = lane % CPR;
+  const int fs = a.H * D;
+  const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
+  const int f0 = cur.tile * kC, qbase = f0 - a.La, kbase = f0 - a.Lb, last = cur.len - 1;
+  const uint16_t *q = a.q + slice, *dout = a.dout + slice, *k = a.k + slice, *v = a.v + slice;
+  for (int r16 = rlo + 16 * lw; r16 < bl; r16 += 64) {
+    int lr0 = slot + r16;
+    lr0 = lr0 >= RR ? lr0 - RR : lr0;
+#pragma unroll
+    for (int u = 0; u < IPB; ++u) {
+      const int r = r16 + u * RPI + rl;
+      const int sw = 8 * (pp ^ seg_swizzle<D>(lr0 + u * RPI + rl));
+      const int qo = min(max(qbase + r, 0), last) * fs + sw;
+      const int ko = min(max(kbase + r, 0), last) * fs + sw;
+      const int dst = (lr0 + u * RPI) * D;
+      __builtin_amdgcn_global_load_lds(q + qo, ring + dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(dout + qo, ring + RR * D + dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(k + ko, ring + 2 * RR * D + dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(v + ko, ring + 3 * RR * D + dst, 16, 0, 0);
+    }
+  }
+}
+
+// out and dout rows and lse values of loader lw's blocks of the same rows.
+template <int D, int SEG>
+__device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor<1>& cur, int rlo, int bl, int lw,
+                                               int lane, RingRegs<D, SEG>& rg) {
+  using R = RingRegs<D, SEG>;
+  const int col = lane & 15, g = lane >> 4;
+  const int fs = a.H * D;
+  const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
+  const int qbase = cur.tile * kC - a.La, last = cur.len - 1;
+  const uint16_t *o = a.o + slice, *dout = a.dout + slice;
+  const float* lse = a.lse + (static_cast<size_t>(cur.b) * a.H + cur.h) * a.T;
+#pragma unroll
+  for (int jj = 0; jj < R::BPL; ++jj) {
+    const int r16 = rlo + 16 * (lw + 4 * jj);
+    if (r16 < bl) {
+      const int fr = min(max(qbase + r16 + col, 0), last);
+#pragma unroll
+      for (int s = 0; s < R::NS; ++s) {
+        rg.of[jj][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
+        rg.df[jj][s] = __builtin_bit_cast(bf16x8, ld16(dout + (fr * fs + 32 * s + 8 * g)));
+      }
+      rg.lse[jj] = lse[fr];
+    }
+  }
+}
+
+// -D and lse log2(e) of those rows into the statistics rings (+inf for rows
+// outside the sequence).
+template <int D, int SEG>
+__device__ __forceinline__ void ring_stats(const RingRegs<D, SEG>& rg, float* ndn, float* lse2, int slot, int qbase,
+                                           int len, int rlo, int bl, int lw, int lane) {
+  using R = RingRegs<D, SEG>;
+  constexpr int RR = 2 * SEG;
+  const int col = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int jj = 0; jj < R::BPL; ++jj) {
+    const int r16 = rlo + 16 * (lw + 4 * jj);
+    if (r16 < bl) {
+      f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < R::NS; ++s)
+        dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rg.df[jj][s], rg.of[jj][s], dd, 0, 0, 0);
+      // the diagonal entry of row col sits in lane g = col / 4, element col % 4
+      const int e = col & 3;
+      const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
+      if ((col >> 2) == g) {
+        int lr = slot + r16 + col;
+        lr = lr >= RR ? lr - RR : lr;
+        const int fr = qbase + r16 + col;
+        ndn[lr] = -dg;
+        lse2[lr] = (fr >= 0 && fr < len) ? rg.lse[jj] * kLog2e : __builtin_huge_valf();
+      }
+    }
+  }
+}
+
+// Workgroup barrier for a wave whose direct copies may still be in flight:
+// waits for its own LDS accesses only (a release fence would also wait for
+// the copies, which are LDS writes).
+__device__ __forceinline__ void barrier_lgkm() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
+// transposed accumulators (lane (g, col): features 16 i + 4 g .. + 3 of row
+// col) through a 16 x D LDS block, whose 16-byte pieces are permuted per row
+// so that both the 8-byte writes and the full-row reads spread over the banks.
+template <int D>
+__device__ __forceinline__ void store_rows_staged(uint16_t* stage, uint16_t* dst, int fs, int r0, int nrows,
+                                                  const f32x4* acc, float mul, bool valid, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR;
+  const int g = lane >> 4, col = lane & 15;
+  const int fw = (col ^ (col >> 3)) & (CPR - 1);
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) {
+    u32x2 pk;
+    pk[0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    pk[1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
+    st8(stage + col * D + 8 * ((2 * i + (g >> 1)) ^ fw) + 4 * (g & 1), pk);
+  }
+#pragma unroll
+  for (int h = 0; h < 16 / RPI; ++h) {
+    const int rr = h * RPI + lane / CPR, c = lane % CPR;
+    const int fr = (rr ^ (rr >> 3)) & (CPR - 1);
+    const u32x4 v = ld16(stage + rr * D + 8 * (c ^ fr));
+    if (rr < nrows) st16(dst + (r0 + rr) * fs + 8 * c, v);
+  }
+}
+
+template <int D, int SEG>
+__global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
+  constexpr int NB = D / 16, RR = 2 * SEG;
+  static_assert(RR % 32 == 0, "the swizzle pattern must survive the wrap of the ring");
+  // q, dout, k, v rings, then the -D and lse log2(e) rings of the query band
+  __shared__ __attribute__((aligned(16))) uint16_t s_ring[4 * RR * D];
+  __shared__ __attribute__((aligned(16))) float s_stat[2 * RR];
+  float* const s_ndn = s_stat;
+  float* const s_lse2 = s_stat + RR;
+
+  const int G = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.T, H = a.H, Lb = a.Lb, La = a.La, fs = H * D;
+  const int nblk = (16 + Lb + La + kSub - 1) / kSub;  // sub-blocks per wave
+  const int bl = 48 + kSub * nblk;                     // band rows of a tile (<= SEG)
+  const SeqTable<1> st(a.lengths, a.B, T, H, lane);
+  const int nsteps = st.total();
+  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * nsteps / G);
+  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
+
+  if (w >= 8) {
+    const int lw = w - 8;
+    if (g0 >= g1) return;
+    RingRegs<D, SEG> rg;
+    TileCursor<1> cur;  // tile t
+    cur.seek(st, g0);
+    int slot = 0, rlo = 0;  // its ring slot and first new band row
+    ring_copy<D, SEG>(a, cur, s_ring, slot, 0, bl, lw, lane);
+    ring_load_regs<D, SEG>(a, cur, 0, bl, lw, lane, rg);
+    for (int t = g0; t < g1; ++t) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): tile t's copies and loads are in
+      ring_stats<D, SEG>(rg, s_ndn, s_lse2, slot, cur.tile * kC - La, cur.len, rlo, bl, lw, lane);
+      barrier_lgkm();  // A: tile t is complete in the rings
+      if (t + 1 < g1) {
+        cur.next(st, H, a.B);
+        // a tile that continues its predecessor needs only its last 64 band
+        // rows; one that starts a (sequence, head) goes behind tile t's band
+        const int inc = cur.tile > 0 ? kC : bl;
+        slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+        rlo = cur.tile > 0 ? bl - kC : 0;
+        ring_copy<D, SEG>(a, cur, s_ring, slot, rlo, bl, lw, lane);
+        ring_load_regs<D, SEG>(a, cur, rlo, bl, lw, lane, rg);
+      }
+      // B: the compute waves are done with the bands of tile t
+      __builtin_amdgcn_s_barrier();
+    }
+    return;
+  }
+
+  // compute waves: first the tiles wholly past a sequence's end
+  {
+    const int nslot = a.B * H * a.ntiles;
+    for (int p = blockIdx.x; p < nslot; p += G) {
+      const int tile = p % a.ntiles, bh = p / a.ntiles;
+      const int b = bh / H, h = bh % H;
+      const int f0 = tile * kC;
+      if (f0 < st.len(b)) continue;
+      zero_rows<D, 512>(a.dk, a.dv, b, h, T, H, f0, min(f0 + kC, T), tid);
+      zero_rows<D, 512>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
+    }
+  }
+  if (g0 >= g1) return;
+  const int col = lane & 15, wq = w & 3;
+  TileCursor<1> cur;
+  cur.seek(st, g0);
+  int slot = 0;
+  for (int t = g0; t < g1; ++t) {
+    lds_barrier();  // A: tile t is in the rings
+    const int len = cur.len, f0 = cur.tile * kC;
+    const BwdBands<D, RR> bands{s_ring, s_ring + RR * D, s_ring + 2 * RR * D, s_ring + 3 * RR * D,
+                                s_ndn, s_lse2, f0 - La, f0 - Lb, slot};
+    const int r0 = f0 + 16 * wq;
+    const bool valid = r0 + col < len;
+    const int nrows = min(16, T - r0);
+    const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
+    // the first 64 band rows of tile t are not part of tile t + 1: after
+    // barrier B each wave stages its output rows in a 16-row block of them
+    int lr = slot + 16 * wq;
+    lr = lr >= RR ? lr - RR : lr;
+    if (w < 4) {
+      f32x4 adv[NB], adk[NB];
+      bwd_key_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
+      lds_barrier();  // B
+      store_rows_staged<D>(s_ring + lr * D, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+      store_rows_staged<D>(s_ring + (RR + lr) * D, a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
+    } else {
+      f32x4 aq[NB];
+      bwd_query_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, aq);
+      lds_barrier();  // B
+      store_rows_staged<D>(s_ring + (2 * RR + lr) * D, a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
+    }
+    cur.next(st, H, a.B);
+    const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;
+    slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+  }
+}
 
 hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   BwdDev d;
@@ -741,7 +1056,12 @@ hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   if (48 + kSub * nblk <= seg_rows) {
     // both sweeps fit one segment: one workgroup per tile
     const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
-    if (a.d == 64)
+    if (a.B <= kPersistMaxB) {
+      if (a.d == 64)
+        hipLaunchKernelGGL((sa_bwd_persist_kernel<64, Seg<64>::kRows>), dim3(compute_units()), dim3(768), 0, stream, d);
+      else
+        hipLaunchKernelGGL((sa_bwd_persist_kernel<32, Seg<32>::kRows>), dim3(compute_units()), dim3(768), 0, stream, d);
+    } else if (a.d == 64)
       hipLaunchKernelGGL(sa_bwd_tile_kernel<64>, dim3(grid), dim3(2 * kThreads), 0, stream, d);
     else
       hipLaunchKernelGGL(sa_bwd_tile_kernel<32>, dim3(grid), dim3(2 * kThreads), 0, stream, d);

@@ -619,6 +619,169 @@ __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
     lse_bh[jb][t] = valid ? (m + log2f(lsum)) * kLn2 : kNegInf;
 }
 
+// ---------------------------------------------------------------------------
+// Persistent bfloat16 SA forward (one output, one band). The work is a list of
+// steps in (sequence, head, tile) order, a step being two consecutive 64-query
+// tiles of one (sequence, head) (or its odd last tile); one workgroup per
+// compute unit walks a contiguous, equal share of it with a producer/consumer
+// split:
+//   * waves 8 and 9 (the loaders) only issue direct global->LDS copies: the
+//     key and value band shared by the step's two tiles (band row r = frame
+//     f0 + lo + r, rows outside the sequence clamped to its first or last
+//     frame, so they hold finite data outside every window) and the step's
+//     128 query rows. Their memory counters hold nothing but these copies,
+//     so waiting for a step's data never waits for stores of earlier steps;
+//   * waves 0-3 compute the step's first tile and waves 4-7 its second (16
+//     queries each), reading only LDS, and store the outputs. They never
+//     wait for their stores, which a workgroup that ends after each tile
+//     would do (a wave's end waits for its outstanding memory operations).
+// Two buffers alternate: while the compute waves work on step s, the loaders
+// fill the other buffer with step s + 1. One workgroup barrier per step hands
+// the buffers over. In a step of one tile the second group idles.
+struct PairFwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;
+  float* lse;
+  int lo, hi;   // window t + lo .. t + hi
+  int nblk;     // sub-blocks of a wave's window
+  int B, T, H;
+  int ntiles;   // 64-query tiles per sequence of T frames
+  const int32_t* lengths;
+  float scale_log2;
+};
+
+// The loaders' copies of one step: band rows [0, SEG2) and 128 query rows into
+// buf; loader wave lw (0 or 1) takes every other copy.
+template <int D, int SEG2>
+__device__ __forceinline__ void pair_issue(const PairFwdArgs& a, const TileCursor<2>& cur, uint16_t* buf, int lw,
+                                           int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR;
+  const int rl = lane / CPR, pp = lane % CPR;
+  const int fs = a.H * D;
+  const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
+  const uint16_t* kp = static_cast<const uint16_t*>(a.k) + slice;
+  const uint16_t* vp = static_cast<const uint16_t*>(a.v) + slice;
+  const uint16_t* qp = static_cast<const uint16_t*>(a.q) + slice;
+  const int f0 = cur.tile * kTq, bbase = f0 + a.lo, last = cur.len - 1;
+#pragma unroll 2
+  for (int I = lw; I < SEG2 / RPI; I += 2) {
+    const int r = I * RPI + rl;
+    const int off = min(max(bbase + r, 0), last) * fs + 8 * (pp ^ seg_swizzle<D>(r));
+    __builtin_amdgcn_global_load_lds(kp + off, buf + I * 512, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vp + off, buf + SEG2 * D + I * 512, 16, 0, 0);
+  }
+#pragma unroll 2
+  for (int I = lw; I < 2 * kTq / RPI; I += 2) {
+    const int r = I * RPI + rl;
+    __builtin_amdgcn_global_load_lds(qp + (min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r))),
+                                     buf + 2 * SEG2 * D + I * 512, 16, 0, 0);
+  }
+}
+
+template <int D, int SEG2, int NBM>
+__global__ __launch_bounds__(640) void band_fwd_pair_kernel(PairFwdArgs a) {
+  constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
+  constexpr int BUF = (2 * SEG2 + 2 * kTq) * D;  // one buffer: K band, V band, 128 query rows
+  static_assert(kTq + 48 + kSub * NBM <= SEG2, "the second tile's sub-blocks must stay inside the band");
+  __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * BUF];
+  __shared__ __attribute__((aligned(16))) uint16_t s_stage[8 * stage_elems<D>()];
+
+  const int G = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.T, H = a.H, fs = H * D;
+  const SeqTable<2> st(a.lengths, a.B, T, H, lane);
+  const int nsteps = st.total();
+  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * nsteps / G);
+  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
+
+  if (w >= 8) {
+    // loaders: step s + 1 is copied while step s is computed
+    const int lw = w - 8;
+    if (g0 >= g1) return;
+    TileCursor<2> cur;
+    cur.seek(st, g0);
+    int g = g0, s = 0;
+    pair_issue<D, SEG2>(a, cur, s_buf, lw, lane);
+    while (g < g1) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this step's copies are in
+      // a plain barrier: this wave reads no LDS and its copies are ordered by
+      // the wait above (a fence would add nothing but the wait)
+      __builtin_amdgcn_s_barrier();
+      ++g;
+      cur.next(st, H, a.B);
+      ++s;
+      if (g < g1) pair_issue<D, SEG2>(a, cur, s_buf + (s & 1) * BUF, lw, lane);
+    }
+    return;
+  }
+
+  // compute waves: first the tiles wholly past a sequence's end
+  {
+    const int nslot = a.B * a.H * a.ntiles;
+    for (int p = blockIdx.x; p < nslot; p += G) {
+      const int tile = p % a.ntiles, bh = p / a.ntiles;
+      const int b = bh / a.H, h = bh % a.H;
+      const int len = st.len(b);
+      const int f0 = tile * kTq;
+      if (f0 < len) continue;
+      const size_t slice = row_index(b, 0, h, T, H, D);
+      uint16_t* out = static_cast<uint16_t*>(a.out) + slice;
+      const int r1 = min(f0 + kTq, T);
+      for (int e = tid; e < (r1 - f0) * CPR; e += 512) st16(out + (f0 + e / CPR) * fs + 8 * (e % CPR), kZero16);
+      if (a.lse) {
+        float* lp = a.lse + (static_cast<size_t>(b) * H + h) * T;
+        for (int r = f0 + tid; r < r1; r += 512) lp[r] = kNegInf;
+      }
+    }
+  }
+  if (g0 >= g1) return;
+  const int col = lane & 15, g = lane >> 4;
+  const int grp = w >> 2, wq = w & 3;  // tile of the step, wave within the tile
+  const float c2 = a.scale_log2;
+  uint16_t* stage = s_stage + w * stage_elems<D>();
+  TileCursor<2> cur;
+  cur.seek(st, g0);
+  int gi = g0, s = 0;
+  while (gi < g1) {
+    const int nst = cur.step_tiles();
+    lds_barrier();  // step s is in buffer s % 2
+    if (grp < nst) {
+      const uint16_t* buf = s_buf + (s & 1) * BUF;
+      const int len = cur.len;
+      const int fA = cur.tile * kTq, bbase = fA + a.lo;
+      const int r0 = fA + kTq * grp + 16 * wq;
+      const int t = r0 + col;
+      const bool valid = t < len;
+      const int wmax = min(r0 + 15, len - 1);
+      bf16x8 qf[NS];
+#pragma unroll
+      for (int k = 0; k < NS; ++k) qf[k] = seg_row8<D>(buf + 2 * SEG2 * D, kTq * grp + 16 * wq + col, 32 * k + 8 * g);
+      float lsum = 0.f;
+      f32x4 acc[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const WaveSeg<D> ws(buf, buf + SEG2 * D, lane, bbase, kTq * grp, a.nblk, a.lo, a.hi, r0, wmax, t, valid, len,
+                          wq);
+      f32x8 y[NBM];
+      float m = max_over_column(seg_scores<D, NBM>(ws, qf, c2, lane, y));
+      m = m == kNegInf ? 0.f : m;  // no key in the window (past the sequence's end)
+      seg_weights_pv<D, NBM>(ws, y, m, acc, lsum);
+      lsum = sum_over_column(lsum);
+      const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
+      store_tile_rows<D>(stage, static_cast<uint16_t*>(a.out) + slice, fs, r0, min(16, T - r0), acc,
+                         valid ? 1.f / lsum : 0.f, valid, lane);
+      if (a.lse && g == 0 && t < T)
+        a.lse[(static_cast<size_t>(cur.b) * H + cur.h) * T + t] = valid ? (m + log2f(lsum)) * kLn2 : kNegInf;
+    }
+    ++gi;
+    cur.next(st, H, a.B);
+    ++s;
+  }
+}
+
 DevSeg to_dev(const BandSegment& s) { return DevSeg{s.k, s.v, s.lo_off, s.hi_off}; }
 
 DevJob to_dev(const BandJob& j) {
@@ -639,6 +802,11 @@ constexpr int kSaRows = 144;                     // SA: 48 + 32 * 3 (Lb + La <= 
 constexpr int kLlsaRows0 = 152, kLlsaRows1 = 88;  // LLSA: both outputs, Lb = 64, La = 8 and smaller
 // Sub-blocks a wave holds in registers per band (the window of one band).
 constexpr int kMaxBlocks0 = 3, kMaxBlocks1 = 1;
+
+// The persistent kernel holds the sequence lengths in the lanes of a wave;
+// past this many sequences the tile kernel is used instead.
+constexpr int kPersistMaxB = 64;
+constexpr int kPairRows = 208;  // band rows of a two-tile step: 64 + 48 + 32 * 3
 
 // Lays the jobs' window segments onto tile-kernel bands (segment i of every job
 // reads band i). Returns false when a band would need more than its rows.
@@ -691,6 +859,26 @@ bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
   const int grid = xcd_slice_grid(a.B * a.H, d.ntiles);
   if (a.njobs == 1 && a.job[0].nseg == 1) {
     if (!plan_tile(a, X * kSaRows, 0, d)) return false;
+    if (a.B <= kPersistMaxB) {
+      PairFwdArgs p;
+      p.q = a.job[0].q;
+      p.k = a.job[0].seg[0].k;
+      p.v = a.job[0].seg[0].v;
+      p.out = a.job[0].out;
+      p.lse = a.job[0].lse;
+      p.lo = a.job[0].seg[0].lo_off;
+      p.hi = a.job[0].seg[0].hi_off;
+      p.nblk = d.job[0].seg[0].nblk;
+      p.B = a.B;
+      p.T = a.T;
+      p.H = a.H;
+      p.ntiles = d.ntiles;
+      p.lengths = a.lengths;
+      p.scale_log2 = d.scale_log2;
+      hipLaunchKernelGGL((band_fwd_pair_kernel<D, kPairRows, kMaxBlocks0>), dim3(compute_units()), dim3(640), 0,
+                         stream, p);
+      return true;
+    }
     hipLaunchKernelGGL((band_fwd_tile_kernel<D, 1, X * kSaRows, 0, 3, 0>), dim3(grid), dim3(256), 0, stream, d);
     return true;
   }

@@ -76,6 +76,22 @@ size_t elem_size(int dtype) { return dtype == SA_BF16 ? 2 : 4; }
 
 }  // namespace
 
+namespace sa {
+
+int compute_units() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+}  // namespace sa
+
 extern "C" {
 
 int sa_abi_version(void) { return 1; }

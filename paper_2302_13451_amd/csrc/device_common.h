@@ -284,6 +284,67 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Frames per tile of the persistent kernels' work lists.
+constexpr int kTileFrames = 64;
+
+// The work of up to 64 sequences, held in one wave's lanes (lane b: sequence
+// b), so that walking it needs no memory access: one vector load of the
+// lengths and a lane prefix sum. The work is a list of steps in (sequence,
+// head, tile) order, a step being TPS consecutive 64-frame tiles of one
+// (sequence, head), or fewer at its end.
+template <int TPS>
+struct SeqTable {
+  int lenv;   // this lane's sequence length (0 past the last sequence)
+  int ntv;    // its 64-frame tiles
+  int incl;   // steps of sequences 0 .. lane, all heads
+  __device__ __forceinline__ SeqTable(const int32_t* lengths, int B, int T, int H, int lane) {
+    int L = 0;
+    if (lane < B) L = lengths ? lengths[lane] : T;
+    lenv = L < 0 ? 0 : (L > T ? T : L);
+    ntv = (lenv + kTileFrames - 1) / kTileFrames;
+    incl = H * ((ntv + TPS - 1) / TPS);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int x = __shfl_up(incl, o);
+      if (lane >= o) incl += x;
+    }
+  }
+  __device__ __forceinline__ int total() const { return __builtin_amdgcn_readlane(incl, 63); }
+  __device__ __forceinline__ int len(int b) const { return __builtin_amdgcn_readlane(lenv, b); }
+  __device__ __forceinline__ int nt(int b) const { return __builtin_amdgcn_readlane(ntv, b); }
+  __device__ __forceinline__ int before(int b) const { return b == 0 ? 0 : __builtin_amdgcn_readlane(incl, b - 1); }
+};
+
+// Cursor over the steps of a SeqTable (all fields wave-uniform).
+template <int TPS>
+struct TileCursor {
+  int b, h, tile, nt, len;
+  __device__ __forceinline__ void seek(const SeqTable<TPS>& st, int g) {
+    // sequences whose steps all come before g: incl <= g
+    b = __builtin_popcountll(__ballot(st.incl <= g));
+    nt = st.nt(b);
+    len = st.len(b);
+    const int sps = (nt + TPS - 1) / TPS;  // steps per (sequence, head)
+    const int local = g - st.before(b);
+    h = local / sps;
+    tile = TPS * (local - h * sps);
+  }
+  // tiles of the current step
+  __device__ __forceinline__ int step_tiles() const { return nt - tile < TPS ? nt - tile : TPS; }
+  __device__ __forceinline__ void next(const SeqTable<TPS>& st, int H, int B) {
+    tile += TPS;
+    if (tile < nt) return;
+    tile = 0;
+    if (++h < H) return;
+    h = 0;
+    do {
+      ++b;
+      nt = b < B ? st.nt(b) : 1;
+    } while (nt == 0);
+    len = b < B ? st.len(b) : 1;
+  }
+};
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2): block bid runs on XCD bid % 8. XCD x walks the (sequence, head) slices
 // x, x + 8, x + 16, ... and, within a slice, its per_slice work items in

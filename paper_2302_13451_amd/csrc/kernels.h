@@ -9,6 +9,10 @@ namespace sa {
 
 enum ElemType { kF32 = 0, kBF16 = 1 };
 
+// Compute units of the current device: the grid of the persistent kernels,
+// one workgroup per compute unit.
+int compute_units();
+
 // One segment of a query's window: frames t + lo_off .. t + hi_off (clipped to
 // the valid frames), with keys and values read from k / v.
 struct BandSegment {

@@ -53,6 +53,10 @@ def test_config1_shape_float32(oracle_mod):
     (2, 260, 2, 64, 72, 8, (70, 260)),
     (2, 300, 2, 64, 100, 20, (50, 300)),
     (1, 600, 2, 32, 250, 60, (300, 600)),
+    # empty sequences between others, and more sequences than a wave has lanes
+    (6, 130, 2, 64, 30, 8, (0, 130, 0, 64, 1, 0)),
+    (66, 70, 1, 64, 20, 4, (0, 70)),
+    (65, 50, 1, 32, 30, 30, (1, 50)),
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_backward_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):

@@ -44,6 +44,10 @@ SHAPES = [
     (2, 190, 1, 64, 70, 0, (64, 190)),
     (1, 40, 2, 64, 5, 3, "full"),
     (2, 97, 2, 32, 200, 200, (30, 97)),
+    # empty sequences between others, and more sequences than a wave has lanes
+    (6, 130, 2, 64, 30, 8, (0, 130, 0, 64, 1, 0)),
+    (66, 70, 1, 64, 20, 4, (0, 70)),
+    (65, 50, 1, 32, 30, 30, (1, 50)),
 ]
 
 
