@@ -908,28 +908,39 @@ __device__ __forceinline__ void barrier_lgkm() {
 }
 
 // Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
-// transposed accumulators (lane (g, col): features 16 i + 4 g .. + 3 of row
-// col) through a 16 x D LDS block, whose 16-byte pieces are permuted per row
-// so that both the 8-byte writes and the full-row reads spread over the banks.
+// transposed accumulators, lane (g, col) holding features 16 i + 4 g .. + 3
+// of row col. Lanes g and g ^ 1 swap 4-feature pieces (permlane16 swap), so
+// that each lane holds whole 8-feature pieces: even g those of i = 0, 2, ...,
+// odd g those of i = 1, 3, ... Each store then writes 64 contiguous bytes of
+// 16 rows (whole rows for D = 32).
 template <int D>
-__device__ __forceinline__ void store_rows_staged(uint16_t* stage, uint16_t* dst, int fs, int r0, int nrows,
-                                                  const f32x4* acc, float mul, bool valid, int lane) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR;
+__device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
+                                                  float mul, bool valid, int lane) {
+  constexpr int NB = D / 16;
   const int g = lane >> 4, col = lane & 15;
-  const int fw = (col ^ (col >> 3)) & (CPR - 1);
+  const bool even = (g & 1) == 0;
+  u32x2 p[NB];
 #pragma unroll
-  for (int i = 0; i < D / 16; ++i) {
-    u32x2 pk;
-    pk[0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
-    pk[1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
-    st8(stage + col * D + 8 * ((2 * i + (g >> 1)) ^ fw) + 4 * (g & 1), pk);
+  for (int i = 0; i < NB; ++i) {
+    p[i][0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    p[i][1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
   }
+  // feature offset of piece j of this lane: 32 j + {0, 16, 8, 24}[g]
+  const int f0 = 8 * (g >> 1) + (even ? 0 : 16);
+  uint16_t* row = dst + (r0 + col) * fs + f0;
 #pragma unroll
-  for (int h = 0; h < 16 / RPI; ++h) {
-    const int rr = h * RPI + lane / CPR, c = lane % CPR;
-    const int fr = (rr ^ (rr >> 3)) & (CPR - 1);
-    const u32x4 v = ld16(stage + rr * D + 8 * (c ^ fr));
-    if (rr < nrows) st16(dst + (r0 + rr) * fs + 8 * c, v);
+  for (int j = 0; j < NB / 2; ++j) {
+    u32x4 v;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // even lanes send piece 2j + 1, odd lanes piece 2j
+      const unsigned send = even ? p[2 * j + 1][h] : p[2 * j][h];
+      const auto r = __builtin_amdgcn_permlane16_swap(send, send, false, false);
+      const unsigned got = even ? r[1] : r[0];
+      v[h] = even ? p[2 * j][h] : got;
+      v[2 + h] = even ? got : p[2 * j + 1][h];
+    }
+    if (col < nrows) st16(row + 32 * j, v);
   }
 }
 
@@ -961,12 +972,14 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
     TileCursor<1> cur;  // tile t
     cur.seek(st, g0);
     int slot = 0, rlo = 0;  // its ring slot and first new band row
-    ring_copy<D, SEG>(a, cur, s_ring, slot, 0, bl, lw, lane);
     ring_load_regs<D, SEG>(a, cur, 0, bl, lw, lane, rg);
+    ring_copy<D, SEG>(a, cur, s_ring, slot, 0, bl, lw, lane);
     for (int t = g0; t < g1; ++t) {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): tile t's copies and loads are in
       ring_stats<D, SEG>(rg, s_ndn, s_lse2, slot, cur.tile * kC - La, cur.len, rlo, bl, lw, lane);
-      barrier_lgkm();  // A: tile t is complete in the rings
+      // tile t is complete in the rings, and the compute waves are done with
+      // tile t - 1, whose rows the copies of tile t + 1 may reuse
+      barrier_lgkm();
       if (t + 1 < g1) {
         cur.next(st, H, a.B);
         // a tile that continues its predecessor needs only its last 64 band
@@ -974,11 +987,11 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
         const int inc = cur.tile > 0 ? kC : bl;
         slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
         rlo = cur.tile > 0 ? bl - kC : 0;
-        ring_copy<D, SEG>(a, cur, s_ring, slot, rlo, bl, lw, lane);
+        // register loads first: the compiler orders them after every older
+        // load that wrote the same registers
         ring_load_regs<D, SEG>(a, cur, rlo, bl, lw, lane, rg);
+        ring_copy<D, SEG>(a, cur, s_ring, slot, rlo, bl, lw, lane);
       }
-      // B: the compute waves are done with the bands of tile t
-      __builtin_amdgcn_s_barrier();
     }
     return;
   }
@@ -1001,7 +1014,7 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   cur.seek(st, g0);
   int slot = 0;
   for (int t = g0; t < g1; ++t) {
-    lds_barrier();  // A: tile t is in the rings
+    lds_barrier();  // tile t is in the rings; the loaders then copy tile t + 1
     const int len = cur.len, f0 = cur.tile * kC;
     const BwdBands<D, RR> bands{s_ring, s_ring + RR * D, s_ring + 2 * RR * D, s_ring + 3 * RR * D,
                                 s_ndn, s_lse2, f0 - La, f0 - Lb, slot};
@@ -1009,21 +1022,15 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
     const bool valid = r0 + col < len;
     const int nrows = min(16, T - r0);
     const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
-    // the first 64 band rows of tile t are not part of tile t + 1: after
-    // barrier B each wave stages its output rows in a 16-row block of them
-    int lr = slot + 16 * wq;
-    lr = lr >= RR ? lr - RR : lr;
     if (w < 4) {
       f32x4 adv[NB], adk[NB];
       bwd_key_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
-      lds_barrier();  // B
-      store_rows_staged<D>(s_ring + lr * D, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
-      store_rows_staged<D>(s_ring + (RR + lr) * D, a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
+      store_rows_direct<D>(a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+      store_rows_direct<D>(a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
     } else {
       f32x4 aq[NB];
       bwd_query_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, aq);
-      lds_barrier();  // B
-      store_rows_staged<D>(s_ring + (2 * RR + lr) * D, a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
+      store_rows_direct<D>(a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
     }
     cur.next(st, H, a.B);
     const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;
