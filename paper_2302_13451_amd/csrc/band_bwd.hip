@@ -485,13 +485,6 @@ struct BwdBands {
   }
 };
 
-// Element offset o of an LDS row taken modulo RR rows (o < 2 RR D).
-template <int D, int RR>
-__device__ __forceinline__ int ring_wrap(int o) {
-  const unsigned u = static_cast<unsigned>(o), w = u - static_cast<unsigned>(RR * D);
-  return static_cast<int>(u < w ? u : w);
-}
-
 // Per-lane operand offsets of the wave's sub-blocks in the bands: the
 // sub-block at band row sb (sb = 16 wq + 32 m) sits at LDS rows slot0 + sb ..,
 // whose swizzle pattern repeats every 32 rows.
@@ -907,43 +900,6 @@ __device__ __forceinline__ void barrier_lgkm() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
-// transposed accumulators, lane (g, col) holding features 16 i + 4 g .. + 3
-// of row col. Lanes g and g ^ 1 swap 4-feature pieces (permlane16 swap), so
-// that each lane holds whole 8-feature pieces: even g those of i = 0, 2, ...,
-// odd g those of i = 1, 3, ... Each store then writes 64 contiguous bytes of
-// 16 rows (whole rows for D = 32).
-template <int D>
-__device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
-                                                  float mul, bool valid, int lane) {
-  constexpr int NB = D / 16;
-  const int g = lane >> 4, col = lane & 15;
-  const bool even = (g & 1) == 0;
-  u32x2 p[NB];
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    p[i][0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
-    p[i][1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
-  }
-  // feature offset of piece j of this lane: 32 j + {0, 16, 8, 24}[g]
-  const int f0 = 8 * (g >> 1) + (even ? 0 : 16);
-  uint16_t* row = dst + (r0 + col) * fs + f0;
-#pragma unroll
-  for (int j = 0; j < NB / 2; ++j) {
-    u32x4 v;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      // even lanes send piece 2j + 1, odd lanes piece 2j
-      const unsigned send = even ? p[2 * j + 1][h] : p[2 * j][h];
-      const auto r = __builtin_amdgcn_permlane16_swap(send, send, false, false);
-      const unsigned got = even ? r[1] : r[0];
-      v[h] = even ? p[2 * j][h] : got;
-      v[2 + h] = even ? got : p[2 * j + 1][h];
-    }
-    if (col < nrows) st16(row + 32 * j, v);
-  }
-}
-
 template <int D, int SEG>
 __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   constexpr int NB = D / 16, RR = 2 * SEG;
@@ -996,14 +952,16 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
     return;
   }
 
-  // compute waves: first the tiles wholly past a sequence's end
+  // compute waves: first this workgroup's share of the tiles wholly past a
+  // sequence's end
   {
-    const int nslot = a.B * H * a.ntiles;
-    for (int p = blockIdx.x; p < nslot; p += G) {
-      const int tile = p % a.ntiles, bh = p / a.ntiles;
-      const int b = bh / H, h = bh % H;
+    const PadTable pt(st, a.B, H, a.ntiles, lane);
+    const int np = pt.total();
+    const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+    for (int i = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); i < p1; ++i) {
+      int b, h, tile;
+      pt.item(i, a.ntiles, b, h, tile);
       const int f0 = tile * kC;
-      if (f0 < st.len(b)) continue;
       zero_rows<D, 512>(a.dk, a.dv, b, h, T, H, f0, min(f0 + kC, T), tid);
       zero_rows<D, 512>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
     }

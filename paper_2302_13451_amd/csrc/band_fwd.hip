@@ -395,11 +395,14 @@ __device__ __forceinline__ float sum_over_column(float x) {
 
 // A wave's window segment inside a staged band: its 16 queries r0 .. r0 + 15
 // (this lane's: t) see frames t + lo .. t + hi, held by band rows from sb0 on.
-template <int D>
+// With RR > 0 the band is a ring of RR rows (a multiple of 32): band row r
+// sits in LDS row (slot0 + r) mod RR, slot0 a multiple of 16.
+template <int D, int RR = 0>
 struct WaveSeg {
   const uint16_t* Xk;
   const uint16_t* Xv;
-  BlockOffsets<D> bo;  // operand offsets of the sub-blocks at sb0 + 32 m
+  BlockOffsets<D> bo;  // operand offsets of the sub-blocks at LDS row x0 + 32 m
+  int x0;              // (unwrapped) LDS row of the wave's first sub-block
   int sb0;             // band row of the wave's first sub-block
   int kb0;             // its frame
   int nblk;            // sub-blocks of the wave's window
@@ -408,9 +411,11 @@ struct WaveSeg {
   unsigned qwidth;     // ... and the width of its window
   int ilo, ihi;        // frames inside the window of every valid query of the wave
   __device__ __forceinline__ WaveSeg(const uint16_t* k, const uint16_t* v, int lane, int bbase, int shift, int nb,
-                                     int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq)
-      : Xk(k), Xv(v), bo(lane, 16 * wq + shift) {
+                                     int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq,
+                                     int slot0 = 0)
+      : Xk(k), Xv(v), bo(lane, (slot0 + 16 * wq + shift) & (RR > 0 ? 16 : ~0)) {
     sb0 = 16 * wq + shift;
+    x0 = slot0 + sb0;
     kb0 = bbase + sb0;
     nblk = lo <= hi ? nb : 0;
     wlo = max(0, r0 + lo);
@@ -422,6 +427,16 @@ struct WaveSeg {
     ilo = max(0, wmax + lo);
     ihi = min(len - 1, r0 + hi);
   }
+  // operand offsets of sub-block m
+  __device__ __forceinline__ void at(int m, int& oa, int& oc, int& ota, int& otc) const {
+    bo.at(x0 + kSub * m, oa, oc, ota, otc);
+    if constexpr (RR > 0) {
+      oa = ring_wrap<D, RR>(oa);
+      oc = ring_wrap<D, RR>(oc);
+      ota = ring_wrap<D, RR>(ota);
+      otc = ring_wrap<D, RR>(otc);
+    }
+  }
 };
 
 // First pass over a segment: the scaled scores y = (q . k) log2(e) / sqrt(d)
@@ -432,15 +447,15 @@ struct WaveSeg {
 // branches, so the LDS reads and MFMAs of different sub-blocks overlap: the
 // band must hold finite data in every row they touch (rows outside the
 // sequence, or past the window, are masked). Returns the lane's maximum.
-template <int D, int NBM>
-__device__ __forceinline__ float seg_scores(const WaveSeg<D>& s, const bf16x8* qf, float c2, int lane, f32x8* y) {
+template <int D, int NBM, int RR>
+__device__ __forceinline__ float seg_scores(const WaveSeg<D, RR>& s, const bf16x8* qf, float c2, int lane, f32x8* y) {
   constexpr int NS = D / 32;
   const int g = lane >> 4;
   bf16x8 ka[NBM][2 * NS];
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
     int oa, oc, ota, otc;
-    s.bo.at(s.sb0 + kSub * m, oa, oc, ota, otc);
+    s.at(m, oa, oc, ota, otc);
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
       ka[m][2 * k] = lds_row8(s.Xk + (oa ^ (32 * k)));
@@ -476,8 +491,8 @@ __device__ __forceinline__ float seg_scores(const WaveSeg<D>& s, const bf16x8* q
 // Second pass: weights p = 2^(y - mx), their float sum, and O^T += V^T P^T
 // with the weights rounded to bfloat16 (lane (g, col) needs
 // V[kb + 8g + j][16 i + col], the transposing LDS read).
-template <int D, int NBM>
-__device__ __forceinline__ void seg_weights_pv(const WaveSeg<D>& s, const f32x8* y, float mx, f32x4* acc,
+template <int D, int NBM, int RR>
+__device__ __forceinline__ void seg_weights_pv(const WaveSeg<D, RR>& s, const f32x8* y, float mx, f32x4* acc,
                                                float& lsum) {
   constexpr int NB = D / 16;
   bf16x8 pf[NBM];
@@ -492,7 +507,7 @@ __device__ __forceinline__ void seg_weights_pv(const WaveSeg<D>& s, const f32x8*
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
     int oa, oc, ota, otc;
-    s.bo.at(s.sb0 + kSub * m, oa, oc, ota, otc);
+    s.at(m, oa, oc, ota, otc);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
       acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s.Xv, ota ^ (16 * i), otc ^ (16 * i)), pf[m], acc[i], 0, 0, 0);
@@ -620,24 +635,26 @@ __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Persistent bfloat16 SA forward (one output, one band). The work is a list of
-// steps in (sequence, head, tile) order, a step being two consecutive 64-query
-// tiles of one (sequence, head) (or its odd last tile); one workgroup per
-// compute unit walks a contiguous, equal share of it with a producer/consumer
-// split:
-//   * waves 8 and 9 (the loaders) only issue direct global->LDS copies: the
-//     key and value band shared by the step's two tiles (band row r = frame
-//     f0 + lo + r, rows outside the sequence clamped to its first or last
-//     frame, so they hold finite data outside every window) and the step's
-//     128 query rows. Their memory counters hold nothing but these copies,
-//     so waiting for a step's data never waits for stores of earlier steps;
+// Persistent bfloat16 SA forward (one output, one band) for up to 64
+// sequences. The work is the list of steps of two 64-query tiles of one
+// (sequence, head) (or its odd last tile); one workgroup per compute unit
+// walks a contiguous, equal share of it with a producer/consumer split:
+//   * waves 8 .. 15 (the loaders) only issue direct global->LDS copies: the
+//     key and value rows of the step's band (band row r = frame f0 + lo + r,
+//     frames outside the sequence clamped to its first or last one, so every
+//     row holds finite data, masked outside the windows) and its 128 query
+//     rows. The key and value bands live in LDS rings: a step that continues
+//     the previous one of its (sequence, head) shares all but 128 rows of its
+//     band with it and copies only those; a step that starts a (sequence,
+//     head) copies its whole band behind the previous one. Their memory
+//     counters hold nothing but these copies, so waiting for a step's data
+//     never waits for stores;
 //   * waves 0-3 compute the step's first tile and waves 4-7 its second (16
-//     queries each), reading only LDS, and store the outputs. They never
-//     wait for their stores, which a workgroup that ends after each tile
-//     would do (a wave's end waits for its outstanding memory operations).
-// Two buffers alternate: while the compute waves work on step s, the loaders
-// fill the other buffer with step s + 1. One workgroup barrier per step hands
-// the buffers over. In a step of one tile the second group idles.
+//     queries each), reading only LDS, and store the outputs straight from
+//     their registers.
+// While the compute waves work on step s the loaders copy step s + 1 into the
+// ring rows and query buffer that step s does not use; one workgroup barrier
+// per step hands them over. In a step of one tile the second group idles.
 struct PairFwdArgs {
   const void* q;
   const void* k;
@@ -645,19 +662,24 @@ struct PairFwdArgs {
   void* out;
   float* lse;
   int lo, hi;   // window t + lo .. t + hi
-  int nblk;     // sub-blocks of a wave's window
   int B, T, H;
   int ntiles;   // 64-query tiles per sequence of T frames
   const int32_t* lengths;
   float scale_log2;
 };
 
-// The loaders' copies of one step: band rows [0, SEG2) and 128 query rows into
-// buf; loader wave lw (0 or 1) takes every other copy.
-template <int D, int SEG2>
-__device__ __forceinline__ void pair_issue(const PairFwdArgs& a, const TileCursor<2>& cur, uint16_t* buf, int lw,
-                                           int lane) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR;
+constexpr int kFwdRingRows = 416;  // two whole two-tile bands (2 (64 + 48 + 32 * 3))
+constexpr int kFwdLoaders = 8;     // loader waves (after the eight compute waves)
+
+// The loaders' copies of one step: band rows [rlo, BL2) into ring rows
+// (slot + r) mod RR (16-row blocks, never split by the wrap) and the step's
+// 128 query rows into qbuf; loader lw of kFwdLoaders takes every
+// kFwdLoaders-th block. (The copy rate of a compute unit grows with the
+// number of waves that issue the copies, up to about eight.)
+template <int D, int BL2>
+__device__ __forceinline__ void ring_fwd_issue(const PairFwdArgs& a, const TileCursor<2>& cur, uint16_t* rk,
+                                               uint16_t* rv, uint16_t* qbuf, int slot, int rlo, int lw, int lane) {
+  constexpr int RR = kFwdRingRows, CPR = D / 8, RPI = 64 / CPR, IPB = 16 / RPI;
   const int rl = lane / CPR, pp = lane % CPR;
   const int fs = a.H * D;
   const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
@@ -665,28 +687,34 @@ __device__ __forceinline__ void pair_issue(const PairFwdArgs& a, const TileCurso
   const uint16_t* vp = static_cast<const uint16_t*>(a.v) + slice;
   const uint16_t* qp = static_cast<const uint16_t*>(a.q) + slice;
   const int f0 = cur.tile * kTq, bbase = f0 + a.lo, last = cur.len - 1;
-#pragma unroll 2
-  for (int I = lw; I < SEG2 / RPI; I += 2) {
-    const int r = I * RPI + rl;
-    const int off = min(max(bbase + r, 0), last) * fs + 8 * (pp ^ seg_swizzle<D>(r));
-    __builtin_amdgcn_global_load_lds(kp + off, buf + I * 512, 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(vp + off, buf + SEG2 * D + I * 512, 16, 0, 0);
+  for (int r16 = rlo + 16 * lw; r16 < BL2; r16 += 16 * kFwdLoaders) {
+    int lr0 = slot + r16;
+    lr0 = lr0 >= RR ? lr0 - RR : lr0;
+#pragma unroll
+    for (int u = 0; u < IPB; ++u) {
+      const int r = r16 + u * RPI + rl;
+      const int off = min(max(bbase + r, 0), last) * fs + 8 * (pp ^ seg_swizzle<D>(lr0 + u * RPI + rl));
+      const int dst = (lr0 + u * RPI) * D;
+      __builtin_amdgcn_global_load_lds(kp + off, rk + dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vp + off, rv + dst, 16, 0, 0);
+    }
   }
-#pragma unroll 2
-  for (int I = lw; I < 2 * kTq / RPI; I += 2) {
+  for (int I = lw; I < 2 * kTq / RPI; I += kFwdLoaders) {
     const int r = I * RPI + rl;
-    __builtin_amdgcn_global_load_lds(qp + (min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r))),
-                                     buf + 2 * SEG2 * D + I * 512, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(qp + (min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r))), qbuf + I * 512,
+                                     16, 0, 0);
   }
 }
 
-template <int D, int SEG2, int NBM>
-__global__ __launch_bounds__(640) void band_fwd_pair_kernel(PairFwdArgs a) {
+template <int D, int NBM>
+__global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(PairFwdArgs a) {
   constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
-  constexpr int BUF = (2 * SEG2 + 2 * kTq) * D;  // one buffer: K band, V band, 128 query rows
-  static_assert(kTq + 48 + kSub * NBM <= SEG2, "the second tile's sub-blocks must stay inside the band");
-  __shared__ __attribute__((aligned(16))) uint16_t s_buf[2 * BUF];
-  __shared__ __attribute__((aligned(16))) uint16_t s_stage[8 * stage_elems<D>()];
+  constexpr int RR = kFwdRingRows;
+  constexpr int BL2 = kTq + 48 + kSub * NBM;  // band rows of a two-tile step
+  static_assert(2 * BL2 <= RR && RR % 32 == 0, "a step's band and the next one must fit the ring");
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[RR * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[RR * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[2 * 2 * kTq * D];
 
   const int G = gridDim.x;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -698,35 +726,39 @@ __global__ __launch_bounds__(640) void band_fwd_pair_kernel(PairFwdArgs a) {
   const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
 
   if (w >= 8) {
-    // loaders: step s + 1 is copied while step s is computed
     const int lw = w - 8;
     if (g0 >= g1) return;
     TileCursor<2> cur;
     cur.seek(st, g0);
-    int g = g0, s = 0;
-    pair_issue<D, SEG2>(a, cur, s_buf, lw, lane);
-    while (g < g1) {
-      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this step's copies are in
+    int slot = 0;
+    ring_fwd_issue<D, BL2>(a, cur, s_k, s_v, s_q, slot, 0, lw, lane);
+    for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): step s is in
       // a plain barrier: this wave reads no LDS and its copies are ordered by
-      // the wait above (a fence would add nothing but the wait)
+      // the wait above (a fence would add nothing but the wait). After it the
+      // compute waves are done with step s - 1.
       __builtin_amdgcn_s_barrier();
-      ++g;
-      cur.next(st, H, a.B);
-      ++s;
-      if (g < g1) pair_issue<D, SEG2>(a, cur, s_buf + (s & 1) * BUF, lw, lane);
+      if (gi + 1 < g1) {
+        cur.next(st, H, a.B);
+        const int inc = cur.tile > 0 ? 2 * kTq : BL2;
+        slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+        ring_fwd_issue<D, BL2>(a, cur, s_k, s_v, s_q + ((s + 1) & 1) * 2 * kTq * D, slot,
+                               cur.tile > 0 ? BL2 - 2 * kTq : 0, lw, lane);
+      }
     }
     return;
   }
 
-  // compute waves: first the tiles wholly past a sequence's end
+  // compute waves: first this workgroup's share of the tiles wholly past a
+  // sequence's end
   {
-    const int nslot = a.B * a.H * a.ntiles;
-    for (int p = blockIdx.x; p < nslot; p += G) {
-      const int tile = p % a.ntiles, bh = p / a.ntiles;
-      const int b = bh / a.H, h = bh % a.H;
-      const int len = st.len(b);
+    const PadTable pt(st, a.B, H, a.ntiles, lane);
+    const int np = pt.total();
+    const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+    for (int i = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); i < p1; ++i) {
+      int b, h, tile;
+      pt.item(i, a.ntiles, b, h, tile);
       const int f0 = tile * kTq;
-      if (f0 < len) continue;
       const size_t slice = row_index(b, 0, h, T, H, D);
       uint16_t* out = static_cast<uint16_t*>(a.out) + slice;
       const int r1 = min(f0 + kTq, T);
@@ -741,15 +773,15 @@ __global__ __launch_bounds__(640) void band_fwd_pair_kernel(PairFwdArgs a) {
   const int col = lane & 15, g = lane >> 4;
   const int grp = w >> 2, wq = w & 3;  // tile of the step, wave within the tile
   const float c2 = a.scale_log2;
-  uint16_t* stage = s_stage + w * stage_elems<D>();
+  const int nblk = (16 + a.hi - a.lo + kSub - 1) / kSub;
   TileCursor<2> cur;
   cur.seek(st, g0);
-  int gi = g0, s = 0;
-  while (gi < g1) {
+  int slot = 0;
+  for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
     const int nst = cur.step_tiles();
-    lds_barrier();  // step s is in buffer s % 2
+    lds_barrier();  // step s is in the rings and query buffer s % 2
     if (grp < nst) {
-      const uint16_t* buf = s_buf + (s & 1) * BUF;
+      const uint16_t* qbuf = s_q + (s & 1) * 2 * kTq * D;
       const int len = cur.len;
       const int fA = cur.tile * kTq, bbase = fA + a.lo;
       const int r0 = fA + kTq * grp + 16 * wq;
@@ -758,27 +790,27 @@ __global__ __launch_bounds__(640) void band_fwd_pair_kernel(PairFwdArgs a) {
       const int wmax = min(r0 + 15, len - 1);
       bf16x8 qf[NS];
 #pragma unroll
-      for (int k = 0; k < NS; ++k) qf[k] = seg_row8<D>(buf + 2 * SEG2 * D, kTq * grp + 16 * wq + col, 32 * k + 8 * g);
+      for (int k = 0; k < NS; ++k) qf[k] = seg_row8<D>(qbuf, kTq * grp + 16 * wq + col, 32 * k + 8 * g);
       float lsum = 0.f;
       f32x4 acc[NB];
 #pragma unroll
       for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const WaveSeg<D> ws(buf, buf + SEG2 * D, lane, bbase, kTq * grp, a.nblk, a.lo, a.hi, r0, wmax, t, valid, len,
-                          wq);
+      const WaveSeg<D, RR> ws(s_k, s_v, lane, bbase, kTq * grp, nblk, a.lo, a.hi, r0, wmax, t, valid, len, wq,
+                              slot);
       f32x8 y[NBM];
       float m = max_over_column(seg_scores<D, NBM>(ws, qf, c2, lane, y));
       m = m == kNegInf ? 0.f : m;  // no key in the window (past the sequence's end)
       seg_weights_pv<D, NBM>(ws, y, m, acc, lsum);
       lsum = sum_over_column(lsum);
       const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
-      store_tile_rows<D>(stage, static_cast<uint16_t*>(a.out) + slice, fs, r0, min(16, T - r0), acc,
-                         valid ? 1.f / lsum : 0.f, valid, lane);
+      store_rows_direct<D>(static_cast<uint16_t*>(a.out) + slice, fs, r0, min(16, T - r0), acc,
+                           valid ? 1.f / lsum : 0.f, valid, lane);
       if (a.lse && g == 0 && t < T)
         a.lse[(static_cast<size_t>(cur.b) * H + cur.h) * T + t] = valid ? (m + log2f(lsum)) * kLn2 : kNegInf;
     }
-    ++gi;
     cur.next(st, H, a.B);
-    ++s;
+    const int inc = cur.tile > 0 ? 2 * kTq : BL2;
+    slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
   }
 }
 
@@ -806,7 +838,6 @@ constexpr int kMaxBlocks0 = 3, kMaxBlocks1 = 1;
 // The persistent kernel holds the sequence lengths in the lanes of a wave;
 // past this many sequences the tile kernel is used instead.
 constexpr int kPersistMaxB = 64;
-constexpr int kPairRows = 208;  // band rows of a two-tile step: 64 + 48 + 32 * 3
 
 // Lays the jobs' window segments onto tile-kernel bands (segment i of every job
 // reads band i). Returns false when a band would need more than its rows.
@@ -868,15 +899,21 @@ bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
       p.lse = a.job[0].lse;
       p.lo = a.job[0].seg[0].lo_off;
       p.hi = a.job[0].seg[0].hi_off;
-      p.nblk = d.job[0].seg[0].nblk;
       p.B = a.B;
       p.T = a.T;
       p.H = a.H;
       p.ntiles = d.ntiles;
       p.lengths = a.lengths;
       p.scale_log2 = d.scale_log2;
-      hipLaunchKernelGGL((band_fwd_pair_kernel<D, kPairRows, kMaxBlocks0>), dim3(compute_units()), dim3(640), 0,
-                         stream, p);
+      // sub-blocks of a wave's window (an empty window still reads one)
+      const int nblk = p.lo <= p.hi ? (16 + p.hi - p.lo + kSub - 1) / kSub : 1;
+      const dim3 grid(compute_units()), block(64 * (8 + kFwdLoaders));
+      if (nblk <= 1)
+        hipLaunchKernelGGL((band_fwd_pair_kernel<D, 1>), grid, block, 0, stream, p);
+      else if (nblk == 2)
+        hipLaunchKernelGGL((band_fwd_pair_kernel<D, 2>), grid, block, 0, stream, p);
+      else
+        hipLaunchKernelGGL((band_fwd_pair_kernel<D, 3>), grid, block, 0, stream, p);
       return true;
     }
     hipLaunchKernelGGL((band_fwd_tile_kernel<D, 1, X * kSaRows, 0, 3, 0>), dim3(grid), dim3(256), 0, stream, d);

@@ -273,6 +273,50 @@ __device__ __forceinline__ void store_tile_rows(uint16_t* stage, uint16_t* dst, 
   }
 }
 
+// Element offset o of an LDS row taken modulo RR rows (o < 2 RR D).
+template <int D, int RR>
+__device__ __forceinline__ int ring_wrap(int o) {
+  const unsigned u = static_cast<unsigned>(o), w = u - static_cast<unsigned>(RR * D);
+  return static_cast<int>(u < w ? u : w);
+}
+
+// Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
+// transposed accumulators, lane (g, col) holding features 16 i + 4 g .. + 3
+// of row col. Lanes g and g ^ 1 swap 4-feature pieces (permlane16 swap), so
+// that each lane holds whole 8-feature pieces: even g those of i = 0, 2, ...,
+// odd g those of i = 1, 3, ... Each store then writes 64 contiguous bytes of
+// 16 rows (whole rows for D = 32).
+template <int D>
+__device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
+                                                  float mul, bool valid, int lane) {
+  constexpr int NB = D / 16;
+  const int g = lane >> 4, col = lane & 15;
+  const bool even = (g & 1) == 0;
+  u32x2 p[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    p[i][0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
+    p[i][1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
+  }
+  // feature offset of piece j of this lane: 32 j + {0, 16, 8, 24}[g]
+  const int f0 = 8 * (g >> 1) + (even ? 0 : 16);
+  uint16_t* row = dst + (r0 + col) * fs + f0;
+#pragma unroll
+  for (int j = 0; j < NB / 2; ++j) {
+    u32x4 v;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // even lanes send piece 2j + 1, odd lanes piece 2j
+      const unsigned send = even ? p[2 * j + 1][h] : p[2 * j][h];
+      const auto r = __builtin_amdgcn_permlane16_swap(send, send, false, false);
+      const unsigned got = even ? r[1] : r[0];
+      v[h] = even ? p[2 * j][h] : got;
+      v[2 + h] = even ? got : p[2 * j + 1][h];
+    }
+    if (col < nrows) st16(row + 32 * j, v);
+  }
+}
+
 // Workgroup barrier that orders LDS accesses only. __syncthreads() also waits
 // for every global load and store of the wave to complete (vmcnt(0)), which
 // would make a wave that has just stored its outputs wait for the stores'
@@ -313,6 +357,34 @@ struct SeqTable {
   __device__ __forceinline__ int len(int b) const { return __builtin_amdgcn_readlane(lenv, b); }
   __device__ __forceinline__ int nt(int b) const { return __builtin_amdgcn_readlane(ntv, b); }
   __device__ __forceinline__ int before(int b) const { return b == 0 ? 0 : __builtin_amdgcn_readlane(incl, b - 1); }
+};
+
+// The padding tiles of a SeqTable's sequences (64-frame tiles wholly past a
+// sequence's end, in sequences of ntiles tiles), all heads, as one list:
+// lane b holds H (ntiles - nt(b)) and the inclusive prefix sum over lanes.
+struct PadTable {
+  int pb;    // this lane's padding tiles per head
+  int incl;  // padding tiles of sequences 0 .. lane, all heads
+  template <int TPS>
+  __device__ __forceinline__ PadTable(const SeqTable<TPS>& st, int B, int H, int ntiles, int lane) {
+    pb = lane < B ? ntiles - st.ntv : 0;
+    incl = H * pb;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int x = __shfl_up(incl, o);
+      if (lane >= o) incl += x;
+    }
+  }
+  __device__ __forceinline__ int total() const { return __builtin_amdgcn_readlane(incl, 63); }
+  // item i (< total()) of the list as (sequence b, head h, tile)
+  __device__ __forceinline__ void item(int i, int ntiles, int& b, int& h, int& tile) const {
+    b = __builtin_popcountll(__ballot(incl <= i));
+    const int before = b == 0 ? 0 : __builtin_amdgcn_readlane(incl, b - 1);
+    const int p = __builtin_amdgcn_readlane(pb, b);
+    const int local = i - before;
+    h = local / p;
+    tile = ntiles - p + (local - h * p);
+  }
 };
 
 // Cursor over the steps of a SeqTable (all fields wave-uniform).
