@@ -143,13 +143,34 @@ def bench_sa(steps, warmup):
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    # per-kernel durations, in a pass of their own
-    tf, tb = EventTimer(), EventTimer()
-    for i in range(min(steps, 50)):
-        sa_step(sets[i % N_SETS], lengths, w, tf, tb)
+    # per-kernel average durations: back-to-back launches of one kernel
+    # between two events (the forward rewrites the same out and lse)
+    n = min(steps, 50)
+
+    def fwd(s):
+        bd.sa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
+                      lse=s["lse"])
+
+    def bwd(s):
+        bd.sa_backward(s["q"], s["k"], s["v"], s["out"], s["lse"], s["dout"], w["Lb"], w["La"],
+                       lengths, dq=s["dq"], dk=s["dk"], dv=s["dv"])
+
+    return dict(total_ms=total_ms, fwd_ms=launch_ms(fwd, sets, n),
+                bwd_ms=launch_ms(bwd, sets, n), lengths=host_lengths)
+
+
+def launch_ms(fn, sets, n):
+    """Average duration of n back-to-back launches, from HIP events recorded on
+    the stream the library launches on (the current one)."""
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    return dict(total_ms=total_ms, fwd_ms=tf.mean_ms(), bwd_ms=tb.mean_ms(),
-                lengths=host_lengths)
+    s0.record()
+    for i in range(n):
+        fn(sets[i % N_SETS])
+    s1.record()
+    torch.cuda.synchronize()
+    return s0.elapsed_time(s1) / n
 
 
 def bench_llsa(steps, warmup):
@@ -168,16 +189,9 @@ def bench_llsa(steps, warmup):
         bd.llsa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
                         lse=s["lse"])
     torch.cuda.synchronize()
-    t = EventTimer()
-    for i in range(steps):
-        s = sets[i % N_SETS]
-        e = t.start()
-        bd.llsa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
-                        lse=s["lse"])
-        t.stop(e)
-    torch.cuda.synchronize()
+    ms = launch_ms(lambda s: bd.llsa_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths,
+                                             out=s["out"], lse=s["lse"]), sets, steps)
     L = x["lengths"].tolist()
-    ms = t.mean_ms()
     byts = acc.llsa_forward_bytes(L, w["H"], w["d"])
     flops = acc.llsa_forward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
     return {
@@ -209,17 +223,22 @@ def bench_stream():
         bd.sa_stream_step(st, q[u], k[u], v[u], out=out)
     st = bd.StreamState(S, H, d, Lb, La, R)
     torch.cuda.synchronize()
-    t = EventTimer()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     start.record()
     for u in range(steps):
-        e = t.start()
         bd.sa_stream_step(st, q[u], k[u], v[u], out=out)
-        t.stop(e)
     end.record()
     torch.cuda.synchronize()
     eager_ms = start.elapsed_time(end)
+    # per-step latency, in a pass of its own (an event per step)
+    st = bd.StreamState(S, H, d, Lb, La, R)
+    t = EventTimer()
+    for u in range(steps):
+        e = t.start()
+        bd.sa_stream_step(st, q[u], k[u], v[u], out=out)
+        t.stop(e)
+    torch.cuda.synchronize()
     lat = sorted(t.all_ms())
     # graph: capture 100 steps, replay 10 times (the counters advance on the device)
     n_cap = 100
