@@ -864,7 +864,8 @@ __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor
 }
 
 // -D and lse log2(e) of those rows into the statistics rings (+inf for rows
-// outside the sequence).
+// outside the sequence). Lane (g, col) holds features 32 s + 8 g .. + 7 of row
+// col: a bfloat16 dot product per lane, summed over the four lanes of the row.
 template <int D, int SEG>
 __device__ __forceinline__ void ring_stats(const RingRegs<D, SEG>& rg, float* ndn, float* lse2, int slot, int qbase,
                                            int len, int rlo, int bl, int lw, int lane) {
@@ -875,14 +876,11 @@ __device__ __forceinline__ void ring_stats(const RingRegs<D, SEG>& rg, float* nd
   for (int jj = 0; jj < R::BPL; ++jj) {
     const int r16 = rlo + 16 * (lw + 4 * jj);
     if (r16 < bl) {
-      f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+      float dp = 0.f;
 #pragma unroll
-      for (int s = 0; s < R::NS; ++s)
-        dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rg.df[jj][s], rg.of[jj][s], dd, 0, 0, 0);
-      // the diagonal entry of row col sits in lane g = col / 4, element col % 4
-      const int e = col & 3;
-      const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
-      if ((col >> 2) == g) {
+      for (int s = 0; s < R::NS; ++s) dp = dot_bf16x8(rg.df[jj][s], rg.of[jj][s], dp);
+      const float dg = sum_over_column(dp);
+      if (g == 0) {
         int lr = slot + r16 + col;
         lr = lr >= RR ? lr - RR : lr;
         const int fr = qbase + r16 + col;

@@ -376,23 +376,6 @@ struct TileArgs {
   float scale_log2;
 };
 
-// Maximum and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 of a query
-// column, with the lane-swap instructions of gfx950 (each swap leaves x[l]
-// and x[l ^ 16] (x[l ^ 32]) in the two results of every lane, so every lane
-// gets the same value).
-__device__ __forceinline__ float max_over_column(float x) {
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float sum_over_column(float x) {
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // A wave's window segment inside a staged band: its 16 queries r0 .. r0 + 15
 // (this lane's: t) see frames t + lo .. t + hi, held by band rows from sb0 on.
 // With RR > 0 the band is a ring of RR rows (a multiple of 32): band row r

@@ -42,6 +42,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// c + x . y over 8 bfloat16 pairs (float accumulation, two pairs per
+// instruction). The pairs are taken with constant shuffles.
+__device__ __forceinline__ float dot_bf16x8(bf16x8 x, bf16x8 y, float c) {
+  typedef __bf16 v8 __attribute__((ext_vector_type(8)));
+  const v8 a = __builtin_bit_cast(v8, x), b = __builtin_bit_cast(v8, y);
+  c = __builtin_amdgcn_fdot2_f32_bf16(a.s01, b.s01, c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(a.s23, b.s23, c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(a.s45, b.s45, c, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(a.s67, b.s67, c, false);
+}
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 // MFMA operand of a product that contracts over frames, read from a row-major
@@ -278,6 +290,23 @@ template <int D, int RR>
 __device__ __forceinline__ int ring_wrap(int o) {
   const unsigned u = static_cast<unsigned>(o), w = u - static_cast<unsigned>(RR * D);
   return static_cast<int>(u < w ? u : w);
+}
+
+// Maximum and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 of a query
+// column, with the lane-swap instructions of gfx950 (each swap leaves x[l]
+// and x[l ^ 16] (x[l ^ 32]) in the two results of every lane, so every lane
+// gets the same value).
+__device__ __forceinline__ float max_over_column(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_over_column(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
