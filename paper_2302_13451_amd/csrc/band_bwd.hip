@@ -891,6 +891,22 @@ __device__ __forceinline__ void ring_stats(const RingRegs<D, SEG>& rg, float* nd
   }
 }
 
+// This workgroup's share (of G) of the tiles wholly past a sequence's end:
+// zero dq, dk and dv rows (NT threads, thread i).
+template <int D, int NT>
+__device__ __forceinline__ void zero_padding_tiles(const BwdDev& a, const SeqTable<1>& st, int G, int i) {
+  const PadTable pt(st, a.B, a.H, a.ntiles, threadIdx.x & 63);
+  const int np = pt.total();
+  const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+  for (int p = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); p < p1; ++p) {
+    int b, h, tile;
+    pt.item(p, a.ntiles, b, h, tile);
+    const int f0 = tile * kC, f1 = min(f0 + kC, a.T);
+    zero_rows<D, NT>(a.dk, a.dv, b, h, a.T, a.H, f0, f1, i);
+    zero_rows<D, NT>(a.dq, nullptr, b, h, a.T, a.H, f0, f1, i);
+  }
+}
+
 // Workgroup barrier for a wave whose direct copies may still be in flight:
 // waits for its own LDS accesses only (a release fence would also wait for
 // the copies, which are LDS writes).
@@ -921,7 +937,10 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
 
   if (w >= 8) {
     const int lw = w - 8;
-    if (g0 >= g1) return;
+    if (g0 >= g1) {
+      zero_padding_tiles<D, 256>(a, st, G, tid - 512);
+      return;
+    }
     RingRegs<D, SEG> rg;
     TileCursor<1> cur;  // tile t
     cur.seek(st, g0);
@@ -947,23 +966,12 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
         ring_copy<D, SEG>(a, cur, s_ring, slot, rlo, bl, lw, lane);
       }
     }
+    // with nothing left to copy, the loaders write this workgroup's share of
+    // the tiles wholly past a sequence's end while the compute waves finish
+    zero_padding_tiles<D, 256>(a, st, G, tid - 512);
     return;
   }
 
-  // compute waves: first this workgroup's share of the tiles wholly past a
-  // sequence's end
-  {
-    const PadTable pt(st, a.B, H, a.ntiles, lane);
-    const int np = pt.total();
-    const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
-    for (int i = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); i < p1; ++i) {
-      int b, h, tile;
-      pt.item(i, a.ntiles, b, h, tile);
-      const int f0 = tile * kC;
-      zero_rows<D, 512>(a.dk, a.dv, b, h, T, H, f0, min(f0 + kC, T), tid);
-      zero_rows<D, 512>(a.dq, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
-    }
-  }
   if (g0 >= g1) return;
   const int col = lane & 15, wq = w & 3;
   TileCursor<1> cur;

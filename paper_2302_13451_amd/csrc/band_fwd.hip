@@ -378,8 +378,8 @@ struct TileArgs {
 
 // A wave's window segment inside a staged band: its 16 queries r0 .. r0 + 15
 // (this lane's: t) see frames t + lo .. t + hi, held by band rows from sb0 on.
-// With RR > 0 the band is a ring of RR rows (a multiple of 32): band row r
-// sits in LDS row (slot0 + r) mod RR, slot0 a multiple of 16.
+// With RR > 0 the band is a ring of RR rows (a multiple of 32, so the swizzle
+// pattern survives the wrap): band row r sits in LDS row (slot0 + r) mod RR.
 template <int D, int RR = 0>
 struct WaveSeg {
   const uint16_t* Xk;
@@ -396,7 +396,7 @@ struct WaveSeg {
   __device__ __forceinline__ WaveSeg(const uint16_t* k, const uint16_t* v, int lane, int bbase, int shift, int nb,
                                      int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq,
                                      int slot0 = 0)
-      : Xk(k), Xv(v), bo(lane, (slot0 + 16 * wq + shift) & (RR > 0 ? 16 : ~0)) {
+      : Xk(k), Xv(v), bo(lane, (slot0 + 16 * wq + shift) & (RR > 0 ? 31 : ~0)) {
     sb0 = 16 * wq + shift;
     x0 = slot0 + sb0;
     kb0 = bbase + sb0;
@@ -684,14 +684,36 @@ __device__ __forceinline__ void ring_fwd_issue(const PairFwdArgs& a, const TileC
   }
   for (int I = lw; I < 2 * kTq / RPI; I += kFwdLoaders) {
     const int r = I * RPI + rl;
-    __builtin_amdgcn_global_load_lds(qp + (min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r))), qbuf + I * 512,
-                                     16, 0, 0);
+    const int off = min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r));
+    __builtin_amdgcn_global_load_lds(qp + off, qbuf + I * 512, 16, 0, 0);
+  }
+}
+
+// This workgroup's share (of G) of the tiles wholly past a sequence's end:
+// zero output rows and -inf lse (64 kFwdLoaders threads, thread i).
+template <int D>
+__device__ __forceinline__ void zero_padding_tiles(const PairFwdArgs& a, const SeqTable<2>& st, int G, int i) {
+  constexpr int NT = 64 * kFwdLoaders, CPR = D / 8;
+  const int T = a.T, H = a.H, fs = H * D;
+  const PadTable pt(st, a.B, H, a.ntiles, threadIdx.x & 63);
+  const int np = pt.total();
+  const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+  for (int p = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); p < p1; ++p) {
+    int b, h, tile;
+    pt.item(p, a.ntiles, b, h, tile);
+    const int f0 = tile * kTq, r1 = min(f0 + kTq, T);
+    uint16_t* out = static_cast<uint16_t*>(a.out) + row_index(b, 0, h, T, H, D);
+    for (int e = i; e < (r1 - f0) * CPR; e += NT) st16(out + (f0 + e / CPR) * fs + 8 * (e % CPR), kZero16);
+    if (a.lse) {
+      float* lp = a.lse + (static_cast<size_t>(b) * H + h) * T;
+      for (int r = f0 + i; r < r1; r += NT) lp[r] = kNegInf;
+    }
   }
 }
 
 template <int D, int NBM>
 __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(PairFwdArgs a) {
-  constexpr int NS = D / 32, NB = D / 16, CPR = D / 8;
+  constexpr int NS = D / 32, NB = D / 16;
   constexpr int RR = kFwdRingRows;
   constexpr int BL2 = kTq + 48 + kSub * NBM;  // band rows of a two-tile step
   static_assert(2 * BL2 <= RR && RR % 32 == 0, "a step's band and the next one must fit the ring");
@@ -710,7 +732,10 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
 
   if (w >= 8) {
     const int lw = w - 8;
-    if (g0 >= g1) return;
+    if (g0 >= g1) {
+      zero_padding_tiles<D>(a, st, G, tid - 512);
+      return;
+    }
     TileCursor<2> cur;
     cur.seek(st, g0);
     int slot = 0;
@@ -729,29 +754,12 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
                                cur.tile > 0 ? BL2 - 2 * kTq : 0, lw, lane);
       }
     }
+    // with nothing left to copy, the loaders write this workgroup's share of
+    // the tiles wholly past a sequence's end while the compute waves finish
+    zero_padding_tiles<D>(a, st, G, tid - 512);
     return;
   }
 
-  // compute waves: first this workgroup's share of the tiles wholly past a
-  // sequence's end
-  {
-    const PadTable pt(st, a.B, H, a.ntiles, lane);
-    const int np = pt.total();
-    const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
-    for (int i = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); i < p1; ++i) {
-      int b, h, tile;
-      pt.item(i, a.ntiles, b, h, tile);
-      const int f0 = tile * kTq;
-      const size_t slice = row_index(b, 0, h, T, H, D);
-      uint16_t* out = static_cast<uint16_t*>(a.out) + slice;
-      const int r1 = min(f0 + kTq, T);
-      for (int e = tid; e < (r1 - f0) * CPR; e += 512) st16(out + (f0 + e / CPR) * fs + 8 * (e % CPR), kZero16);
-      if (a.lse) {
-        float* lp = a.lse + (static_cast<size_t>(b) * H + h) * T;
-        for (int r = f0 + tid; r < r1; r += 512) lp[r] = kNegInf;
-      }
-    }
-  }
   if (g0 >= g1) return;
   const int col = lane & 15, g = lane >> 4;
   const int grp = w >> 2, wq = w & 3;  // tile of the step, wave within the tile
@@ -794,6 +802,195 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
     cur.next(st, H, a.B);
     const int inc = cur.tile > 0 ? 2 * kTq : BL2;
     slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent bfloat16 LLSA forward (two outputs, each over two window
+// segments: branch L and branch C, Eq. 14/15) for up to 64 sequences. The
+// structure of the SA kernel above with one 64-query tile per step: the K/V
+// bands of branch L (band 0) and branch C (band 1) live in LDS rings, a tile
+// that continues its predecessor copies only 64 new rows of each, and the
+// query rows of both outputs go to a double buffer. Waves 0-3 compute the
+// causal output, waves 4-7 the look-ahead output (16 queries each), waves
+// 8-15 copy: those with lw < 4 band 0, the others band 1, all of them query
+// rows.
+struct LlsaRingArgs {
+  const void* q[2];      // queries of output j (0: causal, 1: look-ahead)
+  const void* k[2];      // keys and values of band i (0: branch L, 1: branch C)
+  const void* v[2];
+  void* out[2];
+  float* lse[2];
+  int base[2];           // band i's row 0 is frame f0 + base[i] of a tile at f0
+  int bl[2];             // rows of band i per tile (multiple of 16)
+  int lo[2][2], hi[2][2];  // output j, segment i: frames t + lo .. t + hi
+  int nblk[2][2];        // sub-blocks of a wave's window in that segment
+  int B, T, H;
+  int ntiles;
+  const int32_t* lengths;
+  float scale_log2;
+};
+
+constexpr int kLlsaRing0 = 320, kLlsaRing1 = 192;  // ring rows of bands 0 and 1 (twice a band)
+
+// The loaders' copies of one tile: band rows [rlo_i, bl_i) of each band into
+// ring rows (slot_i + r) mod RR_i (16-row blocks; loaders 0-3 band 0, 4-7
+// band 1) and 64 query rows of each output into qbuf (all loaders).
+template <int D>
+__device__ __forceinline__ void llsa_ring_issue(const LlsaRingArgs& a, const TileCursor<1>& cur, uint16_t* ring0,
+                                                uint16_t* ring1, uint16_t* qbuf, int slot0, int slot1, bool cont,
+                                                int lw, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, IPB = 16 / RPI;
+  const int rl = lane / CPR, pp = lane % CPR;
+  const int fs = a.H * D;
+  const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
+  const int f0 = cur.tile * kTq, last = cur.len - 1;
+  const int i = lw >> 2, lq = lw & 3;
+  const int RR = i ? kLlsaRing1 : kLlsaRing0;
+  uint16_t* const rk = i ? ring1 : ring0;
+  uint16_t* const rv = rk + RR * D;
+  const uint16_t* kp = static_cast<const uint16_t*>(a.k[i]) + slice;
+  const uint16_t* vp = static_cast<const uint16_t*>(a.v[i]) + slice;
+  const int bl = a.bl[i], bbase = f0 + a.base[i], slot = i ? slot1 : slot0;
+  for (int r16 = (cont ? bl - kTq : 0) + 16 * lq; r16 < bl; r16 += 64) {
+    int lr0 = slot + r16;
+    lr0 = lr0 >= RR ? lr0 - RR : lr0;
+#pragma unroll
+    for (int u = 0; u < IPB; ++u) {
+      const int r = r16 + u * RPI + rl;
+      const int off = min(max(bbase + r, 0), last) * fs + 8 * (pp ^ seg_swizzle<D>(lr0 + u * RPI + rl));
+      const int dst = (lr0 + u * RPI) * D;
+      __builtin_amdgcn_global_load_lds(kp + off, rk + dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vp + off, rv + dst, 16, 0, 0);
+    }
+  }
+  // 2 x 64 query rows: copy I of 2 * kTq / RPI fills rows RPI (I % (kTq / RPI)) .. of output I / (kTq / RPI)
+  for (int I = lw; I < 2 * kTq / RPI; I += 8) {
+    const int j = I / (kTq / RPI), r = (I % (kTq / RPI)) * RPI + rl;
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q[j]) + slice;
+    // (offsets go through a variable: a call to min inside the builtin's
+    // arguments fails overload resolution in the host pass)
+    const int off = min(f0 + r, last) * fs + 8 * (pp ^ seg_swizzle<D>(r));
+    __builtin_amdgcn_global_load_lds(qp + off, qbuf + j * kTq * D + (I % (kTq / RPI)) * 512, 16, 0, 0);
+  }
+}
+
+// This workgroup's share (of G) of the tiles wholly past a sequence's end:
+// zero output rows and -inf lse of both outputs (512 threads, thread i).
+template <int D>
+__device__ __forceinline__ void llsa_zero_padding(const LlsaRingArgs& a, const SeqTable<1>& st, int G, int i) {
+  constexpr int CPR = D / 8;
+  const int T = a.T, H = a.H, fs = H * D;
+  const PadTable pt(st, a.B, H, a.ntiles, threadIdx.x & 63);
+  const int np = pt.total();
+  const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+  for (int p = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); p < p1; ++p) {
+    int b, h, tile;
+    pt.item(p, a.ntiles, b, h, tile);
+    const int f0 = tile * kTq, r1 = min(f0 + kTq, T);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      uint16_t* out = static_cast<uint16_t*>(a.out[j]) + row_index(b, 0, h, T, H, D);
+      for (int e = i; e < (r1 - f0) * CPR; e += 512) st16(out + (f0 + e / CPR) * fs + 8 * (e % CPR), kZero16);
+      if (a.lse[j]) {
+        float* lp = a.lse[j] + (static_cast<size_t>(b) * H + h) * T;
+        for (int r = f0 + i; r < r1; r += 512) lp[r] = kNegInf;
+      }
+    }
+  }
+}
+
+template <int D, int NB0, int NB1>
+__global__ __launch_bounds__(1024) void llsa_fwd_ring_kernel(LlsaRingArgs a) {
+  constexpr int NS = D / 32, NB = D / 16;
+  constexpr int R0 = kLlsaRing0, R1 = kLlsaRing1;
+  __shared__ __attribute__((aligned(16))) uint16_t s_r0[2 * R0 * D];  // band 0 keys, then values
+  __shared__ __attribute__((aligned(16))) uint16_t s_r1[2 * R1 * D];  // band 1 keys, then values
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[2 * 2 * kTq * D];  // two buffers of 2 x 64 query rows
+
+  const int G = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.T, H = a.H, fs = H * D;
+  const SeqTable<1> st(a.lengths, a.B, T, H, lane);
+  const int nsteps = st.total();
+  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * nsteps / G);
+  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
+
+  if (w >= 8) {
+    const int lw = w - 8;
+    if (g0 < g1) {
+      TileCursor<1> cur;
+      cur.seek(st, g0);
+      int slot0 = 0, slot1 = 0;
+      llsa_ring_issue<D>(a, cur, s_r0, s_r1, s_q, slot0, slot1, false, lw, lane);
+      for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): tile s is in
+        // a plain barrier: this wave reads no LDS and its copies are ordered
+        // by the wait above. After it the compute waves are done with tile
+        // s - 1, whose rows and query buffer the copies of tile s + 1 reuse.
+        __builtin_amdgcn_s_barrier();
+        if (gi + 1 < g1) {
+          cur.next(st, H, a.B);
+          const bool cont = cur.tile > 0;
+          const int i0 = cont ? kTq : a.bl[0], i1 = cont ? kTq : a.bl[1];
+          slot0 = slot0 + i0 >= R0 ? slot0 + i0 - R0 : slot0 + i0;
+          slot1 = slot1 + i1 >= R1 ? slot1 + i1 - R1 : slot1 + i1;
+          llsa_ring_issue<D>(a, cur, s_r0, s_r1, s_q + ((s + 1) & 1) * 2 * kTq * D, slot0, slot1, cont, lw, lane);
+        }
+      }
+    }
+    // with nothing left to copy, the loaders write this workgroup's share of
+    // the tiles wholly past a sequence's end while the compute waves finish
+    llsa_zero_padding<D>(a, st, G, tid - 512);
+    return;
+  }
+  if (g0 >= g1) return;
+
+  const int col = lane & 15, g = lane >> 4;
+  const int j = w >> 2, wq = w & 3;  // output, wave within the tile
+  const float c2 = a.scale_log2;
+  TileCursor<1> cur;
+  cur.seek(st, g0);
+  int slot0 = 0, slot1 = 0;
+  for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
+    lds_barrier();  // tile s is in the rings and query buffer s % 2
+    const uint16_t* qbuf = s_q + (s & 1) * 2 * kTq * D + j * kTq * D;
+    const int len = cur.len;
+    const int f0 = cur.tile * kTq;
+    const int r0 = f0 + 16 * wq;
+    const int t = r0 + col;
+    const bool valid = t < len;
+    const int wmax = min(r0 + 15, len - 1);
+    bf16x8 qf[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) qf[k] = seg_row8<D>(qbuf, 16 * wq + col, 32 * k + 8 * g);
+    float lsum = 0.f;
+    f32x4 acc[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // two passes over the window, which a wave holds in registers whole
+    const WaveSeg<D, R0> ws0(s_r0, s_r0 + R0 * D, lane, f0 + a.base[0], a.lo[j][0] - a.base[0], a.nblk[j][0],
+                             a.lo[j][0], a.hi[j][0], r0, wmax, t, valid, len, wq, slot0);
+    const WaveSeg<D, R1> ws1(s_r1, s_r1 + R1 * D, lane, f0 + a.base[1], a.lo[j][1] - a.base[1], a.nblk[j][1],
+                             a.lo[j][1], a.hi[j][1], r0, wmax, t, valid, len, wq, slot1);
+    f32x8 y0[NB0], y1[NB1];
+    float mx = fmaxf(seg_scores<D, NB0>(ws0, qf, c2, lane, y0), seg_scores<D, NB1>(ws1, qf, c2, lane, y1));
+    mx = max_over_column(mx);
+    mx = mx == kNegInf ? 0.f : mx;  // no key in the window (past the sequence's end)
+    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
+    seg_weights_pv<D, NB1>(ws1, y1, mx, acc, lsum);
+    lsum = sum_over_column(lsum);
+    const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
+    store_rows_direct<D>(static_cast<uint16_t*>(a.out[j]) + slice, fs, r0, min(16, T - r0), acc,
+                         valid ? 1.f / lsum : 0.f, valid, lane);
+    if (a.lse[j] && g == 0 && t < T)
+      a.lse[j][(static_cast<size_t>(cur.b) * H + cur.h) * T + t] = valid ? (mx + log2f(lsum)) * kLn2 : kNegInf;
+    cur.next(st, H, a.B);
+    const bool cont = cur.tile > 0;
+    const int i0 = cont ? kTq : a.bl[0], i1 = cont ? kTq : a.bl[1];
+    slot0 = slot0 + i0 >= R0 ? slot0 + i0 - R0 : slot0 + i0;
+    slot1 = slot1 + i1 >= R1 ? slot1 + i1 - R1 : slot1 + i1;
   }
 }
 
@@ -860,6 +1057,62 @@ bool plan_tile(const BandForwardArgs& a, int rows0, int rows1, TileArgs& d) {
   return true;
 }
 
+// The LLSA forward on the ring kernel, when both bands of every output fit it
+// (band 0 a common base and at most kLlsaRing0 / 2 rows, band 1 at most
+// kLlsaRing1 / 2, windows of at most 3 and 1 sub-blocks per wave).
+template <int D>
+bool launch_llsa_ring(const BandForwardArgs& a, int ntiles, float scale_log2, hipStream_t stream) {
+  LlsaRingArgs r{};
+  int nb[2] = {0, 0};
+  for (int i = 0; i < 2; ++i) {
+    const BandSegment& s0 = a.job[0].seg[i];
+    const BandSegment& s1 = a.job[1].seg[i];
+    if (s0.k != s1.k || s0.v != s1.v) return false;
+    r.k[i] = s0.k;
+    r.v[i] = s0.v;
+    r.base[i] = s0.lo_off < s1.lo_off ? s0.lo_off : s1.lo_off;
+    int rows = 0;
+    for (int j = 0; j < 2; ++j) {
+      const BandSegment& sg = a.job[j].seg[i];
+      r.lo[j][i] = sg.lo_off;
+      r.hi[j][i] = sg.hi_off;
+      // an empty segment still reads one sub-block (fully masked)
+      const int n = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + kSub - 1) / kSub : 1;
+      r.nblk[j][i] = sg.lo_off <= sg.hi_off ? n : 0;
+      nb[i] = nb[i] > n ? nb[i] : n;
+      const long long need = static_cast<long long>(sg.lo_off) - r.base[i] + 48 + kSub * static_cast<long long>(n);
+      if (need > rows) rows = static_cast<int>(need > (1 << 20) ? (1 << 20) : need);
+    }
+    r.bl[i] = (rows + 15) / 16 * 16;
+  }
+  if (nb[1] > 1 || 2 * r.bl[0] > kLlsaRing0 || 2 * r.bl[1] > kLlsaRing1) return false;
+  for (int j = 0; j < 2; ++j) {  // every sub-block a kernel instance reads must lie in its band
+    if (r.lo[j][0] - r.base[0] + 48 + kSub * nb[0] > r.bl[0]) return false;
+    if (r.lo[j][1] - r.base[1] + 48 + kSub * 1 > r.bl[1]) return false;
+  }
+  for (int j = 0; j < 2; ++j) {
+    r.q[j] = a.job[j].q;
+    r.out[j] = a.job[j].out;
+    r.lse[j] = a.job[j].lse;
+  }
+  r.B = a.B;
+  r.T = a.T;
+  r.H = a.H;
+  r.ntiles = ntiles;
+  r.lengths = a.lengths;
+  r.scale_log2 = scale_log2;
+  const dim3 grid(compute_units()), block(1024);
+  if (nb[0] <= 1)
+    hipLaunchKernelGGL((llsa_fwd_ring_kernel<D, 1, 1>), grid, block, 0, stream, r);
+  else if (nb[0] == 2)
+    hipLaunchKernelGGL((llsa_fwd_ring_kernel<D, 2, 1>), grid, block, 0, stream, r);
+  else if (nb[0] == 3)
+    hipLaunchKernelGGL((llsa_fwd_ring_kernel<D, 3, 1>), grid, block, 0, stream, r);
+  else
+    return false;
+  return true;
+}
+
 template <int D>
 bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
   TileArgs d{};
@@ -903,6 +1156,7 @@ bool launch_tile(const BandForwardArgs& a, hipStream_t stream) {
     return true;
   }
   if (a.njobs == 2 && a.job[0].nseg == 2) {
+    if (a.B <= kPersistMaxB && launch_llsa_ring<D>(a, d.ntiles, d.scale_log2, stream)) return true;
     if (!plan_tile(a, X * kLlsaRows0, X * kLlsaRows1, d)) return false;
     hipLaunchKernelGGL((band_fwd_tile_kernel<D, 2, X * kLlsaRows0, X * kLlsaRows1, 3, 1>), dim3(grid), dim3(512), 0,
                        stream, d);

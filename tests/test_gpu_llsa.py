@@ -34,6 +34,12 @@ def run(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths, scale="rsqrt_d", p
     (2, 170, 3, 64, 0, 9, (100, 170)),
     (1, 99, 2, 64, 10, 1, "full"),
     (2, 70, 1, 32, 300, 300, (10, 70)),
+    # the largest look-ahead the persistent kernel takes, and one past it;
+    # empty sequences between others; more sequences than a wave has lanes
+    (2, 190, 2, 64, 64, 16, (60, 190)),
+    (2, 190, 2, 64, 64, 17, (60, 190)),
+    (6, 140, 2, 64, 40, 8, (0, 140, 0, 70, 1, 0)),
+    (66, 80, 1, 64, 30, 4, (0, 80)),
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):
