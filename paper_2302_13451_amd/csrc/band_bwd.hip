@@ -936,6 +936,9 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
 
   if (w >= 8) {
+    // the loaders share each SIMD with two compute waves: at a higher issue
+    // priority their few instructions go out as soon as they are ready
+    __builtin_amdgcn_s_setprio(3);
     const int lw = w - 8;
     if (g0 >= g1) {
       zero_padding_tiles<D, 256>(a, st, G, tid - 512);

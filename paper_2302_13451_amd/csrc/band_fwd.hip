@@ -731,6 +731,9 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
   const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
 
   if (w >= 8) {
+    // the loaders share each SIMD with two compute waves: at a higher issue
+    // priority their few instructions go out as soon as they are ready
+    __builtin_amdgcn_s_setprio(3);
     const int lw = w - 8;
     if (g0 >= g1) {
       zero_padding_tiles<D>(a, st, G, tid - 512);
@@ -918,6 +921,7 @@ __global__ __launch_bounds__(1024) void llsa_fwd_ring_kernel(LlsaRingArgs a) {
   const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
 
   if (w >= 8) {
+    __builtin_amdgcn_s_setprio(3);  // as in the SA kernel
     const int lw = w - 8;
     if (g0 < g1) {
       TileCursor<1> cur;
