@@ -485,24 +485,6 @@ struct BwdBands {
   }
 };
 
-// Per-lane operand offsets of the wave's sub-blocks in the bands: the
-// sub-block at band row sb (sb = 16 wq + 32 m) sits at LDS rows slot0 + sb ..,
-// whose swizzle pattern repeats every 32 rows.
-template <int D, int RR>
-struct RingOffsets {
-  BlockOffsets<D> bo;
-  int s0;
-  __device__ __forceinline__ RingOffsets(int lane, int slot0, int wq)
-      : bo(lane, 16 * (((slot0 >> 4) + wq) & 1)), s0(slot0) {}
-  __device__ __forceinline__ void at(int sb, int& oa, int& oc, int& ota, int& otc) const {
-    bo.at(s0 + sb, oa, oc, ota, otc);
-    oa = ring_wrap<D, RR>(oa);
-    oc = ring_wrap<D, RR>(oc);
-    ota = ring_wrap<D, RR>(ota);
-    otc = ring_wrap<D, RR>(otc);
-  }
-};
-
 // Key role of one wave: keys r0 .. r0 + 15 against the query band. Each of the
 // wave's nblk sub-blocks starts at band row 16 wq + 32 m, so the wave's window
 // [r0 - La, r0 + 15 + Lb] starts at the same place in the first one; window
@@ -535,22 +517,23 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
   // every query of it (queries outside the sequence weigh zero anyway)
   const int ilo = wmax - La, ihi = r0 + Lb;
   const int sb0 = 16 * wq;
-  const RingOffsets<D, RR> ro(lane, bd.slot0, wq);
+  const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
+  const uint32_t xq = lds_addr(bd.q), xd = lds_addr(bd.dout);
   for (int m = 0; m < nblk; ++m) {
     const int sb = sb0 + kSub * m, qb = bd.qbase + sb;
     if (qb > whi || qb + kSub - 1 < wlo) continue;
-    int oa, oc, ota, otc;
-    ro.at(sb, oa, oc, ota, otc);
+    const uint32_t orow = sa.row(m), otr = sa.tr(m);
     const int st = bd.row(sb + 8 * g);  // statistics of rows sb + 8g .. + 7 (never split by the wrap)
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
     f32x4 dp0 = *reinterpret_cast<const f32x4*>(bd.ndn + st);
     f32x4 dp1 = *reinterpret_cast<const f32x4*>(bd.ndn + st + 4);
+    const uint32_t aq = xq + orow, ad = xd + orow;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.q + (oa ^ (32 * s))), kf[s], sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.q + (oc ^ (32 * s))), kf[s], sc1, 0, 0, 0);
-      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.dout + (oa ^ (32 * s))), vf[s], dp0, 0, 0, 0);
-      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.dout + (oc ^ (32 * s))), vf[s], dp1, 0, 0, 0);
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(aq ^ (64 * s)), kf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((aq ^ (64 * s)) + 8 * D), kf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(ad ^ (64 * s)), vf[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((ad ^ (64 * s)) + 8 * D), vf[s], dp1, 0, 0, 0);
     }
     const f32x4 l0 = *reinterpret_cast<const f32x4*>(bd.lse2 + st);
     const f32x4 l1 = *reinterpret_cast<const f32x4*>(bd.lse2 + st + 4);
@@ -574,10 +557,11 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
     const bf16x8 pf = __builtin_convertvector(x, bf16x8);
     const bf16x8 dsf = __builtin_convertvector(ds, bf16x8);
     // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
+    const uint32_t tq = xq + otr, td = xd + otr;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.dout, ota ^ (16 * i), otc ^ (16 * i)), pf, adv[i], 0, 0, 0);
-      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.q, ota ^ (16 * i), otc ^ (16 * i)), dsf, adk[i], 0, 0, 0);
+      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(td ^ (32 * i)), pf, adv[i], 0, 0, 0);
+      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(tq ^ (32 * i)), dsf, adk[i], 0, 0, 0);
     }
   }
 }
@@ -612,20 +596,21 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
   // valid query of the wave (and so inside the sequence)
   const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
   const int sb0 = 16 * wq;
-  const RingOffsets<D, RR> ro(lane, bd.slot0, wq);
+  const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
+  const uint32_t xk = lds_addr(bd.k), xv = lds_addr(bd.v);
   for (int m = 0; m < nblk; ++m) {
     const int sb = sb0 + kSub * m, kb = bd.kbase + sb;
     if (kb > whi || kb + kSub - 1 < wlo) continue;
-    int oa, oc, ota, otc;
-    ro.at(sb, oa, oc, ota, otc);
+    const uint32_t orow = sa.row(m);
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
     f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
+    const uint32_t ak = xk + orow, av = xv + orow;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.k + (oa ^ (32 * s))), qf[s], sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.k + (oc ^ (32 * s))), qf[s], sc1, 0, 0, 0);
-      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.v + (oa ^ (32 * s))), df[s], dp0, 0, 0, 0);
-      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_row8(bd.v + (oc ^ (32 * s))), df[s], dp1, 0, 0, 0);
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(ak ^ (64 * s)), qf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((ak ^ (64 * s)) + 8 * D), qf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(av ^ (64 * s)), df[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((av ^ (64 * s)) + 8 * D), df[s], dp1, 0, 0, 0);
     }
     f32x8 x;
 #pragma unroll
@@ -642,9 +627,10 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
     for (int j = 0; j < 8; ++j) x[j] = fast_exp2(x[j]) * (j < 4 ? dp0[j] : dp1[j - 4]);
     const bf16x8 dsf = __builtin_convertvector(x, bf16x8);
     // dq^T += k^T dS^T, contracting over the 32 keys
+    const uint32_t tk = xk + sa.tr(m);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(bd.k, ota ^ (16 * i), otc ^ (16 * i)), dsf, aq[i], 0, 0, 0);
+      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(tk ^ (32 * i)), dsf, aq[i], 0, 0, 0);
   }
 }
 
@@ -676,7 +662,7 @@ void sa_bwd_tile_kernel(BwdDev a) {
   static_assert(SEG % 16 == 0, "the D product covers the band in 16-row blocks");
   // the four bands; once every wave is done with them, the first part holds
   // each wave's output rows on their way to memory
-  __shared__ __attribute__((aligned(16))) uint16_t s_band[4 * SEG * D];
+  __shared__ __attribute__((aligned(128))) uint16_t s_band[4 * SEG * D];
   static_assert(8 * 2 * stage_elems<D>() <= 4 * SEG * D, "staging must fit in the bands");
   uint16_t* const s_q = s_band;
   uint16_t* const s_do = s_band + SEG * D;
@@ -919,7 +905,7 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   constexpr int NB = D / 16, RR = 2 * SEG;
   static_assert(RR % 32 == 0, "the swizzle pattern must survive the wrap of the ring");
   // q, dout, k, v rings, then the -D and lse log2(e) rings of the query band
-  __shared__ __attribute__((aligned(16))) uint16_t s_ring[4 * RR * D];
+  __shared__ __attribute__((aligned(128))) uint16_t s_ring[4 * RR * D];
   __shared__ __attribute__((aligned(16))) float s_stat[2 * RR];
   float* const s_ndn = s_stat;
   float* const s_lse2 = s_stat + RR;

@@ -382,10 +382,8 @@ struct TileArgs {
 // pattern survives the wrap): band row r sits in LDS row (slot0 + r) mod RR.
 template <int D, int RR = 0>
 struct WaveSeg {
-  const uint16_t* Xk;
-  const uint16_t* Xv;
-  BlockOffsets<D> bo;  // operand offsets of the sub-blocks at LDS row x0 + 32 m
-  int x0;              // (unwrapped) LDS row of the wave's first sub-block
+  uint32_t Xk, Xv;     // LDS byte addresses of the key and value arrays (128-byte aligned)
+  SubBlockAddr<D, RR> sa;
   int sb0;             // band row of the wave's first sub-block
   int kb0;             // its frame
   int nblk;            // sub-blocks of the wave's window
@@ -393,12 +391,14 @@ struct WaveSeg {
   int qlo_l;           // this lane's first frame (1 << 30: empty window)
   unsigned qwidth;     // ... and the width of its window
   int ilo, ihi;        // frames inside the window of every valid query of the wave
+  // The first sub-block starts at the multiple of 8 at or below the window's
+  // row 16 wq + shift (nb counts the sub-blocks from there); slot0 and the
+  // ring size are multiples of 16 and 32.
   __device__ __forceinline__ WaveSeg(const uint16_t* k, const uint16_t* v, int lane, int bbase, int shift, int nb,
                                      int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq,
                                      int slot0 = 0)
-      : Xk(k), Xv(v), bo(lane, (slot0 + 16 * wq + shift) & (RR > 0 ? 31 : ~0)) {
-    sb0 = 16 * wq + shift;
-    x0 = slot0 + sb0;
+      : Xk(lds_addr(k)), Xv(lds_addr(v)), sa(lane, slot0 + 16 * wq + (shift & ~7)) {
+    sb0 = 16 * wq + (shift & ~7);
     kb0 = bbase + sb0;
     nblk = lo <= hi ? nb : 0;
     wlo = max(0, r0 + lo);
@@ -410,39 +410,33 @@ struct WaveSeg {
     ilo = max(0, wmax + lo);
     ihi = min(len - 1, r0 + hi);
   }
-  // operand offsets of sub-block m
-  __device__ __forceinline__ void at(int m, int& oa, int& oc, int& ota, int& otc) const {
-    bo.at(x0 + kSub * m, oa, oc, ota, otc);
-    if constexpr (RR > 0) {
-      oa = ring_wrap<D, RR>(oa);
-      oc = ring_wrap<D, RR>(oc);
-      ota = ring_wrap<D, RR>(ota);
-      otc = ring_wrap<D, RR>(otc);
-    }
-  }
+  // LDS byte addresses of sub-block m's reads: row xa of the keys and row xt
+  // of the values (their pieces and the rows 4 further as SubBlockAddr says)
+  __device__ __forceinline__ uint32_t key_addr(int m) const { return Xk + sa.row(m); }
+  __device__ __forceinline__ uint32_t val_addr(int m) const { return Xv + sa.tr(m); }
 };
 
-// First pass over a segment: the scaled scores y = (q . k) log2(e) / sqrt(d)
-// of the wave's NBM sub-blocks (lane (g, col): keys kb + 8g + 0..7 of query
-// col; the score tiles take the key rows in the order 8(r/4) + r%4 and + 4,
-// which puts them straight into the weight operand layout of the PV product),
-// -inf outside the lane's window. All NBM sub-blocks are computed without
-// branches, so the LDS reads and MFMAs of different sub-blocks overlap: the
-// band must hold finite data in every row they touch (rows outside the
-// sequence, or past the window, are masked). Returns the lane's maximum.
+// First pass over a segment: the scores q . k of the wave's NBM sub-blocks
+// (lane (g, col): keys kb + 8g + 0..7 of query col; the score tiles take the
+// key rows in the order 8(r/4) + r%4 and + 4, which puts them straight into
+// the weight operand layout of the PV product), -inf outside the lane's
+// window. All NBM sub-blocks are computed without branches, so the LDS reads
+// and MFMAs of different sub-blocks overlap: the band must hold finite data in
+// every row they touch (rows outside the sequence, or past the window, are
+// masked). Returns the lane's maximum. The scale is applied in the second
+// pass (it is positive, so the maximum commutes with it).
 template <int D, int NBM, int RR>
-__device__ __forceinline__ float seg_scores(const WaveSeg<D, RR>& s, const bf16x8* qf, float c2, int lane, f32x8* y) {
+__device__ __forceinline__ float seg_scores(const WaveSeg<D, RR>& s, const bf16x8* qf, int lane, f32x8* y) {
   constexpr int NS = D / 32;
   const int g = lane >> 4;
   bf16x8 ka[NBM][2 * NS];
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
-    int oa, oc, ota, otc;
-    s.at(m, oa, oc, ota, otc);
+    const uint32_t a = s.key_addr(m);
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
-      ka[m][2 * k] = lds_row8(s.Xk + (oa ^ (32 * k)));
-      ka[m][2 * k + 1] = lds_row8(s.Xk + (oc ^ (32 * k)));
+      ka[m][2 * k] = lds_rd8(a ^ (64 * k));
+      ka[m][2 * k + 1] = lds_rd8((a ^ (64 * k)) + 8 * D);
     }
   }
   float ymax = kNegInf;
@@ -456,8 +450,8 @@ __device__ __forceinline__ float seg_scores(const WaveSeg<D, RR>& s, const bf16x
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      y[m][j] = s0[j] * c2;
-      y[m][j + 4] = s1[j] * c2;
+      y[m][j] = s0[j];
+      y[m][j + 4] = s1[j];
     }
     const int kb = s.kb0 + kSub * m;
     if (!(m < s.nblk && kb >= s.ilo && kb + kSub - 1 <= s.ihi)) {  // not inside every window: mask
@@ -465,36 +459,42 @@ __device__ __forceinline__ float seg_scores(const WaveSeg<D, RR>& s, const bf16x
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[m][j] = static_cast<unsigned>(base + j) <= s.qwidth ? y[m][j] : kNegInf;
     }
-    ymax = fmaxf(ymax, fmaxf(fmaxf(fmaxf(y[m][0], y[m][1]), fmaxf(y[m][2], y[m][3])),
-                             fmaxf(fmaxf(y[m][4], y[m][5]), fmaxf(y[m][6], y[m][7]))));
+    ymax = vmax(vmax(vmax(ymax, y[m][0]), vmax(y[m][1], y[m][2])),
+                vmax(vmax(y[m][3], y[m][4]), vmax(vmax(y[m][5], y[m][6]), y[m][7])));
   }
   return ymax;
 }
 
-// Second pass: weights p = 2^(y - mx), their float sum, and O^T += V^T P^T
-// with the weights rounded to bfloat16 (lane (g, col) needs
-// V[kb + 8g + j][16 i + col], the transposing LDS read).
+// Second pass: weights p = 2^(c2 y - mx) (mx: the scaled maximum), their
+// float sum, and O^T += V^T P^T with the weights rounded to bfloat16 (lane
+// (g, col) needs V[kb + 8g + j][16 i + col], the transposing LDS read).
 template <int D, int NBM, int RR>
-__device__ __forceinline__ void seg_weights_pv(const WaveSeg<D, RR>& s, const f32x8* y, float mx, f32x4* acc,
-                                               float& lsum) {
+__device__ __forceinline__ void seg_weights_pv(const WaveSeg<D, RR>& s, const f32x8* y, float c2, float mx,
+                                               f32x4* acc, float& lsum) {
   constexpr int NB = D / 16;
   bf16x8 pf[NBM];
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
     f32x8 p;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) p[j] = fast_exp2(y[m][j] - mx);
+    for (int j = 0; j < 8; ++j) p[j] = fast_exp2(__builtin_fmaf(y[m][j], c2, -mx));
     lsum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
     pf[m] = __builtin_convertvector(p, bf16x8);
   }
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
-    int oa, oc, ota, otc;
-    s.at(m, oa, oc, ota, otc);
+    const uint32_t t = s.val_addr(m);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8(s.Xv, ota ^ (16 * i), otc ^ (16 * i)), pf[m], acc[i], 0, 0, 0);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(t ^ (32 * i)), pf[m], acc[i], 0, 0, 0);
   }
+}
+
+// Scaled maximum of a query's window from the lanes' raw maxima (0 for an
+// empty window, past the sequence's end).
+__device__ __forceinline__ float scaled_max(float ymax, float c2) {
+  const float m = max_over_column(ymax);
+  return m == kNegInf ? 0.f : m * c2;
 }
 
 template <int D, int NJOB, int SEG0, int SEG1, int NB0, int NB1>
@@ -502,11 +502,12 @@ __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
   constexpr int NT = 256 * NJOB, NW = 4 * NJOB;
   constexpr int NS = D / 32, NB = D / 16;
   constexpr int CPR = D / 8;
-  __shared__ __attribute__((aligned(16))) uint16_t s_kv[2 * (SEG0 + SEG1) * D];
+  __shared__ __attribute__((aligned(128))) uint16_t s_kv[2 * (SEG0 + SEG1) * D];
   static_assert(NW * stage_elems<D>() <= 2 * (SEG0 + SEG1) * D, "staging must fit in the bands");
   uint16_t* const bk[2] = {s_kv, s_kv + 2 * SEG0 * D};
   uint16_t* const bv[2] = {s_kv + SEG0 * D, s_kv + (2 * SEG0 + SEG1) * D};
   constexpr int brows[2] = {SEG0, SEG1};
+  static_assert(SEG0 * D * 2 % 128 == 0 && SEG1 * D * 2 % 128 == 0, "band arrays must stay 128-byte aligned");
 
   int bh, tile;
   if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
@@ -589,23 +590,19 @@ __global__ __launch_bounds__(256 * NJOB) void band_fwd_tile_kernel(TileArgs a) {
   const WaveSeg<D> ws0(bk[0], bv[0], lane, f0 + a.band[0].base, sg0.shift, sg0.nblk, sg0.lo, sg0.hi, r0, wmax, t,
                        valid, len, w & 3);
   f32x8 y0[NB0];
-  float ymax = seg_scores<D, NB0>(ws0, qf, c2, lane, y0);
+  float ymax = seg_scores<D, NB0>(ws0, qf, lane, y0);
   if constexpr (NB1 > 0) {
     const TileSeg sg1 = job.seg[1];
     const WaveSeg<D> ws1(bk[1], bv[1], lane, f0 + a.band[1].base, sg1.shift, sg1.nblk, sg1.lo, sg1.hi, r0, wmax,
                          t, valid, len, w & 3);
     f32x8 y1[NB1];
-    ymax = fmaxf(ymax, seg_scores<D, NB1>(ws1, qf, c2, lane, y1));
-    float mx = max_over_column(ymax);
-    mx = mx == kNegInf ? 0.f : mx;  // no key in the window (past the sequence's end)
-    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
-    seg_weights_pv<D, NB1>(ws1, y1, mx, acc, lsum);
-    ymax = mx;
+    ymax = vmax(ymax, seg_scores<D, NB1>(ws1, qf, lane, y1));
+    ymax = scaled_max(ymax, c2);
+    seg_weights_pv<D, NB0>(ws0, y0, c2, ymax, acc, lsum);
+    seg_weights_pv<D, NB1>(ws1, y1, c2, ymax, acc, lsum);
   } else {
-    float mx = max_over_column(ymax);
-    mx = mx == kNegInf ? 0.f : mx;
-    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
-    ymax = mx;
+    ymax = scaled_max(ymax, c2);
+    seg_weights_pv<D, NB0>(ws0, y0, c2, ymax, acc, lsum);
   }
   const float m = ymax;
 
@@ -717,8 +714,8 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
   constexpr int RR = kFwdRingRows;
   constexpr int BL2 = kTq + 48 + kSub * NBM;  // band rows of a two-tile step
   static_assert(2 * BL2 <= RR && RR % 32 == 0, "a step's band and the next one must fit the ring");
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[RR * D];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[RR * D];
+  __shared__ __attribute__((aligned(128))) uint16_t s_k[RR * D];
+  __shared__ __attribute__((aligned(128))) uint16_t s_v[RR * D];
   __shared__ __attribute__((aligned(16))) uint16_t s_q[2 * 2 * kTq * D];
 
   const int G = gridDim.x;
@@ -792,9 +789,8 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
       const WaveSeg<D, RR> ws(s_k, s_v, lane, bbase, kTq * grp, nblk, a.lo, a.hi, r0, wmax, t, valid, len, wq,
                               slot);
       f32x8 y[NBM];
-      float m = max_over_column(seg_scores<D, NBM>(ws, qf, c2, lane, y));
-      m = m == kNegInf ? 0.f : m;  // no key in the window (past the sequence's end)
-      seg_weights_pv<D, NBM>(ws, y, m, acc, lsum);
+      const float m = scaled_max(seg_scores<D, NBM>(ws, qf, lane, y), c2);
+      seg_weights_pv<D, NBM>(ws, y, c2, m, acc, lsum);
       lsum = sum_over_column(lsum);
       const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
       store_rows_direct<D>(static_cast<uint16_t*>(a.out) + slice, fs, r0, min(16, T - r0), acc,
@@ -907,9 +903,10 @@ template <int D, int NB0, int NB1>
 __global__ __launch_bounds__(1024) void llsa_fwd_ring_kernel(LlsaRingArgs a) {
   constexpr int NS = D / 32, NB = D / 16;
   constexpr int R0 = kLlsaRing0, R1 = kLlsaRing1;
-  __shared__ __attribute__((aligned(16))) uint16_t s_r0[2 * R0 * D];  // band 0 keys, then values
-  __shared__ __attribute__((aligned(16))) uint16_t s_r1[2 * R1 * D];  // band 1 keys, then values
+  __shared__ __attribute__((aligned(128))) uint16_t s_r0[2 * R0 * D];  // band 0 keys, then values
+  __shared__ __attribute__((aligned(128))) uint16_t s_r1[2 * R1 * D];  // band 1 keys, then values
   __shared__ __attribute__((aligned(16))) uint16_t s_q[2 * 2 * kTq * D];  // two buffers of 2 x 64 query rows
+  static_assert(R0 * D * 2 % 128 == 0 && R1 * D * 2 % 128 == 0, "band arrays must stay 128-byte aligned");
 
   const int G = gridDim.x;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -979,11 +976,9 @@ __global__ __launch_bounds__(1024) void llsa_fwd_ring_kernel(LlsaRingArgs a) {
     const WaveSeg<D, R1> ws1(s_r1, s_r1 + R1 * D, lane, f0 + a.base[1], a.lo[j][1] - a.base[1], a.nblk[j][1],
                              a.lo[j][1], a.hi[j][1], r0, wmax, t, valid, len, wq, slot1);
     f32x8 y0[NB0], y1[NB1];
-    float mx = fmaxf(seg_scores<D, NB0>(ws0, qf, c2, lane, y0), seg_scores<D, NB1>(ws1, qf, c2, lane, y1));
-    mx = max_over_column(mx);
-    mx = mx == kNegInf ? 0.f : mx;  // no key in the window (past the sequence's end)
-    seg_weights_pv<D, NB0>(ws0, y0, mx, acc, lsum);
-    seg_weights_pv<D, NB1>(ws1, y1, mx, acc, lsum);
+    const float mx = scaled_max(vmax(seg_scores<D, NB0>(ws0, qf, lane, y0), seg_scores<D, NB1>(ws1, qf, lane, y1)), c2);
+    seg_weights_pv<D, NB0>(ws0, y0, c2, mx, acc, lsum);
+    seg_weights_pv<D, NB1>(ws1, y1, c2, mx, acc, lsum);
     lsum = sum_over_column(lsum);
     const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
     store_rows_direct<D>(static_cast<uint16_t*>(a.out[j]) + slice, fs, r0, min(16, T - r0), acc,
@@ -1046,7 +1041,8 @@ bool plan_tile(const BandForwardArgs& a, int rows0, int rows1, TileArgs& d) {
       ts.lo = sg.lo_off;
       ts.hi = sg.hi_off;
       ts.shift = sg.lo_off - base;
-      ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + kSub) / kSub : 0;
+      // the waves' sub-blocks start up to 7 rows before their windows
+      ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + (ts.shift & 7) + kSub - 1) / kSub : 0;
       // every wave computes all of the kernel's sub-blocks of a band, the
       // last of them starting at row shift + 48 + 32 (blocks - 1)
       const int blocks = i == 0 ? kMaxBlocks0 : kMaxBlocks1;
@@ -1080,8 +1076,9 @@ bool launch_llsa_ring(const BandForwardArgs& a, int ntiles, float scale_log2, hi
       const BandSegment& sg = a.job[j].seg[i];
       r.lo[j][i] = sg.lo_off;
       r.hi[j][i] = sg.hi_off;
-      // an empty segment still reads one sub-block (fully masked)
-      const int n = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + kSub - 1) / kSub : 1;
+      // an empty segment still reads one sub-block (fully masked); the waves'
+      // sub-blocks start up to 7 rows before their windows
+      const int n = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + ((sg.lo_off - r.base[i]) & 7) + kSub - 1) / kSub : 1;
       r.nblk[j][i] = sg.lo_off <= sg.hi_off ? n : 0;
       nb[i] = nb[i] > n ? nb[i] : n;
       const long long need = static_cast<long long>(sg.lo_off) - r.base[i] + 48 + kSub * static_cast<long long>(n);

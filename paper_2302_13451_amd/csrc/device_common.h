@@ -292,15 +292,70 @@ __device__ __forceinline__ int ring_wrap(int o) {
   return static_cast<int>(u < w ? u : w);
 }
 
+// The same for a byte offset (o < 4 RR D).
+template <int D, int RR>
+__device__ __forceinline__ uint32_t ring_wrap_bytes(uint32_t o) {
+  const uint32_t w = o - static_cast<uint32_t>(2 * RR * D);
+  return o < w ? o : w;
+}
+
+// MFMA operand reads at 32-bit LDS byte addresses. An array whose base is a
+// multiple of 128 bytes keeps the low seven bits of its offsets, so the
+// other 16-byte pieces of a swizzled row are reached by XOR on the address
+// itself (base + (o ^ c) == (base + o) ^ c for c < 128), and the rows 4
+// further (same swizzle) by a constant that the read's offset field holds.
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)p));
+}
+__device__ __forceinline__ bf16x8 lds_rd8(uint32_t a) { return *(const lds_bf16x8*)(uintptr_t)a; }
+// transposing read (the lds_col8 pattern) of rows at byte address a and of the
+// rows 4 further, hi bytes on
+template <int HI>
+__device__ __forceinline__ bf16x8 lds_tr8_at(uint32_t a) {
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(uintptr_t)a);
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(uintptr_t)(a + HI));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Byte offsets of a lane's MFMA operand reads in the 32-row sub-blocks of a
+// swizzled band whose first sub-block starts at LDS row x0 (sub-block m at
+// rows x0 + 32 m, modulo RR rows when RR > 0; RR a multiple of 32, so the
+// swizzle survives the wrap). x0 must be a multiple of 8: then the lane's rows
+// xa and xa + 4 (row read) and xt and xt + 4 (transposing read) share their
+// swizzle and one 8-row block, which the wrap never splits, so the second
+// read of each pair is 8 D bytes after the first. Requires x0 + 32 m < 2 RR.
+template <int D, int RR>
+struct SubBlockAddr {
+  uint32_t ua, ut;  // row xa (row read), row xt (transposing read) of sub-block 0
+  __device__ __forceinline__ SubBlockAddr(int lane, int x0) {
+    const int col = lane & 15, g = lane >> 4;
+    ua = 2u * static_cast<uint32_t>(seg_row_off<D>(x0 + 8 * (col >> 2) + (col & 3), g));
+    ut = 2u * static_cast<uint32_t>(seg_tr_off<D>(x0 + 8 * g + (col >> 2), col));
+  }
+  __device__ __forceinline__ uint32_t wrap(uint32_t o) const {
+    if constexpr (RR > 0) o = ring_wrap_bytes<D, RR>(o);
+    return o;
+  }
+  // row read of sub-block m: piece 4 s + g of row xa is this XOR 64 s
+  __device__ __forceinline__ uint32_t row(int m) const { return wrap(ua + static_cast<uint32_t>(m * 64 * D)); }
+  // transposing read of sub-block m: the block of columns 16 i is this XOR 32 i
+  __device__ __forceinline__ uint32_t tr(int m) const { return wrap(ut + static_cast<uint32_t>(m * 64 * D)); }
+};
+
+// Maximum that propagates NaN (IEEE maximum): unlike fmaxf it needs no
+// canonicalising of its operands, and three of them fit one instruction.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 // Maximum and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 of a query
 // column, with the lane-swap instructions of gfx950 (each swap leaves x[l]
 // and x[l ^ 16] (x[l ^ 32]) in the two results of every lane, so every lane
 // gets the same value).
 __device__ __forceinline__ float max_over_column(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  x = vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
   r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float sum_over_column(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
