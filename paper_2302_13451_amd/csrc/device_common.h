@@ -35,14 +35,19 @@ __device__ __forceinline__ float bf2f(uint16_t u) {
   return __uint_as_float(static_cast<uint32_t>(u) << 16);
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to nearest even bfloat16, lo in the low half: one paired
+// conversion (v_cvt_pk_bf16_f32), where two scalar ones and a shift and merge
+// are what separate conversions compile to.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // c + x . y over 8 bfloat16 pairs (float accumulation, two pairs per
 // instruction). The pairs are taken with constant shuffles.
