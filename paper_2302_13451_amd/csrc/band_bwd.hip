@@ -490,7 +490,7 @@ struct BwdBands {
 // [r0 - La, r0 + 15 + Lb] starts at the same place in the first one; window
 // tests are made only in sub-blocks that cross a window edge. Accumulates
 // dv^T and (dk sqrt d)^T.
-template <int D, int RR>
+template <int D, int RR, bool EARLY>
 __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
                                              int nblk, float c2, int lane, f32x4* adv, f32x4* adk) {
   constexpr int NS = D / 32, NB = D / 16;
@@ -527,13 +527,33 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
     f32x4 dp0 = *reinterpret_cast<const f32x4*>(bd.ndn + st);
     f32x4 dp1 = *reinterpret_cast<const f32x4*>(bd.ndn + st + 4);
-    const uint32_t aq = xq + orow, ad = xd + orow;
+    const uint32_t aq = xq + orow, ad = xd + orow, tq = xq + otr, td = xd + otr;
+    // with EARLY every operand read of the sub-block goes out first: the
+    // transposed ones of the dv and dk products do not depend on the scores,
+    // so their latency hides behind the score products and the weights (32
+    // more registers: the tile kernel, at four waves per SIMD, reads them late)
+    bf16x8 rq[2 * NS], rd[2 * NS], tdo[NB], tqq[NB];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(aq ^ (64 * s)), kf[s], sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((aq ^ (64 * s)) + 8 * D), kf[s], sc1, 0, 0, 0);
-      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(ad ^ (64 * s)), vf[s], dp0, 0, 0, 0);
-      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((ad ^ (64 * s)) + 8 * D), vf[s], dp1, 0, 0, 0);
+      rq[2 * s] = lds_rd8(aq ^ (64 * s));
+      rq[2 * s + 1] = lds_rd8((aq ^ (64 * s)) + 8 * D);
+      rd[2 * s] = lds_rd8(ad ^ (64 * s));
+      rd[2 * s + 1] = lds_rd8((ad ^ (64 * s)) + 8 * D);
+    }
+    if constexpr (EARLY) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        tdo[i] = lds_tr8_at<8 * D>(td ^ (32 * i));
+        tqq[i] = lds_tr8_at<8 * D>(tq ^ (32 * i));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rq[2 * s], kf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rq[2 * s + 1], kf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rd[2 * s], vf[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rd[2 * s + 1], vf[s], dp1, 0, 0, 0);
     }
     const f32x4 l0 = *reinterpret_cast<const f32x4*>(bd.lse2 + st);
     const f32x4 l1 = *reinterpret_cast<const f32x4*>(bd.lse2 + st + 4);
@@ -557,18 +577,21 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
     const bf16x8 pf = __builtin_convertvector(x, bf16x8);
     const bf16x8 dsf = __builtin_convertvector(ds, bf16x8);
     // dv^T += dout^T P and dk^T += q^T dS, contracting over the 32 queries
-    const uint32_t tq = xq + otr, td = xd + otr;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(td ^ (32 * i)), pf, adv[i], 0, 0, 0);
-      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(tq ^ (32 * i)), dsf, adk[i], 0, 0, 0);
+      if constexpr (!EARLY) {
+        tdo[i] = lds_tr8_at<8 * D>(td ^ (32 * i));
+        tqq[i] = lds_tr8_at<8 * D>(tq ^ (32 * i));
+      }
+      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tdo[i], pf, adv[i], 0, 0, 0);
+      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tqq[i], dsf, adk[i], 0, 0, 0);
     }
   }
 }
 
 // Query role of one wave: queries r0 .. r0 + 15 against the key band, in the
 // same sub-block arrangement. Accumulates (dq sqrt d)^T.
-template <int D, int RR>
+template <int D, int RR, bool EARLY>
 __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
                                                int nblk, float c2, int lane, f32x4* aq) {
   constexpr int NS = D / 32, NB = D / 16;
@@ -604,13 +627,27 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
     const uint32_t orow = sa.row(m);
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
     f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
-    const uint32_t ak = xk + orow, av = xv + orow;
+    const uint32_t ak = xk + orow, av = xv + orow, tk = xk + sa.tr(m);
+    // every operand read of the sub-block goes out first (as in the key role)
+    bf16x8 rk[2 * NS], rv[2 * NS], tkk[NB];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(ak ^ (64 * s)), qf[s], sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((ak ^ (64 * s)) + 8 * D), qf[s], sc1, 0, 0, 0);
-      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8(av ^ (64 * s)), df[s], dp0, 0, 0, 0);
-      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_rd8((av ^ (64 * s)) + 8 * D), df[s], dp1, 0, 0, 0);
+      rk[2 * s] = lds_rd8(ak ^ (64 * s));
+      rk[2 * s + 1] = lds_rd8((ak ^ (64 * s)) + 8 * D);
+      rv[2 * s] = lds_rd8(av ^ (64 * s));
+      rv[2 * s + 1] = lds_rd8((av ^ (64 * s)) + 8 * D);
+    }
+    if constexpr (EARLY) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i) tkk[i] = lds_tr8_at<8 * D>(tk ^ (32 * i));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rk[2 * s], qf[s], sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rk[2 * s + 1], qf[s], sc1, 0, 0, 0);
+      dp0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rv[2 * s], df[s], dp0, 0, 0, 0);
+      dp1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rv[2 * s + 1], df[s], dp1, 0, 0, 0);
     }
     f32x8 x;
 #pragma unroll
@@ -627,10 +664,11 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
     for (int j = 0; j < 8; ++j) x[j] = fast_exp2(x[j]) * (j < 4 ? dp0[j] : dp1[j - 4]);
     const bf16x8 dsf = __builtin_convertvector(x, bf16x8);
     // dq^T += k^T dS^T, contracting over the 32 keys
-    const uint32_t tk = xk + sa.tr(m);
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(tk ^ (32 * i)), dsf, aq[i], 0, 0, 0);
+    for (int i = 0; i < NB; ++i) {
+      if constexpr (!EARLY) tkk[i] = lds_tr8_at<8 * D>(tk ^ (32 * i));
+      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tkk[i], dsf, aq[i], 0, 0, 0);
+    }
   }
 }
 
@@ -755,14 +793,14 @@ void sa_bwd_tile_kernel(BwdDev a) {
   const int nrows = min(16, T - r0);
   if (w < 4) {
     f32x4 adv[NB], adk[NB];
-    bwd_key_role<D, SEG>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
+    bwd_key_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
     __syncthreads();  // every wave is done with the bands
     uint16_t* stage = s_band + w * 2 * stage_elems<D>();
     store_tile_rows<D>(stage, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
     store_tile_rows<D>(stage + stage_elems<D>(), a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   } else {
     f32x4 aq[NB];
-    bwd_query_role<D, SEG>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, aq);
+    bwd_query_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, aq);
     __syncthreads();  // every wave is done with the bands
     store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
   }
@@ -977,12 +1015,12 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
     const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
     if (w < 4) {
       f32x4 adv[NB], adk[NB];
-      bwd_key_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
+      bwd_key_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
       store_rows_direct<D>(a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
       store_rows_direct<D>(a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
     } else {
       f32x4 aq[NB];
-      bwd_query_role<D, RR>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, aq);
+      bwd_query_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, aq);
       store_rows_direct<D>(a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
     }
     cur.next(st, H, a.B);
