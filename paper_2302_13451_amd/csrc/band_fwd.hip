@@ -472,6 +472,16 @@ template <int D, int NBM, int RR>
 __device__ __forceinline__ void seg_weights_pv(const WaveSeg<D, RR>& s, const f32x8* y, float c2, float mx,
                                                f32x4* acc, float& lsum) {
   constexpr int NB = D / 16;
+  // the value operands of the first sub-block are read before the weights
+  // are formed, those of sub-block m + 1 before the products of sub-block m,
+  // so their latency hides behind arithmetic
+  bf16x8 tv[2][NB];
+  {
+    const uint32_t t = s.val_addr(0);
+#pragma unroll
+    for (int i = 0; i < NB; ++i) tv[0][i] = lds_tr8_at<8 * D>(t ^ (32 * i));
+  }
+  __builtin_amdgcn_sched_barrier(0);
   bf16x8 pf[NBM];
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
@@ -483,10 +493,15 @@ __device__ __forceinline__ void seg_weights_pv(const WaveSeg<D, RR>& s, const f3
   }
 #pragma unroll
   for (int m = 0; m < NBM; ++m) {
-    const uint32_t t = s.val_addr(m);
+    if (m + 1 < NBM) {
+      const uint32_t t = s.val_addr(m + 1);
+#pragma unroll
+      for (int i = 0; i < NB; ++i) tv[(m + 1) & 1][i] = lds_tr8_at<8 * D>(t ^ (32 * i));
+      __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_tr8_at<8 * D>(t ^ (32 * i)), pf[m], acc[i], 0, 0, 0);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tv[m & 1][i], pf[m], acc[i], 0, 0, 0);
   }
 }
 
