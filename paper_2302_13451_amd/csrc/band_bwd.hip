@@ -28,6 +28,8 @@
 //
 // float path (VALU): one thread per query row computes dq, one thread per key
 // row computes dk and dv.
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -202,6 +204,7 @@ struct BwdDev {
   int ntiles;
   const int32_t* lengths;
   float scale, scale_log2;
+  float log2_scale;  // log2 of the score scale
 };
 
 __device__ __forceinline__ float dot8_bf16(u32x4 x, u32x4 y) {
@@ -489,7 +492,9 @@ struct BwdBands {
 // wave's nblk sub-blocks starts at band row 16 wq + 32 m, so the wave's window
 // [r0 - La, r0 + 15 + Lb] starts at the same place in the first one; window
 // tests are made only in sub-blocks that cross a window edge. Accumulates
-// dv^T and (dk sqrt d)^T.
+// dv^T and (dk sqrt d)^T. The first sub-block always meets the window (or the
+// wave has no valid key and its rows are stored as zeros), so it is computed
+// unconditionally and starts the accumulators.
 template <int D, int RR, bool EARLY>
 __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
                                              int nblk, float c2, int lane, f32x4* adv, f32x4* adk) {
@@ -506,8 +511,6 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
     kf[s] = seg_row8<D>(bd.k, kr, 32 * s + 8 * g);
     vf[s] = seg_row8<D>(bd.v, kr, 32 * s + 8 * g);
   }
-#pragma unroll
-  for (int i = 0; i < NB; ++i) adv[i] = adk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int wlo = max(0, r0 - La);
   const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
   const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
@@ -519,9 +522,9 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
   const int sb0 = 16 * wq;
   const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
   const uint32_t xq = lds_addr(bd.q), xd = lds_addr(bd.dout);
-  for (int m = 0; m < nblk; ++m) {
+  auto sub_block = [&](int m, auto first) {
+    constexpr bool F = decltype(first)::value;
     const int sb = sb0 + kSub * m, qb = bd.qbase + sb;
-    if (qb > whi || qb + kSub - 1 < wlo) continue;
     const uint32_t orow = sa.row(m), otr = sa.tr(m);
     const int st = bd.row(sb + 8 * g);  // statistics of rows sb + 8g .. + 7 (never split by the wrap)
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
@@ -583,17 +586,25 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
         tdo[i] = lds_tr8_at<8 * D>(td ^ (32 * i));
         tqq[i] = lds_tr8_at<8 * D>(tq ^ (32 * i));
       }
-      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tdo[i], pf, adv[i], 0, 0, 0);
-      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tqq[i], dsf, adk[i], 0, 0, 0);
+      adv[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tdo[i], pf, F ? f32x4{0.f, 0.f, 0.f, 0.f} : adv[i], 0, 0, 0);
+      adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tqq[i], dsf, F ? f32x4{0.f, 0.f, 0.f, 0.f} : adk[i], 0, 0, 0);
     }
+  };
+  sub_block(0, std::true_type{});
+  for (int m = 1; m < nblk; ++m) {
+    const int qb = bd.qbase + sb0 + kSub * m;
+    if (qb > whi || qb + kSub - 1 < wlo) continue;
+    sub_block(m, std::false_type{});
   }
 }
 
 // Query role of one wave: queries r0 .. r0 + 15 against the key band, in the
-// same sub-block arrangement. Accumulates (dq sqrt d)^T.
+// same sub-block arrangement (the first sub-block again unconditional).
+// Accumulates dq^T: lq is lse log2(e) minus log2 of the score scale, so the
+// weights, and with them dS and the product, come out already scaled.
 template <int D, int RR, bool EARLY>
 __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
-                                               int nblk, float c2, int lane, f32x4* aq) {
+                                               int nblk, float c2, float log2_scale, int lane, f32x4* aq) {
   constexpr int NS = D / 32, NB = D / 16;
   const int col = lane & 15, g = lane >> 4;
   const int me = r0 + col;
@@ -607,9 +618,7 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
     qf[s] = seg_row8<D>(bd.q, qr, 32 * s + 8 * g);
     df[s] = seg_row8<D>(bd.dout, qr, 32 * s + 8 * g);
   }
-  const float ndn = bd.ndn[qr], lse2 = bd.lse2[qr];
-#pragma unroll
-  for (int i = 0; i < NB; ++i) aq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float ndn = bd.ndn[qr], lq = bd.lse2[qr] - log2_scale;
   const int wlo = max(0, r0 - Lb);
   const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
   const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
@@ -621,9 +630,9 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
   const int sb0 = 16 * wq;
   const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
   const uint32_t xk = lds_addr(bd.k), xv = lds_addr(bd.v);
-  for (int m = 0; m < nblk; ++m) {
+  auto sub_block = [&](int m, auto first) {
+    constexpr bool F = decltype(first)::value;
     const int sb = sb0 + kSub * m, kb = bd.kbase + sb;
-    if (kb > whi || kb + kSub - 1 < wlo) continue;
     const uint32_t orow = sa.row(m);
     f32x4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = sc0;
     f32x4 dp0 = {ndn, ndn, ndn, ndn}, dp1 = dp0;
@@ -652,8 +661,8 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
     f32x8 x;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      x[j] = __builtin_fmaf(sc0[j], c2, -lse2);
-      x[j + 4] = __builtin_fmaf(sc1[j], c2, -lse2);
+      x[j] = __builtin_fmaf(sc0[j], c2, -lq);
+      x[j + 4] = __builtin_fmaf(sc1[j], c2, -lq);
     }
     if (!(kb >= ilo && kb + kSub - 1 <= ihi)) {
       const int d0 = kb + 8 * g - mylo_v;  // key kb + 8g + j is in my window iff 0 <= d0 + j <= span
@@ -667,8 +676,14 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       if constexpr (!EARLY) tkk[i] = lds_tr8_at<8 * D>(tk ^ (32 * i));
-      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tkk[i], dsf, aq[i], 0, 0, 0);
+      aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tkk[i], dsf, F ? f32x4{0.f, 0.f, 0.f, 0.f} : aq[i], 0, 0, 0);
     }
+  };
+  sub_block(0, std::true_type{});
+  for (int m = 1; m < nblk; ++m) {
+    const int kb = bd.kbase + sb0 + kSub * m;
+    if (kb > whi || kb + kSub - 1 < wlo) continue;
+    sub_block(m, std::false_type{});
   }
 }
 
@@ -800,9 +815,9 @@ void sa_bwd_tile_kernel(BwdDev a) {
     store_tile_rows<D>(stage + stage_elems<D>(), a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   } else {
     f32x4 aq[NB];
-    bwd_query_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, aq);
+    bwd_query_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, a.log2_scale, lane, aq);
     __syncthreads();  // every wave is done with the bands
-    store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
+    store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, nrows, aq, 1.f, valid, lane);
   }
 }
 
@@ -1020,8 +1035,8 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
       store_rows_direct<D>(a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
     } else {
       f32x4 aq[NB];
-      bwd_query_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, aq);
-      store_rows_direct<D>(a.dq + slice, fs, r0, nrows, aq, a.scale, valid, lane);
+      bwd_query_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, a.log2_scale, lane, aq);
+      store_rows_direct<D>(a.dq + slice, fs, r0, nrows, aq, 1.f, valid, lane);
     }
     cur.next(st, H, a.B);
     const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;
@@ -1048,6 +1063,7 @@ hipError_t launch_mfma(const SaBackwardArgs& a, hipStream_t stream) {
   d.lengths = a.lengths;
   d.scale = 1.f / sqrtf(static_cast<float>(a.d));
   d.scale_log2 = kLog2e * d.scale;
+  d.log2_scale = -0.5f * log2f(static_cast<float>(a.d));
   d.ntiles = (a.T + kC - 1) / kC;
   const int seg_rows = a.d == 64 ? Seg<64>::kRows : Seg<32>::kRows;
   const long long nblk = (16LL + a.Lb + a.La + kSub - 1) / kSub;
