@@ -496,20 +496,22 @@ struct BwdBands {
 // wave has no valid key and its rows are stored as zeros), so it is computed
 // unconditionally and starts the accumulators.
 template <int D, int RR, bool EARLY>
-__device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
-                                             int nblk, float c2, int lane, f32x4* adv, f32x4* adk) {
+__device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, const SubBlockAddr<D, RR>& sa, uint32_t own,
+                                             int r0, int wq, int len, int Lb, int La, int nblk, float c2, int lane,
+                                             f32x4* adv, f32x4* adk) {
   constexpr int NS = D / 32, NB = D / 16;
   const int col = lane & 15, g = lane >> 4;
   const int me = r0 + col;
   const bool valid = me < len;
-  const int mec = min(me, len - 1);  // lanes past the end read the last frame's rows, masked out
   const int wmax = min(r0 + 15, len - 1);
+  // the lane's own k and v rows (own: byte offset of its row read; a frame
+  // past the sequence's end holds the last frame, and is masked out)
   bf16x8 kf[NS], vf[NS];
-  const int kr = bd.row(mec - bd.kbase);
+  const uint32_t xk = lds_addr(bd.k) + own, xv = lds_addr(bd.v) + own;
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    kf[s] = seg_row8<D>(bd.k, kr, 32 * s + 8 * g);
-    vf[s] = seg_row8<D>(bd.v, kr, 32 * s + 8 * g);
+    kf[s] = lds_rd8(xk ^ (64 * s));
+    vf[s] = lds_rd8(xv ^ (64 * s));
   }
   const int wlo = max(0, r0 - La);
   const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
@@ -520,7 +522,6 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
   // every query of it (queries outside the sequence weigh zero anyway)
   const int ilo = wmax - La, ihi = r0 + Lb;
   const int sb0 = 16 * wq;
-  const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
   const uint32_t xq = lds_addr(bd.q), xd = lds_addr(bd.dout);
   auto sub_block = [&](int m, auto first) {
     constexpr bool F = decltype(first)::value;
@@ -603,20 +604,22 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, int r0, 
 // Accumulates dq^T: lq is lse log2(e) minus log2 of the score scale, so the
 // weights, and with them dS and the product, come out already scaled.
 template <int D, int RR, bool EARLY>
-__device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0, int wq, int len, int Lb, int La,
+__device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, const SubBlockAddr<D, RR>& sa,
+                                               uint32_t own, int qr, int r0, int wq, int len, int Lb, int La,
                                                int nblk, float c2, float log2_scale, int lane, f32x4* aq) {
   constexpr int NS = D / 32, NB = D / 16;
   const int col = lane & 15, g = lane >> 4;
   const int me = r0 + col;
   const bool valid = me < len;
-  const int mec = min(me, len - 1);
   const int wmax = min(r0 + 15, len - 1);
+  // the lane's own q and dout rows and statistics (ring row qr, row-read
+  // offset own; rows past the sequence's end have lse = +inf)
   bf16x8 qf[NS], df[NS];
-  const int qr = bd.row(mec - bd.qbase);
+  const uint32_t xq = lds_addr(bd.q) + own, xd = lds_addr(bd.dout) + own;
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    qf[s] = seg_row8<D>(bd.q, qr, 32 * s + 8 * g);
-    df[s] = seg_row8<D>(bd.dout, qr, 32 * s + 8 * g);
+    qf[s] = lds_rd8(xq ^ (64 * s));
+    df[s] = lds_rd8(xd ^ (64 * s));
   }
   const float ndn = bd.ndn[qr], lq = bd.lse2[qr] - log2_scale;
   const int wlo = max(0, r0 - Lb);
@@ -628,7 +631,6 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, int r0
   // valid query of the wave (and so inside the sequence)
   const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
   const int sb0 = 16 * wq;
-  const SubBlockAddr<D, RR> sa(lane, bd.slot0 + sb0);
   const uint32_t xk = lds_addr(bd.k), xv = lds_addr(bd.v);
   auto sub_block = [&](int m, auto first) {
     constexpr bool F = decltype(first)::value;
@@ -806,16 +808,22 @@ void sa_bwd_tile_kernel(BwdDev a) {
   const int nblk = (16 + Lb + La + kSub - 1) / kSub;  // sub-blocks per wave
   const BwdBands<D, SEG> bands{s_q, s_do, s_k, s_v, s_ndn, s_lse2, qbase, kbase, 0};
   const int nrows = min(16, T - r0);
+  // the lane's own band row (key role: in the key band, query role: in the
+  // query band) and the offsets of its reads
+  const int c_own = (w < 4 ? Lb : La) + 16 * (w & 3) + col;
+  const SubBlockAddr<D, SEG> sa(lane, 16 * (w & 3));
+  const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
   if (w < 4) {
     f32x4 adv[NB], adk[NB];
-    bwd_key_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
+    bwd_key_role<D, SEG, false>(bands, sa, own, r0, w & 3, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
     __syncthreads();  // every wave is done with the bands
     uint16_t* stage = s_band + w * 2 * stage_elems<D>();
     store_tile_rows<D>(stage, a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
     store_tile_rows<D>(stage + stage_elems<D>(), a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   } else {
     f32x4 aq[NB];
-    bwd_query_role<D, SEG, false>(bands, r0, w & 3, len, Lb, La, nblk, a.scale_log2, a.log2_scale, lane, aq);
+    bwd_query_role<D, SEG, false>(bands, sa, own, c_own, r0, w & 3, len, Lb, La, nblk, a.scale_log2, a.log2_scale,
+                                  lane, aq);
     __syncthreads();  // every wave is done with the bands
     store_tile_rows<D>(s_band + w * 2 * stage_elems<D>(), a.dq + slice, fs, r0, nrows, aq, 1.f, valid, lane);
   }
@@ -1016,6 +1024,11 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
 
   if (g0 >= g1) return;
   const int col = lane & 15, wq = w & 3;
+  // lane offsets that only shift from tile to tile: the sub-blocks' reads, the
+  // lane's own band row (key role: frame r0 + col at key-band row Lb + 16 wq +
+  // col; query role: at query-band row La + 16 wq + col) and its stores
+  const RingLaneBase<D, RR> rb(lane, (w < 4 ? Lb : La) + 16 * wq + col);
+  const int sloff = store_lane_offset<D>(fs, lane);
   TileCursor<1> cur;
   cur.seek(st, g0);
   int slot = 0;
@@ -1026,17 +1039,23 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
                                 s_ndn, s_lse2, f0 - La, f0 - Lb, slot};
     const int r0 = f0 + 16 * wq;
     const bool valid = r0 + col < len;
-    const int nrows = min(16, T - r0);
-    const size_t slice = row_index(cur.b, 0, cur.h, T, H, D);
+    const bool in_range = col < T - r0;
+    const size_t first = row_index(cur.b, r0, cur.h, T, H, D);
+    const int x0 = slot + 16 * wq;
+    const SubBlockAddr<D, RR> sa = rb.at(x0 >= RR ? x0 - RR : x0);
+    int own_row;
+    uint32_t own;
+    rb.own_at(slot, own_row, own);
     if (w < 4) {
       f32x4 adv[NB], adk[NB];
-      bwd_key_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
-      store_rows_direct<D>(a.dv + slice, fs, r0, nrows, adv, 1.f, valid, lane);
-      store_rows_direct<D>(a.dk + slice, fs, r0, nrows, adk, a.scale, valid, lane);
+      bwd_key_role<D, RR, true>(bands, sa, own, r0, wq, len, Lb, La, nblk, a.scale_log2, lane, adv, adk);
+      store_rows_at<D>(a.dv + first, sloff, in_range, adv, 1.f, valid, lane);
+      store_rows_at<D>(a.dk + first, sloff, in_range, adk, a.scale, valid, lane);
     } else {
       f32x4 aq[NB];
-      bwd_query_role<D, RR, true>(bands, r0, wq, len, Lb, La, nblk, a.scale_log2, a.log2_scale, lane, aq);
-      store_rows_direct<D>(a.dq + slice, fs, r0, nrows, aq, 1.f, valid, lane);
+      bwd_query_role<D, RR, true>(bands, sa, own, own_row, r0, wq, len, Lb, La, nblk, a.scale_log2,
+                                  a.log2_scale, lane, aq);
+      store_rows_at<D>(a.dq + first, sloff, in_range, aq, 1.f, valid, lane);
     }
     cur.next(st, H, a.B);
     const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;

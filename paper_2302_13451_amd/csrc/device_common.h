@@ -333,6 +333,7 @@ __device__ __forceinline__ bf16x8 lds_tr8_at(uint32_t a) {
 template <int D, int RR>
 struct SubBlockAddr {
   uint32_t ua, ut;  // row xa (row read), row xt (transposing read) of sub-block 0
+  __device__ __forceinline__ SubBlockAddr(uint32_t a, uint32_t t) : ua(a), ut(t) {}
   __device__ __forceinline__ SubBlockAddr(int lane, int x0) {
     const int col = lane & 15, g = lane >> 4;
     ua = 2u * static_cast<uint32_t>(seg_row_off<D>(x0 + 8 * (col >> 2) + (col & 3), g));
@@ -346,6 +347,46 @@ struct SubBlockAddr {
   __device__ __forceinline__ uint32_t row(int m) const { return wrap(ua + static_cast<uint32_t>(m * 64 * D)); }
   // transposing read of sub-block m: the block of columns 16 i is this XOR 32 i
   __device__ __forceinline__ uint32_t tr(int m) const { return wrap(ut + static_cast<uint32_t>(m * 64 * D)); }
+};
+
+// The lane offsets of SubBlockAddr, and of the row read of the lane's own
+// band row c, depend on where a band starts in its ring only through that
+// position modulo 32 rows, which is 0 or 16 for the multiples of 16 the
+// persistent kernels use: a wave computes both variants once and shifts them
+// per tile.
+template <int D, int RR>
+struct RingLaneBase {
+  uint32_t ua[2], ut[2];  // SubBlockAddr offsets of a first sub-block at LDS row 0 / 16
+  uint32_t own[2];        // row-read offset (piece g) of LDS row c / c + 16
+  int c;                  // band row of the lane's own frame
+  __device__ __forceinline__ RingLaneBase(int lane, int c_) : c(c_) {
+    const SubBlockAddr<D, 0> s0(lane, 0), s1(lane, 16);
+    ua[0] = s0.ua;
+    ua[1] = s1.ua;
+    ut[0] = s0.ut;
+    ut[1] = s1.ut;
+    const int g = lane >> 4;
+    own[0] = 2u * static_cast<uint32_t>(seg_row_off<D>(c, g));
+    own[1] = 2u * static_cast<uint32_t>(seg_row_off<D>(c + 16, g));
+  }
+  // sub-blocks starting at LDS row x0 (a multiple of 16, < RR)
+  __device__ __forceinline__ SubBlockAddr<D, RR> at(int x0) const {
+    const bool p = (x0 & 16) != 0;
+    const uint32_t sh = static_cast<uint32_t>((x0 & ~31) * 2 * D);
+    return SubBlockAddr<D, RR>((p ? ua[1] : ua[0]) + sh, (p ? ut[1] : ut[0]) + sh);
+  }
+  // ring row and row-read byte offset of the lane's own frame in a band that
+  // starts at ring row slot (a multiple of 16, slot + c < 2 RR)
+  __device__ __forceinline__ void own_at(int slot, int& row, uint32_t& off) const {
+    int u = slot + c;
+    uint32_t o = ((slot & 16) != 0 ? own[1] : own[0]) + static_cast<uint32_t>((slot & ~31) * 2 * D);
+    if (u >= RR) {
+      u -= RR;
+      o -= static_cast<uint32_t>(2 * RR * D);
+    }
+    row = u;
+    off = o;
+  }
 };
 
 // Maximum that propagates NaN (IEEE maximum): unlike fmaxf it needs no
@@ -374,12 +415,21 @@ __device__ __forceinline__ float sum_over_column(float x) {
 // of row col. Lanes g and g ^ 1 swap 4-feature pieces (permlane16 swap), so
 // that each lane holds whole 8-feature pieces: even g those of i = 0, 2, ...,
 // odd g those of i = 1, 3, ... Each store then writes 64 contiguous bytes of
-// 16 rows (whole rows for D = 32).
+// 16 rows (whole rows for D = 32). store_rows_at takes the wave's first row
+// (base = dst + r0 fs), the lane's element offset from it
+// (store_lane_offset, fixed for a kernel) and whether the lane's row is
+// written, so a persistent kernel computes the lane's part once.
 template <int D>
-__device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
-                                                  float mul, bool valid, int lane) {
-  constexpr int NB = D / 16;
+__device__ __forceinline__ int store_lane_offset(int fs, int lane) {
   const int g = lane >> 4, col = lane & 15;
+  // feature offset of piece j of this lane: 32 j + {0, 16, 8, 24}[g]
+  return col * fs + 8 * (g >> 1) + ((g & 1) == 0 ? 0 : 16);
+}
+template <int D>
+__device__ __forceinline__ void store_rows_at(uint16_t* base, int loff, bool in_range, const f32x4* acc, float mul,
+                                              bool valid, int lane) {
+  constexpr int NB = D / 16;
+  const int g = lane >> 4;
   const bool even = (g & 1) == 0;
   u32x2 p[NB];
 #pragma unroll
@@ -387,9 +437,7 @@ __device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0,
     p[i][0] = valid ? pack_bf16x2(acc[i][0] * mul, acc[i][1] * mul) : 0u;
     p[i][1] = valid ? pack_bf16x2(acc[i][2] * mul, acc[i][3] * mul) : 0u;
   }
-  // feature offset of piece j of this lane: 32 j + {0, 16, 8, 24}[g]
-  const int f0 = 8 * (g >> 1) + (even ? 0 : 16);
-  uint16_t* row = dst + (r0 + col) * fs + f0;
+  uint16_t* row = base + loff;
 #pragma unroll
   for (int j = 0; j < NB / 2; ++j) {
     u32x4 v;
@@ -402,8 +450,14 @@ __device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0,
       v[h] = even ? p[2 * j][h] : got;
       v[2 + h] = even ? got : p[2 * j + 1][h];
     }
-    if (col < nrows) st16(row + 32 * j, v);
+    if (in_range) st16(row + 32 * j, v);
   }
+}
+template <int D>
+__device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
+                                                  float mul, bool valid, int lane) {
+  store_rows_at<D>(dst + static_cast<size_t>(r0) * fs, store_lane_offset<D>(fs, lane), (lane & 15) < nrows, acc, mul,
+                   valid, lane);
 }
 
 // Workgroup barrier that orders LDS accesses only. __syncthreads() also waits
