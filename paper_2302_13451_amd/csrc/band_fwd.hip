@@ -391,14 +391,15 @@ struct WaveSeg {
   int qlo_l;           // this lane's first frame (1 << 30: empty window)
   unsigned qwidth;     // ... and the width of its window
   int ilo, ihi;        // frames inside the window of every valid query of the wave
-  // The first sub-block starts at the multiple of 8 at or below the window's
-  // row 16 wq + shift (nb counts the sub-blocks from there); slot0 and the
-  // ring size are multiples of 16 and 32.
+  // The first sub-block starts at the multiple of 16 at or below the window's
+  // row 16 wq + shift (nb counts the sub-blocks from there), where the
+  // swizzle keeps its reads free of bank conflicts; slot0 and the ring size
+  // are multiples of 16 and 32.
   __device__ __forceinline__ WaveSeg(const uint16_t* k, const uint16_t* v, int lane, int bbase, int shift, int nb,
                                      int lo, int hi, int r0, int wmax, int t, bool valid, int len, int wq,
                                      int slot0 = 0)
-      : Xk(lds_addr(k)), Xv(lds_addr(v)), sa(lane, slot0 + 16 * wq + (shift & ~7)) {
-    sb0 = 16 * wq + (shift & ~7);
+      : Xk(lds_addr(k)), Xv(lds_addr(v)), sa(lane, slot0 + 16 * wq + (shift & ~15)) {
+    sb0 = 16 * wq + (shift & ~15);
     kb0 = bbase + sb0;
     nblk = lo <= hi ? nb : 0;
     wlo = max(0, r0 + lo);
@@ -1056,8 +1057,8 @@ bool plan_tile(const BandForwardArgs& a, int rows0, int rows1, TileArgs& d) {
       ts.lo = sg.lo_off;
       ts.hi = sg.hi_off;
       ts.shift = sg.lo_off - base;
-      // the waves' sub-blocks start up to 7 rows before their windows
-      ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + (ts.shift & 7) + kSub - 1) / kSub : 0;
+      // the waves' sub-blocks start up to 15 rows before their windows
+      ts.nblk = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + (ts.shift & 15) + kSub - 1) / kSub : 0;
       // every wave computes all of the kernel's sub-blocks of a band, the
       // last of them starting at row shift + 48 + 32 (blocks - 1)
       const int blocks = i == 0 ? kMaxBlocks0 : kMaxBlocks1;
@@ -1092,8 +1093,8 @@ bool launch_llsa_ring(const BandForwardArgs& a, int ntiles, float scale_log2, hi
       r.lo[j][i] = sg.lo_off;
       r.hi[j][i] = sg.hi_off;
       // an empty segment still reads one sub-block (fully masked); the waves'
-      // sub-blocks start up to 7 rows before their windows
-      const int n = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + ((sg.lo_off - r.base[i]) & 7) + kSub - 1) / kSub : 1;
+      // sub-blocks start up to 15 rows before their windows
+      const int n = sg.lo_off <= sg.hi_off ? (16 + sg.hi_off - sg.lo_off + ((sg.lo_off - r.base[i]) & 15) + kSub - 1) / kSub : 1;
       r.nblk[j][i] = sg.lo_off <= sg.hi_off ? n : 0;
       nb[i] = nb[i] > n ? nb[i] : n;
       const long long need = static_cast<long long>(sg.lo_off) - r.base[i] + 48 + kSub * static_cast<long long>(n);
