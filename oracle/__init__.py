@@ -13,6 +13,8 @@ float64 arrays:
 * :func:`sa_backward`  -- Eq. 7-13 (explicit softmax Jacobian, M_n for the keys)
 * :func:`llsa_forward` -- Eq. 14/15, general channel form with an alias map
 * :func:`llsa_two_branch` / :func:`llsa_paper` -- the two instances used here
+* :func:`llsa_backward` / :func:`llsa_two_branch_backward` -- the exact adjoint
+  of the LLSA forward (Eq. 16 gives only its value part)
 * :class:`StreamOracle` -- the streaming step as a literal ring-buffer simulation
 
 Layouts: frame tensors are ``[B][T][H][d]``; log-sum-exp is ``[B][H][T]``.
@@ -64,10 +66,12 @@ def _load():
     lib.oracle_sa_backward.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, i, i, i, i, i, i, _IP, i]
     lib.oracle_llsa_forward.argtypes = [_DP, _DP, _DP, i, _IP, i, _IP, _IP, i, _DP, _DP,
                                         i, i, i, i, i, i, _IP, i]
+    lib.oracle_llsa_backward.argtypes = [_DP, _DP, _DP, _DP, i, _IP, i, _IP, _IP, i, _DP, _DP,
+                                         _DP, i, i, i, i, i, i, _IP, i]
     lib.oracle_sa_stream_step.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, i, _IP, _IP,
                                           i, i, i, i, i, _IP]
     for fn in (lib.oracle_sa_forward, lib.oracle_sa_backward, lib.oracle_llsa_forward,
-               lib.oracle_sa_stream_step):
+               lib.oracle_llsa_backward, lib.oracle_sa_stream_step):
         fn.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -168,6 +172,37 @@ def llsa_forward(q, k, v, alias, out_channels, q_branches, Lb: int, La: int, len
     return y, lse
 
 
+def llsa_backward(q, k, v, dy, alias, out_channels, q_branches, Lb: int, La: int, lengths=None,
+                  convention: str = "text", threads: int = 0):
+    """Gradient of the LLSA forward (same arguments as :func:`llsa_forward`)
+    for the output gradient ``dy [nout][B][T][H][d]``: the exact adjoint of
+    the forward's gather. Returns ``(dq, dk, dv)``, each
+    ``[nbranch][B][T][H][d]``."""
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    nb, B, T, H, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one shape")
+    alias = np.ascontiguousarray(np.asarray(alias, dtype=np.int32))
+    outc = np.ascontiguousarray(np.asarray(out_channels, dtype=np.int32))
+    qb = np.ascontiguousarray(np.asarray(q_branches, dtype=np.int32))
+    if alias.shape != (La + 1,):
+        raise ValueError("alias must have La + 1 entries")
+    if outc.shape != qb.shape:
+        raise ValueError("out_channels and q_branches must have the same length")
+    nout = outc.shape[0]
+    if dy.shape != (nout, B, T, H, d):
+        raise ValueError("dy must have shape %s" % ((nout, B, T, H, d),))
+    conv = {"text": 0, "eq14": 1}[convention]
+    ln = _lengths(lengths, B)
+    dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
+    rc = _load().oracle_llsa_backward(_dp(q), _dp(k), _dp(v), _dp(dy), nb, _ip(alias), nout,
+                                      _ip(outc), _ip(qb), conv, _dp(dq), _dp(dk), _dp(dv), B, T,
+                                      H, d, int(Lb), int(La), _ip(ln),
+                                      threads or default_threads())
+    _check(rc, "oracle_llsa_backward")
+    return dq, dk, dv
+
+
 # Branch indices of the two-branch LLSA tensors.
 CAUSAL = 0
 LOOKAHEAD = 1
@@ -184,6 +219,15 @@ def llsa_two_branch(q, k, v, Lb: int, La: int, lengths=None, threads: int = 0):
     alias = [CAUSAL] * La + [LOOKAHEAD]
     return llsa_forward(q, k, v, alias, [0, La], [CAUSAL, LOOKAHEAD], Lb, La, lengths,
                         "text", threads)
+
+
+def llsa_two_branch_backward(q, k, v, dy, Lb: int, La: int, lengths=None, threads: int = 0):
+    """Gradient of :func:`llsa_two_branch` for ``dy [2][B][T][H][d]``;
+    returns ``(dq, dk, dv)``, each ``[2][B][T][H][d]`` (index 0 = causal
+    branch, 1 = look-ahead branch)."""
+    alias = [CAUSAL] * La + [LOOKAHEAD]
+    return llsa_backward(q, k, v, dy, alias, [0, La], [CAUSAL, LOOKAHEAD], Lb, La, lengths,
+                         "text", threads)
 
 
 def llsa_paper(q, k, v, Lb: int, La: int, lengths=None, convention: str = "text",

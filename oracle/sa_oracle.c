@@ -18,6 +18,8 @@
  *   - LLSA forward: Eq. 14/15 in the general channel form, with a channel ->
  *     tensor alias map, so that both the paper's (A+1)-channel module and the
  *     two-branch (causal + look-ahead) variant are instances of it.
+ *   - LLSA backward: the exact adjoint of that forward, row by row as for
+ *     SA (the paper's Eq. 16 covers only the values).
  *   - SA streaming step: a literal simulation of per-stream ring buffers.
  *
  * Readings of the paper taken here (Sec. "Streaming Attention" is silent on
@@ -332,6 +334,134 @@ int oracle_llsa_forward(const double* q, const double* k, const double* v, int n
         }
         free(a); free(kr); free(vr);
       }
+    }
+  }
+  return err;
+}
+
+/* ------------------------------------------------------------------------ */
+/* LLSA backward, general channel form: the adjoint of the forward gather    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Same arguments as oracle_llsa_forward plus dy ([nout][B][T][H][d], the
+ * gradient of the loss with respect to each output); writes dq, dk, dv
+ * ([nbranch][B][T][H][d]). The paper gives the LLSA gradient only in part
+ * (Eq. 16, the values); here it is the exact adjoint of the forward, taken
+ * per output row exactly as for SA (Eq. 7-13): with a the row's weights over
+ * its window and g_j = dy . v_j, e = g J with J = diag(a) - a a^T (Eq. 9),
+ *   dq[q_branch] row t  += (1/sqrt d) sum_j e_j k_j          (Eq. 10)
+ *   dk[branch of j] row tau_j += (1/sqrt d) e_j q              (Eq. 11-13)
+ *   dv[branch of j] row tau_j += a_j dy                        (Eq. 7/8)
+ * where the window, and the branch every key/value frame comes from, are the
+ * forward's (the same channel map). Rows past a sequence's end get zero.
+ */
+int oracle_llsa_backward(const double* q, const double* k, const double* v, const double* dy,
+                         int nbranch, const int32_t* alias, int nout, const int32_t* out_channel,
+                         const int32_t* q_branch, int convention, double* dq, double* dk,
+                         double* dv, int B, int T, int H, int d, int Lb, int La,
+                         const int32_t* lengths, int threads) {
+  if (B < 0 || T < 0 || H < 0 || d <= 0 || Lb < 0 || La < 0 || nbranch <= 0 || nout < 0)
+    return ORC_ERR_INVALID;
+  if (convention != 0 && convention != 1) return ORC_ERR_INVALID;
+  if (!alias || (nout > 0 && (!out_channel || !q_branch))) return ORC_ERR_INVALID;
+  for (int c = 0; c <= La; ++c)
+    if (alias[c] < 0 || alias[c] >= nbranch) return ORC_ERR_INVALID;
+  for (int o = 0; o < nout; ++o) {
+    if (out_channel[o] < 0 || out_channel[o] > La) return ORC_ERR_INVALID;
+    if (q_branch[o] < 0 || q_branch[o] >= nbranch) return ORC_ERR_INVALID;
+  }
+  if (B == 0 || T == 0 || H == 0) return ORC_OK;
+  if (!q || !k || !v || !dq || !dk || !dv || (nout > 0 && !dy)) return ORC_ERR_INVALID;
+  const double scale = 1.0 / sqrt((double)d);
+  const size_t bstride = (size_t)B * T * H * d;
+  int err = ORC_OK;
+  /* one (sequence, head) per task: every write lands in its own rows */
+#pragma omp parallel for collapse(2) schedule(dynamic) num_threads(threads > 0 ? threads : 1)
+  for (int b = 0; b < B; ++b) {
+    for (int h = 0; h < H; ++h) {
+      const int len = clamp_len(lengths, b, T);
+      for (int br = 0; br < nbranch; ++br)
+        for (int t = 0; t < T; ++t) {
+          memset(dq + br * bstride + row_off(b, t, h, T, H, d), 0, sizeof(double) * (size_t)d);
+          memset(dk + br * bstride + row_off(b, t, h, T, H, d), 0, sizeof(double) * (size_t)d);
+          memset(dv + br * bstride + row_off(b, t, h, T, H, d), 0, sizeof(double) * (size_t)d);
+        }
+      double* a = (double*)malloc(sizeof(double) * (size_t)T);
+      double* g = (double*)malloc(sizeof(double) * (size_t)T);
+      double* e = (double*)malloc(sizeof(double) * (size_t)T);
+      double* J = (double*)malloc(sizeof(double) * (size_t)T * (size_t)T);
+      double* ytmp = (double*)malloc(sizeof(double) * (size_t)d);
+      long* tau = (long*)malloc(sizeof(long) * (size_t)T);
+      int* chb = (int*)malloc(sizeof(int) * (size_t)T);
+      const double** kr = (const double**)malloc(sizeof(double*) * (size_t)T);
+      const double** vr = (const double**)malloc(sizeof(double*) * (size_t)T);
+      if (!a || !g || !e || !J || !ytmp || !tau || !chb || !kr || !vr) {
+#pragma omp atomic write
+        err = ORC_ERR_NOMEM;
+        free(a); free(g); free(e); free(J); free(ytmp); free(tau); free(chb); free(kr); free(vr);
+        continue;
+      }
+      for (int o = 0; o < nout; ++o) {
+        const int c = out_channel[o];
+        const size_t qb = (size_t)q_branch[o] * bstride;
+        for (int t = 0; t < len; ++t) {
+          /* the forward's window and channel map (oracle_llsa_forward) */
+          long lo, hi;
+          if (convention == 0) {
+            lo = (long)t + c - La - Lb;
+            hi = (long)t + c;
+          } else {
+            lo = (long)t - c - Lb;
+            hi = (long)t + La - c;
+          }
+          lo = lmax(0, lo);
+          hi = lmin((long)len - 1, hi);
+          const int W = (int)(hi - lo + 1);
+          for (int j = 0; j < W; ++j) {
+            tau[j] = lo + j;
+            long ch;
+            if (convention == 0) {
+              ch = lmin(La, (long)t + c - tau[j]);
+            } else {
+              ch = (tau[j] <= (long)t - c) ? La : La - (tau[j] - ((long)t - c));
+            }
+            chb[j] = alias[ch];
+            kr[j] = k + (size_t)chb[j] * bstride + row_off(b, tau[j], h, T, H, d);
+            vr[j] = v + (size_t)chb[j] * bstride + row_off(b, tau[j], h, T, H, d);
+          }
+          const double* qt = q + qb + row_off(b, t, h, T, H, d);
+          attend_row(qt, kr, vr, W, d, a, ytmp);
+          const double* dyt = dy + (size_t)o * bstride + row_off(b, t, h, T, H, d);
+          for (int j = 0; j < W; ++j) {
+            double acc = 0.0;
+            for (int i = 0; i < d; ++i) acc += dyt[i] * vr[j][i];
+            g[j] = acc;
+          }
+          for (int i = 0; i < W; ++i)
+            for (int j = 0; j < W; ++j) J[(size_t)i * W + j] = a[i] * ((i == j ? 1.0 : 0.0) - a[j]);
+          for (int j = 0; j < W; ++j) {
+            double acc = 0.0;
+            for (int i = 0; i < W; ++i) acc += g[i] * J[(size_t)i * W + j];
+            e[j] = acc;
+          }
+          double* dqt = dq + qb + row_off(b, t, h, T, H, d);
+          for (int i = 0; i < d; ++i) {
+            double acc = 0.0;
+            for (int j = 0; j < W; ++j) acc += e[j] * kr[j][i];
+            dqt[i] += scale * acc;
+          }
+          for (int j = 0; j < W; ++j) {
+            double* dkj = dk + (size_t)chb[j] * bstride + row_off(b, tau[j], h, T, H, d);
+            double* dvj = dv + (size_t)chb[j] * bstride + row_off(b, tau[j], h, T, H, d);
+            for (int i = 0; i < d; ++i) {
+              dkj[i] += e[j] * (scale * qt[i]);
+              dvj[i] += a[j] * dyt[i];
+            }
+          }
+        }
+      }
+      free(a); free(g); free(e); free(J); free(ytmp); free(tau); free(chb); free(kr); free(vr);
     }
   }
   return err;
