@@ -120,6 +120,30 @@ int llsa_forward(const void* q, const void* k, const void* v, void* out, float* 
                  const int32_t* lengths, int dtype, void* stream);
 
 /*
+ * Two-branch LLSA backward: gradients of a loss l with respect to q, k, v of
+ * both branches given dout = dl/dout of both outputs, for llsa_forward with
+ * the same arguments. It is the adjoint of llsa_forward's gather (the paper's
+ * Eq. 16 gives only the value part): every output row contributes as in
+ * sa_backward (Eq. 7-13) over its window, the key/value rows of each frame
+ * tau going to the branch that frame was read from:
+ *   dq[j]_t  = (1/sqrt d) sum_tau dz_(t,tau) k[br(j,t,tau)]_tau
+ *   dk[i]_tau = (1/sqrt d) sum over (j, t) reading tau from branch i of dz_(t,tau) q[j]_t
+ *   dv[i]_tau = sum over the same (j, t) of a_(t,tau) dout[j]_t
+ * with dz = J^T (v . dout) per output row and J the softmax Jacobian.
+ *
+ * q, k, v, out, dout : [2][B][T][H][d] inputs; out is llsa_forward's output
+ * lse                : float [2][B][H][T] from llsa_forward (required)
+ * dq, dk, dv         : [2][B][T][H][d] outputs (padding frames written as 0)
+ * Supported: dtype SA_BF16, and windows whose bands fit one staged segment:
+ * every Lb + La <= 40 (104 at d = 32), and Lb + La <= 80 (208 at d = 32)
+ * when La <= 15. Other cases return SA_ERR_UNSUPPORTED.
+ */
+int llsa_backward(const void* q, const void* k, const void* v, const void* out,
+                  const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                  int B, int T, int H, int d, int Lb, int La,
+                  const int32_t* lengths, int dtype, void* stream);
+
+/*
  * One step of streaming SA inference (infer_sa) for S independent streams.
  * Per stream s with step counter u = step[s]:
  *   1. if 0 <= u < lengths[s], the new frame (q, k, v [s]) is stored in slot

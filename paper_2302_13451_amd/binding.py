@@ -37,6 +37,8 @@ _SIGNATURES = {
     "sa_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
                     _i, _vp],
     "llsa_forward": [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp],
+    "llsa_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
+                      _i, _vp],
     "sa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _vp,
                        _i, _vp],
     "sa_last_error": [],
@@ -178,6 +180,31 @@ def llsa_forward(q, k, v, Lb: int, La: int, lengths=None, out=None, lse=None, *,
                                        d, int(Lb), int(La), _ptr(lengths), code,
                                        _stream(q.device, stream)))
     return out, lse
+
+
+def llsa_backward(q, k, v, out, lse, dout, Lb: int, La: int, lengths=None, dq=None, dk=None,
+                  dv=None, *, stream=None):
+    """Two-branch LLSA backward. Every tensor is [2][B][T][H][d] (index 0 =
+    causal branch, 1 = look-ahead branch), lse [2][B][H][T] from
+    llsa_forward. Returns (dq, dk, dv)."""
+    two, B, T, H, d = q.shape
+    if two != 2:
+        raise SAError(SA_ERR_INVALID, "LLSA tensors must have a leading dimension of 2")
+    for n, t in (("q", q), ("k", k), ("v", v), ("out", out), ("dout", dout)):
+        _require(t, n, (2, B, T, H, d), q.dtype, q.device)
+    _require(lse, "lse", (2, B, H, T), torch.float32, q.device)
+    code = _dtype_code(q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _require(t, n, (2, B, T, H, d), q.dtype, q.device)
+    lengths = _lengths(lengths, B, q.device)
+    _check(load_library().llsa_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                        _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), B, T, H, d,
+                                        int(Lb), int(La), _ptr(lengths), code,
+                                        _stream(q.device, stream)))
+    return dq, dk, dv
 
 
 class StreamState:

@@ -488,17 +488,20 @@ struct BwdBands {
   }
 };
 
-// Key role of one wave: keys r0 .. r0 + 15 against the query band. Each of the
-// wave's nblk sub-blocks starts at band row 16 wq + 32 m, so the wave's window
-// [r0 - La, r0 + 15 + Lb] starts at the same place in the first one; window
-// tests are made only in sub-blocks that cross a window edge. Accumulates
-// dv^T and (dk sqrt d)^T. The first sub-block always meets the window (or the
-// wave has no valid key and its rows are stored as zeros), so it is computed
-// unconditionally and starts the accumulators.
-template <int D, int RR, bool EARLY>
+// Key role of one wave: keys r0 .. r0 + 15 against the query band. Query t
+// sees key tau for t - Lb <= tau <= t + La (Lb and La may be negative: a
+// window that does not contain its own frame). Each of the wave's nblk
+// sub-blocks starts at band row 16 wq + sbs + 32 m, where the first query that
+// sees key r0 sits at most 15 rows further (sbs a multiple of 16, band rows
+// from the first sub-block on hold finite data); window tests are made only in
+// sub-blocks that cross a window edge. Accumulates dv^T and (dk sqrt d)^T. The
+// first sub-block always meets the window (or the wave has no valid key and
+// its rows are stored as zeros), so it is computed unconditionally and starts
+// the accumulators, unless ACC continues them (a second window segment).
+template <int D, int RR, bool EARLY, bool ACC = false>
 __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, const SubBlockAddr<D, RR>& sa, uint32_t own,
                                              int r0, int wq, int len, int Lb, int La, int nblk, float c2, int lane,
-                                             f32x4* adv, f32x4* adk) {
+                                             f32x4* adv, f32x4* adk, int sbs = 0) {
   constexpr int NS = D / 32, NB = D / 16;
   const int col = lane & 15, g = lane >> 4;
   const int me = r0 + col;
@@ -516,12 +519,14 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, const Su
   const int wlo = max(0, r0 - La);
   const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + Lb);
   const int mylo = max(0, me - La), myhi = min(len - 1, me + Lb);  // queries that see me
-  const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
-  const int mylo_v = valid ? mylo : 1 << 30;
+  // (none when the window does not hold the key's own frame and is clipped away)
+  const bool seen = valid && myhi >= mylo;
+  const unsigned span = seen ? static_cast<unsigned>(myhi - mylo) : 0u;
+  const int mylo_v = seen ? mylo : 1 << 30;
   // a sub-block needs no window test when every valid key of the wave sees
   // every query of it (queries outside the sequence weigh zero anyway)
   const int ilo = wmax - La, ihi = r0 + Lb;
-  const int sb0 = 16 * wq;
+  const int sb0 = 16 * wq + sbs;
   const uint32_t xq = lds_addr(bd.q), xd = lds_addr(bd.dout);
   auto sub_block = [&](int m, auto first) {
     constexpr bool F = decltype(first)::value;
@@ -591,7 +596,7 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, const Su
       adk[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tqq[i], dsf, F ? f32x4{0.f, 0.f, 0.f, 0.f} : adk[i], 0, 0, 0);
     }
   };
-  sub_block(0, std::true_type{});
+  sub_block(0, std::integral_constant<bool, !ACC>{});
   for (int m = 1; m < nblk; ++m) {
     const int qb = bd.qbase + sb0 + kSub * m;
     if (qb > whi || qb + kSub - 1 < wlo) continue;
@@ -600,13 +605,15 @@ __device__ __forceinline__ void bwd_key_role(const BwdBands<D, RR>& bd, const Su
 }
 
 // Query role of one wave: queries r0 .. r0 + 15 against the key band, in the
-// same sub-block arrangement (the first sub-block again unconditional).
+// same sub-block arrangement (the first sub-block again unconditional; sbs
+// and ACC as in the key role).
 // Accumulates dq^T: lq is lse log2(e) minus log2 of the score scale, so the
 // weights, and with them dS and the product, come out already scaled.
-template <int D, int RR, bool EARLY>
+template <int D, int RR, bool EARLY, bool ACC = false>
 __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, const SubBlockAddr<D, RR>& sa,
                                                uint32_t own, int qr, int r0, int wq, int len, int Lb, int La,
-                                               int nblk, float c2, float log2_scale, int lane, f32x4* aq) {
+                                               int nblk, float c2, float log2_scale, int lane, f32x4* aq,
+                                               int sbs = 0) {
   constexpr int NS = D / 32, NB = D / 16;
   const int col = lane & 15, g = lane >> 4;
   const int me = r0 + col;
@@ -625,12 +632,14 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, const 
   const int wlo = max(0, r0 - Lb);
   const int whi = (wmax < r0) ? -1 : min(len - 1, wmax + La);
   const int mylo = max(0, me - Lb), myhi = min(len - 1, me + La);  // my window
-  const unsigned span = valid ? static_cast<unsigned>(myhi - mylo) : 0u;
-  const int mylo_v = valid ? mylo : 1 << 30;
+  // (empty when it does not hold the query's own frame and is clipped away)
+  const bool sees = valid && myhi >= mylo;
+  const unsigned span = sees ? static_cast<unsigned>(myhi - mylo) : 0u;
+  const int mylo_v = sees ? mylo : 1 << 30;
   // a sub-block needs no window test when it lies in the window of every
   // valid query of the wave (and so inside the sequence)
   const int ilo = max(0, wmax - Lb), ihi = min(r0 + La, len - 1);
-  const int sb0 = 16 * wq;
+  const int sb0 = 16 * wq + sbs;
   const uint32_t xk = lds_addr(bd.k), xv = lds_addr(bd.v);
   auto sub_block = [&](int m, auto first) {
     constexpr bool F = decltype(first)::value;
@@ -681,7 +690,7 @@ __device__ __forceinline__ void bwd_query_role(const BwdBands<D, RR>& bd, const 
       aq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tkk[i], dsf, F ? f32x4{0.f, 0.f, 0.f, 0.f} : aq[i], 0, 0, 0);
     }
   };
-  sub_block(0, std::true_type{});
+  sub_block(0, std::integral_constant<bool, !ACC>{});
   for (int m = 1; m < nblk; ++m) {
     const int kb = bd.kbase + sb0 + kSub * m;
     if (kb > whi || kb + kSub - 1 < wlo) continue;
@@ -1125,6 +1134,285 @@ hipError_t launch_valu(const SaBackwardArgs& a, hipStream_t stream) {
 hipError_t launch_sa_backward(const SaBackwardArgs& a, ElemType et, hipStream_t stream) {
   if (et == kBF16) return launch_mfma(a, stream);
   return launch_valu<float>(a, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Two-branch LLSA backward: the adjoint of the LLSA forward (Eq. 14/15). Each
+// output j reads, per query t, two window segments, one from each branch i:
+// keys tau in [t + lo[j][i], t + hi[j][i]]. Every (output, branch) segment is
+// an SA-type band relation with its own offsets, so its gradient is the SA
+// backward's (Eq. 7-13) with the segment's window, the output's lse and
+// D_t = dout_t . out_t, and the weights P = exp(s - lse) already normalised
+// over the whole window. The gradients sum over segments:
+//   dq[j] = sum_i (query role of segment (j, i)),
+//   dk[i], dv[i] = sum_j (key role of segment (j, i)).
+namespace {
+
+struct LlsaBwdDev {
+  const uint16_t *q[2], *o[2], *dout[2], *k[2], *v[2];
+  const float* lse[2];
+  uint16_t *dq[2], *dk[2], *dv[2];
+  int B, T, H, ntiles;
+  const int32_t* lengths;
+  float scale, scale_log2, log2_scale;
+  int lo[2][2], hi[2][2];  // segment (output j, branch i); lo > hi: empty
+  int qoff[2];             // frame of query band j's row 0, relative to the tile's first frame
+  int koff[2];             // frame of key band i's row 0, relative to the tile's first frame
+};
+
+// One workgroup of 16 waves per (sequence, head, 64-frame tile). LDS holds
+// the key and value bands of both branches and the query and dout bands of
+// both outputs (SEG rows each, frames outside the sequence zero-filled), and
+// -D and lse log2(e) of both query bands. Waves 0-3 / 4-7 take the query role
+// of output 0 / 1 (both segments), waves 8-11 / 12-15 the key role of branch
+// 0 / 1 (both outputs); each wave owns 16 rows and stores them.
+template <int D>
+__global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
+  constexpr int NT = 1024;
+  constexpr int SEG = Seg<D>::kRows;
+  constexpr int NS = D / 32, NB = D / 16;
+  constexpr int NB16 = SEG / 16;            // 16-row blocks of one D product
+  constexpr int BPW = (2 * NB16 + 15) / 16;  // ... of both, per wave
+  static_assert(SEG % 16 == 0, "the D product covers the band in 16-row blocks");
+  __shared__ __attribute__((aligned(128))) uint16_t s_band[8 * SEG * D];
+  __shared__ __attribute__((aligned(16))) float s_stat[4 * SEG];  // -D and lse log2(e) of query bands 0, 1
+  // band x of the eight (q, dout of output 0; q, dout of output 1; k, v of
+  // branch 0; k, v of branch 1) starts at s_band + x SEG D
+  auto band = [&](int x) { return s_band + x * SEG * D; };
+  auto s_qb = [&](int j) { return band(2 * j); };      // q of output j
+  auto s_db = [&](int j) { return band(2 * j + 1); };  // dout of output j
+  auto s_kb = [&](int i) { return band(4 + 2 * i); };  // k of branch i
+  auto s_vb = [&](int i) { return band(5 + 2 * i); };  // v of branch i
+
+  int bh, tile;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int T = a.T, H = a.H;
+  const int len = clamp_len_uniform(a.lengths, b, T);
+  const int f0 = tile * kC;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, g = lane >> 4;
+
+  if (f0 >= len) {  // padding tile
+    for (int j = 0; j < 2; ++j) {
+      zero_rows<D, NT>(a.dq[j], nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
+      zero_rows<D, NT>(a.dk[j], a.dv[j], b, h, T, H, f0, min(f0 + kC, T), tid);
+    }
+    return;
+  }
+  const size_t slice = row_index(b, 0, h, T, H, D);
+  const int fs = H * D;
+  int qbase[2], kbase[2], blo[4], bhi[4];
+  for (int j = 0; j < 2; ++j) {
+    qbase[j] = f0 + a.qoff[j];
+    kbase[j] = f0 + a.koff[j];
+    blo[j] = max(0, -qbase[j]);
+    bhi[j] = min(SEG, len - qbase[j]);
+    blo[2 + j] = max(0, -kbase[j]);
+    bhi[2 + j] = min(SEG, len - kbase[j]);
+  }
+  for (int j = 0; j < 2; ++j) {
+    seg_issue_rows<D, 16>(s_qb(j), a.q[j] + slice, fs, qbase[j], blo[j], bhi[j], w, lane);
+    seg_issue_rows<D, 16>(s_db(j), a.dout[j] + slice, fs, qbase[j], blo[j], bhi[j], w, lane);
+    seg_issue_rows<D, 16>(s_kb(j), a.k[j] + slice, fs, kbase[j], blo[2 + j], bhi[2 + j], w, lane);
+    seg_issue_rows<D, 16>(s_vb(j), a.v[j] + slice, fs, kbase[j], blo[2 + j], bhi[2 + j], w, lane);
+  }
+  // out rows of both query bands as the B operand of the D products (zero
+  // outside the sequence): wave w takes the 16-row blocks w, w + 16, ... of
+  // the 2 NB16 blocks (band j = blk / NB16)
+  bf16x8 of[BPW][NS];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int blk = w + 16 * i;
+    const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
+    const int fr = qbase[jb] + 16 * rb + col;
+    const bool in = blk < 2 * NB16 && fr >= 0 && fr < len;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      of[i][s] = bf16x8{};
+      if (in) of[i][s] = __builtin_bit_cast(bf16x8, ld16(a.o[jb] + slice + (fr * fs + 32 * s + 8 * g)));
+    }
+  }
+  // lse of both query bands: thread j SEG + r holds row r of band j
+  float lsev = 0.f;
+  const int lj = tid >= SEG ? 1 : 0, lr = tid - lj * SEG;
+  const int lfr = qbase[lj] + lr;
+  const bool lin = tid < 2 * SEG && lfr >= 0 && lfr < len;
+  if (lin) lsev = a.lse[lj][(static_cast<size_t>(b) * H + h) * T + lfr];
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const int bi = x < 4 ? x / 2 : 2 + (x - 4) / 2;  // its row range: query band j or key band 2 + i
+    if (blo[bi] > 0) seg_zero_rows<D, NT>(band(x), 0, min(blo[bi], SEG), tid);
+    if (bhi[bi] < SEG) seg_zero_rows<D, NT>(band(x), max(bhi[bi], 0), SEG, tid);
+  }
+  __syncthreads();
+  if (tid < 2 * SEG) s_stat[2 * SEG * lj + SEG + lr] = lin ? lsev * kLog2e : __builtin_huge_valf();
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int blk = w + 16 * i;
+    if (blk < 2 * NB16) {
+      const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
+      f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(seg_row8<D>(s_db(jb), 16 * rb + col, 32 * s + 8 * g), of[i][s],
+                                                     dd, 0, 0, 0);
+      // the diagonal entry of row 16 rb + col sits in lane g = col / 4, element col % 4
+      const int e = col & 3;
+      const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
+      if ((col >> 2) == g) s_stat[2 * SEG * jb + 16 * rb + col] = -dg;
+    }
+  }
+  __syncthreads();
+
+  const int wq = w & 3, role = w >> 2;  // 0, 1: query role of output role; 2, 3: key role of branch role - 2
+  const int r0 = f0 + 16 * wq;
+  const bool valid = r0 + col < len;
+  const int nrows = min(16, T - r0);
+  // the window of segment (j, i) in the role functions' terms: t - Lb .. t + La
+  auto seg_nonempty = [&](int j, int i) { return a.lo[j][i] <= a.hi[j][i]; };
+  if (role < 2) {
+    const int j = role;
+    f32x4 aq[NB];
+    bool any = false;
+    const int c_own = 16 * wq + col - a.qoff[j];  // query band row of frame r0 + col
+    const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
+    for (int i = 1; i >= 0; --i) {  // branch L first: its segment is never empty
+      if (!seg_nonempty(j, i)) continue;
+      const BwdBands<D, SEG> bd{s_qb(j), s_db(j), s_kb(i), s_vb(i), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
+                                qbase[j], kbase[i], 0};
+      const int lo = a.lo[j][i], hi = a.hi[j][i];
+      const int rel = lo - a.koff[i];  // key band row of the first key of query f0
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
+      if (!any)
+        bwd_query_role<D, SEG, false, false>(bd, sa, own, c_own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
+                                             a.log2_scale, lane, aq, sbs);
+      else
+        bwd_query_role<D, SEG, false, true>(bd, sa, own, c_own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
+                                            a.log2_scale, lane, aq, sbs);
+      any = true;
+    }
+    store_rows_direct<D>(a.dq[j] + slice, fs, r0, nrows, aq, 1.f, valid && any, lane);
+  } else {
+    const int i = role - 2;
+    f32x4 adv[NB], adk[NB];
+    bool any = false;
+    const int c_own = 16 * wq + col - a.koff[i];  // key band row of frame r0 + col
+    const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
+    for (int j = 0; j < 2; ++j) {
+      if (!seg_nonempty(j, i)) continue;
+      const BwdBands<D, SEG> bd{s_qb(j), s_db(j), s_kb(i), s_vb(i), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
+                                qbase[j], kbase[i], 0};
+      const int lo = a.lo[j][i], hi = a.hi[j][i];
+      const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
+      if (!any)
+        bwd_key_role<D, SEG, false, false>(bd, sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk,
+                                           sbs);
+      else
+        bwd_key_role<D, SEG, false, true>(bd, sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk,
+                                          sbs);
+      any = true;
+    }
+    store_rows_direct<D>(a.dv[i] + slice, fs, r0, nrows, adv, 1.f, valid && any, lane);
+    store_rows_direct<D>(a.dk[i] + slice, fs, r0, nrows, adk, a.scale, valid && any, lane);
+  }
+}
+
+}  // namespace
+
+namespace {
+
+// The segments of the two outputs and the bands' origins (relative to a
+// tile's first frame); false when some wave would read past its band.
+bool llsa_bwd_geometry(int d, int Lb, int La, LlsaBwdDev& a) {
+  // output 0 (causal): branch 1 (L) for t-La-Lb .. t-La, branch 0 (C) for t-La+1 .. t
+  // output 1 (look-ahead): branch 1 for t-Lb .. t, branch 0 for t+1 .. t+La
+  a.lo[0][1] = -(La + Lb);
+  a.hi[0][1] = -La;
+  a.lo[0][0] = -La + 1;
+  a.hi[0][0] = 0;
+  a.lo[1][1] = -Lb;
+  a.hi[1][1] = 0;
+  a.lo[1][0] = 1;
+  a.hi[1][0] = La;
+  // band origins: every segment's first key (query role) and first query
+  // (key role) inside its band, and each role's own 64 rows
+  for (int i = 0; i < 2; ++i) {
+    int m = 0;
+    for (int j = 0; j < 2; ++j)
+      if (a.lo[j][i] <= a.hi[j][i]) m = m < a.lo[j][i] ? m : a.lo[j][i];
+    a.koff[i] = m;
+  }
+  for (int j = 0; j < 2; ++j) {
+    int m = 0;
+    for (int i = 0; i < 2; ++i)
+      if (a.lo[j][i] <= a.hi[j][i]) m = m < -a.hi[j][i] ? m : -a.hi[j][i];
+    a.qoff[j] = m;
+  }
+  // every row a wave reads must lie in its band: 48 + sbs + 32 nblk rows from
+  // the band's origin (and the 64 own rows)
+  const int seg_rows = d == 64 ? Seg<64>::kRows : Seg<32>::kRows;
+  auto fits = [&](int rel, int lo, int hi) {
+    const long long nb = (16LL + hi - lo + (rel & 15) + kSub - 1) / kSub;
+    return rel >= 0 && 48LL + (rel & ~15) + kSub * nb <= seg_rows;
+  };
+  for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < 2; ++i) {
+      if (a.lo[j][i] > a.hi[j][i]) continue;
+      if (!fits(a.lo[j][i] - a.koff[i], a.lo[j][i], a.hi[j][i])) return false;
+      if (!fits(-a.hi[j][i] - a.qoff[j], a.lo[j][i], a.hi[j][i])) return false;
+    }
+  for (int i = 0; i < 2; ++i)
+    if (64 - a.koff[i] > seg_rows || 64 - a.qoff[i] > seg_rows) return false;
+  return true;
+}
+
+}  // namespace
+
+bool llsa_backward_fits(int d, int Lb, int La) {
+  LlsaBwdDev a{};
+  return llsa_bwd_geometry(d, Lb, La, a);
+}
+
+hipError_t launch_llsa_backward(const LlsaBackwardArgs& x, ElemType et, hipStream_t stream) {
+  if (et != kBF16) return hipErrorNotSupported;
+  LlsaBwdDev a{};
+  if (!llsa_bwd_geometry(x.d, x.Lb, x.La, a)) return hipErrorNotSupported;
+  const size_t branch = static_cast<size_t>(x.B) * x.T * x.H * x.d;
+  for (int j = 0; j < 2; ++j) {
+    a.q[j] = static_cast<const uint16_t*>(x.q) + j * branch;
+    a.o[j] = static_cast<const uint16_t*>(x.out) + j * branch;
+    a.dout[j] = static_cast<const uint16_t*>(x.dout) + j * branch;
+    a.k[j] = static_cast<const uint16_t*>(x.k) + j * branch;
+    a.v[j] = static_cast<const uint16_t*>(x.v) + j * branch;
+    a.lse[j] = x.lse + j * static_cast<size_t>(x.B) * x.H * x.T;
+    a.dq[j] = static_cast<uint16_t*>(x.dq) + j * branch;
+    a.dk[j] = static_cast<uint16_t*>(x.dk) + j * branch;
+    a.dv[j] = static_cast<uint16_t*>(x.dv) + j * branch;
+  }
+  a.B = x.B;
+  a.T = x.T;
+  a.H = x.H;
+  a.ntiles = (x.T + kC - 1) / kC;
+  a.lengths = x.lengths;
+  a.scale = 1.f / sqrtf(static_cast<float>(x.d));
+  a.scale_log2 = kLog2e * a.scale;
+  a.log2_scale = -0.5f * log2f(static_cast<float>(x.d));
+  const int grid = xcd_slice_grid(x.B * x.H, a.ntiles);
+  if (x.d == 64)
+    hipLaunchKernelGGL(llsa_bwd_tile_kernel<64>, dim3(grid), dim3(1024), 0, stream, a);
+  else
+    hipLaunchKernelGGL(llsa_bwd_tile_kernel<32>, dim3(grid), dim3(1024), 0, stream, a);
+  return hipGetLastError();
 }
 
 }  // namespace sa

@@ -194,6 +194,40 @@ int llsa_forward(const void* q, const void* k, const void* v, void* out, float* 
                       fn);
 }
 
+int llsa_backward(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                  const void* dout, void* dq, void* dk, void* dv, int B, int T, int H, int d, int Lb,
+                  int La, const int32_t* lengths, int dtype, void* stream) {
+  const char* fn = "llsa_backward";
+  if (int rc = check_shape(fn, B, T, H, d, Lb, La, dtype)) return rc;
+  if (dtype != SA_BF16) return fail(SA_ERR_UNSUPPORTED, "%s: only bfloat16 is supported", fn);
+  if (B == 0 || T == 0 || H == 0) return SA_OK;
+  if (!lse) return fail(SA_ERR_NULL, "%s: lse (from llsa_forward) is required", fn);
+  if (int rc = check_ptrs(fn, {q, k, v, out, dout, dq, dk, dv}, {lse}, {lengths})) return rc;
+  Lb = Lb < T ? Lb : T;
+  La = La < T ? La : T;
+  if (!sa::llsa_backward_fits(d, Lb, La))
+    return fail(SA_ERR_UNSUPPORTED, "%s: window Lb = %d, La = %d too wide for d = %d", fn, Lb, La, d);
+  sa::LlsaBackwardArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.dout = dout;
+  a.lse = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.B = B;
+  a.T = T;
+  a.H = H;
+  a.d = d;
+  a.Lb = Lb;
+  a.La = La;
+  a.lengths = lengths;
+  return check_launch(sa::launch_llsa_backward(a, elem(dtype), static_cast<hipStream_t>(stream)),
+                      fn);
+}
+
 int sa_stream_step(const void* q, const void* k, const void* v, void* out, void* q_ring,
                    void* k_ring, void* v_ring, int R, int32_t* step, int32_t* emitted_t, int S,
                    int H, int d, int Lb, int La, const int32_t* lengths, int dtype, void* stream) {

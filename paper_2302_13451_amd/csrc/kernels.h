@@ -52,6 +52,22 @@ struct SaBackwardArgs {
 
 hipError_t launch_sa_backward(const SaBackwardArgs& a, ElemType et, hipStream_t stream);
 
+// Two-branch LLSA backward; every tensor but lse is [2][B][T][H][d] (index 0:
+// causal branch, 1: look-ahead branch), lse is [2][B][H][T]. bfloat16 only.
+struct LlsaBackwardArgs {
+  const void *q, *k, *v, *out, *dout;
+  const float* lse;
+  void *dq, *dk, *dv;
+  int B, T, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+hipError_t launch_llsa_backward(const LlsaBackwardArgs& a, ElemType et, hipStream_t stream);
+
+// Whether launch_llsa_backward supports the window (its bands must fit the
+// staged segment).
+bool llsa_backward_fits(int d, int Lb, int La);
+
 struct StreamStepArgs {
   const void *q, *k, *v;
   void* out;

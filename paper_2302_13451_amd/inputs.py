@@ -85,9 +85,12 @@ def sa_inputs(B: int, T: int, H: int, d: int, seed: int, *, dtype: str = "bf16",
 
 def llsa_inputs(B: int, T: int, H: int, d: int, seed: int, *, dtype: str = "bf16",
                 scale="rsqrt_d", peak: float = 1.0, lengths: LengthSpec = "full",
-                pad_value: float = 0.0) -> dict:
+                pad_value: float = 0.0, with_dout: bool = False) -> dict:
     """Two-branch q, k, v as float32 CPU tensors ``[2][B][T][H][d]``
-    (index 0 = causal branch, 1 = look-ahead branch); ``lengths`` int32 ``[B]``."""
+    (index 0 = causal branch, 1 = look-ahead branch); ``lengths`` int32 ``[B]``;
+    with ``with_dout`` also the gradient of both outputs, ``dout`` N(0, 1)
+    ``[2][B][T][H][d]``, drawn after the lengths (so q, k, v and the lengths
+    do not depend on it)."""
     g = torch.Generator(device="cpu").manual_seed(int(seed))
     s = _scale(scale, d) * float(peak)
     q = torch.randn(2, B, T, H, d, generator=g) * s
@@ -95,6 +98,8 @@ def llsa_inputs(B: int, T: int, H: int, d: int, seed: int, *, dtype: str = "bf16
     v = torch.randn(2, B, T, H, d, generator=g) * s
     ln = _draw_lengths(g, B, T, lengths)
     out = {"q": q, "k": k, "v": v}
+    if with_dout:
+        out["dout"] = torch.randn(2, B, T, H, d, generator=g)
     for name in list(out):
         out[name] = _pad(_round(out[name], dtype), ln, pad_value, 2)
     out["lengths"] = ln

@@ -27,10 +27,10 @@ def lib():
     return bd.load_library()
 
 
-def test_header_declares_the_four_entry_points():
+def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("sa_forward", "sa_backward", "llsa_forward", "sa_stream_step", "sa_last_error",
-              "sa_abi_version"):
+    for n in ("sa_forward", "sa_backward", "llsa_forward", "llsa_backward", "sa_stream_step",
+              "sa_last_error", "sa_abi_version"):
         assert n in names
 
 
@@ -82,6 +82,22 @@ def test_llsa_validation(lib):
     assert ll(q=None) == bd.SA_ERR_NULL
     assert ll(La=-1) == bd.SA_ERR_INVALID
     assert ll(d=100) == bd.SA_ERR_UNSUPPORTED
+
+
+def test_llsa_backward_validation(lib):
+    def lb(lse=FAKE, dv=FAKE, B=2, Lb=2, La=1, d=64, dtype=bd.SA_BF16):
+        return lib.llsa_backward(FAKE, FAKE, FAKE, FAKE, lse, FAKE, FAKE, FAKE, dv, B, 8, 2, d,
+                                 Lb, La, None, dtype, None)
+    assert lb(B=0) == bd.SA_OK
+    assert lb(lse=None) == bd.SA_ERR_NULL
+    assert lb(dv=None) == bd.SA_ERR_NULL
+    assert lb(dv=FAKE_ODD) == bd.SA_ERR_INVALID
+    assert lb(La=-1) == bd.SA_ERR_INVALID
+    assert lb(d=16) == bd.SA_ERR_UNSUPPORTED
+    assert lb(dtype=bd.SA_F32) == bd.SA_ERR_UNSUPPORTED       # bfloat16 only
+    assert lib.llsa_backward(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 200, 2, 64,
+                             70, 20, None, bd.SA_BF16, None) == bd.SA_ERR_UNSUPPORTED  # window too wide
+    assert "too wide" in lib.sa_last_error().decode()
 
 
 def test_stream_validation(lib):
