@@ -9,7 +9,8 @@ HBM before timing; four copies of the batch are rotated so that no step finds
 its inputs in the 256 MB Infinity Cache.
 
 The same run also times, on their own workloads:
-  * llsa_forward, two-branch, same shapes (rows "llsa");
+  * llsa_forward and llsa_backward, two-branch, same shapes (rows "llsa",
+    "llsa_backward");
   * sa_stream_step, 64 streams x 1000 steps, ring of 64 + 8 + 1 frames, eager
     and replayed from a HIP graph (row "stream");
   * masked full attention in PyTorch (dense T x T scores, band mask) as the
@@ -175,14 +176,17 @@ def launch_ms(fn, sets, n):
 
 def bench_llsa(steps, warmup):
     w = WORKLOAD
-    x = llsa_inputs(w["B"], w["T"], w["H"], w["d"], 4, dtype="bf16", lengths=w["lengths"])
-    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v")}
+    x = llsa_inputs(w["B"], w["T"], w["H"], w["d"], 4, dtype="bf16", lengths=w["lengths"],
+                    with_dout=True)
+    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v", "dout")}
     lengths = x["lengths"].cuda()
     sets = []
     for i in range(N_SETS):
         s = {n: (t if i == 0 else t.clone()) for n, t in base.items()}
         s["out"] = torch.empty_like(s["q"])
         s["lse"] = torch.empty(2, w["B"], w["H"], w["T"], dtype=torch.float32, device="cuda")
+        for n in ("dq", "dk", "dv"):
+            s[n] = torch.empty_like(s["q"])
         sets.append(s)
     for i in range(warmup):
         s = sets[i % N_SETS]
@@ -194,7 +198,32 @@ def bench_llsa(steps, warmup):
     L = x["lengths"].tolist()
     byts = acc.llsa_forward_bytes(L, w["H"], w["d"])
     flops = acc.llsa_forward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
-    return {
+
+    def bwd(s):
+        bd.llsa_backward(s["q"], s["k"], s["v"], s["out"], s["lse"], s["dout"], w["Lb"], w["La"],
+                         lengths, dq=s["dq"], dk=s["dk"], dv=s["dv"])
+
+    for i in range(warmup):
+        bwd(sets[i % N_SETS])
+    torch.cuda.synchronize()
+    bms = launch_ms(bwd, sets, steps)
+    bbyts = acc.llsa_backward_bytes(L, w["H"], w["d"])
+    bflops = acc.llsa_backward_flops(L, w["H"], w["d"], w["Lb"], w["La"])
+    backward = {
+        "workload": "LLSA backward (two-branch) bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, "
+                    "lengths U[400,800]",
+        "ms_per_call": bms,
+        "frames_per_s": sum(L) / (bms * 1e-3),
+        "useful_tflops": bflops / (bms * 1e-3) / 1e12,
+        "algorithmic_gbs": bbyts / (bms * 1e-3) / 1e9,
+        "roofline": {"bound": "hbm", "achieved": bbyts / (bms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": bbyts / (bms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": load_traffic("band_bwd_llsa_traffic.json",
+                                             source_sha("band_bwd.hip"))},
+        "algorithmic_bytes": bbyts,
+        "useful_flops": bflops,
+    }
+    return backward, {
         "workload": "LLSA forward (two-branch) bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, "
                     "lengths U[400,800]",
         "ms_per_call": ms,
@@ -426,8 +455,8 @@ def main():
         "algorithmic_gbs_step": (fwd_b + bwd_b) / step_s / 1e9,
     }
     if not args.no_extras:
-        log("LLSA forward")
-        line["llsa"] = bench_llsa(max(20, args.steps // 2), 5)
+        log("LLSA forward and backward")
+        line["llsa_backward"], line["llsa"] = bench_llsa(max(20, args.steps // 2), 5)
         log("streaming step")
         line["stream"] = bench_stream()
         log("masked full attention in PyTorch")

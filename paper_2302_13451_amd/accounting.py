@@ -71,6 +71,12 @@ def llsa_forward_flops(lengths, H: int, d: int, Lb: int, La: int) -> int:
     return 4 * d * H * (c + l)
 
 
+def llsa_backward_flops(lengths, H: int, d: int, Lb: int, La: int) -> int:
+    """The SA backward's products over both outputs' windows."""
+    c, l = llsa_width_sums(lengths, Lb, La)
+    return 8 * d * H * (c + l)
+
+
 def valid_frames(lengths) -> int:
     return sum(int(L) for L in lengths)
 
@@ -94,6 +100,14 @@ def llsa_forward_bytes(lengths, H: int, d: int, dtype: str = "bf16", with_lse: b
     f = valid_frames(lengths)
     e = ELEM_BYTES[dtype]
     return 8 * f * H * d * e + (2 * 4 * f * H if with_lse else 0)
+
+
+def llsa_backward_bytes(lengths, H: int, d: int, dtype: str = "bf16") -> int:
+    """Both outputs' q, out, dout and lse and both branches' k, v read; dq, dk,
+    dv of both written; once per valid frame."""
+    f = valid_frames(lengths)
+    e = ELEM_BYTES[dtype]
+    return 16 * f * H * d * e + 2 * 4 * f * H
 
 
 def stream_step_pairs(window_widths: Iterable[int], H: int) -> int:
