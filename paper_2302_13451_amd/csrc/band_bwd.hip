@@ -1273,54 +1273,57 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
   const int r0 = f0 + 16 * wq;
   const bool valid = r0 + col < len;
   const int nrows = min(16, T - r0);
-  // the window of segment (j, i) in the role functions' terms: t - Lb .. t + La
-  auto seg_nonempty = [&](int j, int i) { return a.lo[j][i] <= a.hi[j][i]; };
+  // segment (j, i) in the role functions' terms: window t - Lb .. t + La with
+  // Lb = -lo, La = hi. Both outputs' branch-L segments are never empty; the
+  // branch-C ones are empty exactly when La = 0 (then lo = hi + 1 for both).
+  const bool has_c = a.lo[0][0] <= a.hi[0][0];
+  auto bands_of = [&](int j, int i) {
+    return BwdBands<D, SEG>{s_qb(j), s_db(j), s_kb(i), s_vb(i), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
+                            qbase[j], kbase[i], 0};
+  };
   if (role < 2) {
     const int j = role;
     f32x4 aq[NB];
-    bool any = false;
     const int c_own = 16 * wq + col - a.qoff[j];  // query band row of frame r0 + col
     const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
-    for (int i = 1; i >= 0; --i) {  // branch L first: its segment is never empty
-      if (!seg_nonempty(j, i)) continue;
-      const BwdBands<D, SEG> bd{s_qb(j), s_db(j), s_kb(i), s_vb(i), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
-                                qbase[j], kbase[i], 0};
-      const int lo = a.lo[j][i], hi = a.hi[j][i];
-      const int rel = lo - a.koff[i];  // key band row of the first key of query f0
+    {
+      const int lo = a.lo[j][1], hi = a.hi[j][1];
+      const int rel = lo - a.koff[1];  // key band row of the first key of query f0
       const int sbs = rel & ~15;
       const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
-      const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
-      if (!any)
-        bwd_query_role<D, SEG, false, false>(bd, sa, own, c_own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
-                                             a.log2_scale, lane, aq, sbs);
-      else
-        bwd_query_role<D, SEG, false, true>(bd, sa, own, c_own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
-                                            a.log2_scale, lane, aq, sbs);
-      any = true;
+      bwd_query_role<D, SEG, false, false>(bands_of(j, 1), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own, c_own,
+                                           r0, wq, len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
     }
-    store_rows_direct<D>(a.dq[j] + slice, fs, r0, nrows, aq, 1.f, valid && any, lane);
+    if (has_c) {
+      const int lo = a.lo[j][0], hi = a.hi[j][0];
+      const int rel = lo - a.koff[0];
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      bwd_query_role<D, SEG, false, true>(bands_of(j, 0), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own, c_own,
+                                          r0, wq, len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
+    }
+    store_rows_direct<D>(a.dq[j] + slice, fs, r0, nrows, aq, 1.f, valid, lane);
   } else {
     const int i = role - 2;
     f32x4 adv[NB], adk[NB];
-    bool any = false;
     const int c_own = 16 * wq + col - a.koff[i];  // key band row of frame r0 + col
     const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
-    for (int j = 0; j < 2; ++j) {
-      if (!seg_nonempty(j, i)) continue;
-      const BwdBands<D, SEG> bd{s_qb(j), s_db(j), s_kb(i), s_vb(i), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
-                                qbase[j], kbase[i], 0};
-      const int lo = a.lo[j][i], hi = a.hi[j][i];
-      const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
-      const int sbs = rel & ~15;
-      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
-      const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
-      if (!any)
-        bwd_key_role<D, SEG, false, false>(bd, sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk,
-                                           sbs);
-      else
-        bwd_key_role<D, SEG, false, true>(bd, sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk,
-                                          sbs);
-      any = true;
+    const bool any = i == 1 || has_c;
+    if (any) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int lo = a.lo[j][i], hi = a.hi[j][i];
+        const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
+        const int sbs = rel & ~15;
+        const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+        const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
+        if (j == 0)
+          bwd_key_role<D, SEG, false, false>(bands_of(j, i), sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
+                                             lane, adv, adk, sbs);
+        else
+          bwd_key_role<D, SEG, false, true>(bands_of(j, i), sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
+                                            lane, adv, adk, sbs);
+      }
     }
     store_rows_direct<D>(a.dv[i] + slice, fs, r0, nrows, adv, 1.f, valid && any, lane);
     store_rows_direct<D>(a.dk[i] + slice, fs, r0, nrows, adk, a.scale, valid && any, lane);
