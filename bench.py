@@ -355,6 +355,93 @@ def bench_masked_attention(steps=5):
             "frames_per_s": sum(x["lengths"].tolist()) / (ms * 1e-3)}
 
 
+MEMORY_EXPERIMENT = {"B": 4, "T": 1000, "d": 64, "heads": (8, 16), "La": 8,
+                     "widths": tuple(range(10, 491, 40))}
+
+
+def _peak_bytes(fn):
+    """Peak bytes the caching allocator hands out while fn runs, above what
+    was allocated when it started (fn allocates its own inputs)."""
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    fn()
+    torch.cuda.synchronize()
+    return torch.cuda.max_memory_allocated() - base
+
+
+def sa_training_memory(B, T, H, d, Lb, La):
+    """Peak memory of one SA layer's forward + backward through the library:
+    q, k, v and dout, out and lse, dq, dk and dv (bf16, lse float32). The
+    kernels allocate nothing, so this is the tensors themselves."""
+    def run():
+        g = torch.Generator(device="cuda").manual_seed(7)
+        q, k, v, do = (torch.empty(B, T, H, d, dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+                       for _ in range(4))
+        out, lse = bd.sa_forward(q, k, v, Lb, La)
+        dq, dk, dv = bd.sa_backward(q, k, v, out, lse, do, Lb, La)
+        torch.cuda.synchronize()
+        del q, k, v, do, out, lse, dq, dk, dv
+    return _peak_bytes(run)
+
+
+def sa_tensors_memory(B, T, H, d):
+    """Peak memory of allocating the same tensors as sa_training_memory, in the
+    same order, with no kernel run: what the allocator's rounding makes of
+    them."""
+    def run():
+        ts = [torch.empty(B, T, H, d, dtype=torch.bfloat16, device="cuda") for _ in range(5)]
+        ts.append(torch.empty(B, H, T, dtype=torch.float32, device="cuda"))
+        ts += [torch.empty(B, T, H, d, dtype=torch.bfloat16, device="cuda") for _ in range(3)]
+        torch.cuda.synchronize()
+        del ts
+    return _peak_bytes(run)
+
+
+def maa_training_memory(B, T, H, d, Lb, La):
+    """Peak memory of masked acausal attention (the paper's MAA: dense T x T
+    scores, band mask) forward + backward with PyTorch autograd, on the same
+    bf16 tensors, float32 scores and softmax."""
+    def run():
+        g = torch.Generator(device="cuda").manual_seed(7)
+        q, k, v, do = (torch.empty(B, H, T, d, dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+                       for _ in range(4))
+        t = torch.arange(T, device="cuda")
+        mask = (t[None, :] >= t[:, None] - Lb) & (t[None, :] <= t[:, None] + La)
+        qq, kk, vv = (a.detach().requires_grad_(True) for a in (q, k, v))
+        s_ = torch.matmul(qq.float(), kk.float().transpose(-1, -2).contiguous()) / math.sqrt(d)
+        s_ = s_.masked_fill(~mask, float("-inf"))
+        p = torch.softmax(s_, dim=-1)
+        o = torch.matmul(p, vv.float()).to(torch.bfloat16)
+        o.backward(do)
+        torch.cuda.synchronize()
+        del q, k, v, do, qq, kk, vv, s_, p, o, mask
+    return _peak_bytes(run)
+
+
+def memory_experiment():
+    """Memory per training vector (one sequence) of one attention layer's
+    forward + backward against the receptive field W = Lb + La + 1, SA through
+    the library against MAA in PyTorch (Sec. "Lower Memory Usage", Fig. 5),
+    at d = 64, N_T = 1000, H = 8 and 16, La = 8."""
+    c = MEMORY_EXPERIMENT
+    B, T, d, La = c["B"], c["T"], c["d"], c["La"]
+    maa_training_memory(B, T, c["heads"][0], d, 9, La)  # first-call workspaces of the library GEMMs
+    rows = []
+    for H in c["heads"]:
+        for W in c["widths"]:
+            Lb = W - 1 - La
+            sa = sa_training_memory(B, T, H, d, Lb, La)
+            maa = maa_training_memory(B, T, H, d, Lb, La)
+            rows.append({"H": H, "W": W, "Lb": Lb, "La": La, "sa_bytes_per_vector": sa / B,
+                         "maa_bytes_per_vector": maa / B,
+                         "sa_tensors_allocated_per_vector": sa_tensors_memory(B, T, H, d) / B,
+                         "sa_tensor_bytes_per_vector": acc.sa_training_tensor_bytes(T, H, d)})
+    return {"experiment": "memory per training vector, one attention layer forward+backward, "
+                          "B=%d, T=%d, d=%d, bf16 tensors" % (B, T, d), "rows": rows}
+
+
 def cpu_baseline(min_seconds=10.0):
     """The fp64 oracle on the host cores: repeated passes of forward+backward
     over the first sequences of the workload until ~10 s have elapsed."""
@@ -391,6 +478,8 @@ def main():
                     help="time only the SA forward+backward step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 512 MiB (counter calibration)")
+    ap.add_argument("--memory-experiment", action="store_true",
+                    help="only measure memory per training vector, SA against masked attention")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: --gpus %d is not supported (the band kernels shard "
@@ -407,6 +496,9 @@ def main():
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n}))
         return
     bd.load_library()
+    if args.memory_experiment:
+        print(json.dumps(memory_experiment()), flush=True)
+        return
     log("SA forward+backward: %d warmup + %d timed steps" % (args.warmup, args.steps))
     r = bench_sa(args.steps, args.warmup)
     w = WORKLOAD

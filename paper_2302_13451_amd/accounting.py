@@ -110,6 +110,13 @@ def llsa_backward_bytes(lengths, H: int, d: int, dtype: str = "bf16") -> int:
     return 16 * f * H * d * e + 2 * 4 * f * H
 
 
+def sa_training_tensor_bytes(T: int, H: int, d: int, dtype: str = "bf16") -> int:
+    """Bytes of every tensor of one sequence in an SA layer's forward +
+    backward through the library: q, k, v, dout, out, dq, dk, dv and lse (no
+    score, weight or mask tensor is kept)."""
+    return 8 * T * H * d * ELEM_BYTES[dtype] + 4 * T * H
+
+
 def stream_step_pairs(window_widths: Iterable[int], H: int) -> int:
     return H * sum(int(w) for w in window_widths)
 
