@@ -65,6 +65,9 @@ extern "C" {
 /* Largest window Lb + La + 1 accepted by sa_stream_step. */
 #define SA_STREAM_MAX_WINDOW 1024
 
+/* Largest look-ahead La (channels La + 1) accepted by llsa_paper_forward. */
+#define SA_LLSA_PAPER_MAX_LA 64
+
 /*
  * SA forward (Eq. 4-6): for every valid frame t,
  *   z_j = k_(lo+j) . q_t / sqrt(d),  a_t = softmax(z),  out_t = sum_j a_j v_(lo+j)
@@ -118,6 +121,26 @@ int sa_backward(const void* q, const void* k, const void* v, const void* out,
 int llsa_forward(const void* q, const void* k, const void* v, void* out, float* lse,
                  int B, int T, int H, int d, int Lb, int La,
                  const int32_t* lengths, int dtype, void* stream);
+
+/*
+ * The paper's LLSA forward with La + 1 channels (Eq. 14/15, Fig. 4): every
+ * channel c = 0 .. La is a branch of its own and is computed with its own
+ * query. Output channel c of frame t reads the window t+c-La-Lb .. t+c,
+ * frame tau from input channel min(La, t+c-tau): channel c counts how many
+ * frames of look-ahead its output has seen. Channel La is the look-ahead
+ * output (window t-Lb .. t+La, all frames up to t from channel La), channel 0
+ * the causal one. Windows are clipped to [0, length).
+ *
+ * q, k, v : [La+1][B][T][H][d] inputs (channel-major)
+ * out     : [La+1][B][T][H][d] outputs (padding frames written as 0)
+ * lse     : float [La+1][B][H][T] (required; it holds the band part's
+ *           log-sum-exp between the two passes; -inf on padding frames)
+ * La must not exceed SA_LLSA_PAPER_MAX_LA. Lb is clipped to T; La is not
+ * (it fixes the channel count).
+ */
+int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, float* lse,
+                       int B, int T, int H, int d, int Lb, int La,
+                       const int32_t* lengths, int dtype, void* stream);
 
 /*
  * Two-branch LLSA backward: gradients of a loss l with respect to q, k, v of

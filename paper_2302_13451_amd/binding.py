@@ -37,6 +37,7 @@ _SIGNATURES = {
     "sa_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
                     _i, _vp],
     "llsa_forward": [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp],
+    "llsa_paper_forward": [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp],
     "llsa_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
                       _i, _vp],
     "sa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _vp,
@@ -179,6 +180,28 @@ def llsa_forward(q, k, v, Lb: int, La: int, lengths=None, out=None, lse=None, *,
     _check(load_library().llsa_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, T, H,
                                        d, int(Lb), int(La), _ptr(lengths), code,
                                        _stream(q.device, stream)))
+    return out, lse
+
+
+def llsa_paper_forward(q, k, v, Lb: int, La: int, lengths=None, out=None, lse=None, *,
+                       stream=None):
+    """The paper's (La+1)-channel LLSA forward. q, k, v: [La+1][B][T][H][d],
+    channel c computed with its own query. Returns (out [La+1][B][T][H][d],
+    lse [La+1][B][H][T])."""
+    C, B, T, H, d = q.shape
+    if C != La + 1:
+        raise SAError(SA_ERR_INVALID, "paper LLSA tensors must have La + 1 = %d channels" % (La + 1))
+    for n, t in (("q", q), ("k", k), ("v", v)):
+        _require(t, n, (C, B, T, H, d), q.dtype, q.device)
+    code = _dtype_code(q)
+    out = torch.empty_like(q) if out is None else out
+    _require(out, "out", (C, B, T, H, d), q.dtype, q.device)
+    lse = torch.empty((C, B, H, T), dtype=torch.float32, device=q.device) if lse is None else lse
+    _require(lse, "lse", (C, B, H, T), torch.float32, q.device)
+    lengths = _lengths(lengths, B, q.device)
+    _check(load_library().llsa_paper_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B,
+                                             T, H, d, int(Lb), int(La), _ptr(lengths), code,
+                                             _stream(q.device, stream)))
     return out, lse
 
 

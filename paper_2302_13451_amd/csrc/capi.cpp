@@ -194,6 +194,36 @@ int llsa_forward(const void* q, const void* k, const void* v, void* out, float* 
                       fn);
 }
 
+int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, float* lse, int B,
+                       int T, int H, int d, int Lb, int La, const int32_t* lengths, int dtype,
+                       void* stream) {
+  const char* fn = "llsa_paper_forward";
+  if (int rc = check_shape(fn, B, T, H, d, Lb, La, dtype)) return rc;
+  if (La > SA_LLSA_PAPER_MAX_LA)
+    return fail(SA_ERR_INVALID, "%s: La = %d exceeds %d", fn, La, SA_LLSA_PAPER_MAX_LA);
+  if (B == 0 || T == 0 || H == 0) return SA_OK;
+  if (!lse) return fail(SA_ERR_NULL, "%s: lse is required", fn);
+  if (int rc = check_ptrs(fn, {q, k, v, out}, {lse}, {lengths})) return rc;
+  if (static_cast<long long>(La + 1) * B * T * H > (1LL << 31) - 1)
+    return fail(SA_ERR_INVALID, "%s: (La+1)*B*T*H exceeds 2^31-1", fn);
+  Lb = Lb < T ? Lb : T;  // La stays: it fixes the channel count
+  sa::LlsaPaperArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.B = B;
+  a.T = T;
+  a.H = H;
+  a.d = d;
+  a.Lb = Lb;
+  a.La = La;
+  a.lengths = lengths;
+  return check_launch(
+      sa::launch_llsa_paper_forward(a, elem(dtype), static_cast<hipStream_t>(stream)), fn);
+}
+
 int llsa_backward(const void* q, const void* k, const void* v, const void* out, const float* lse,
                   const void* dout, void* dq, void* dk, void* dv, int B, int T, int H, int d, int Lb,
                   int La, const int32_t* lengths, int dtype, void* stream) {

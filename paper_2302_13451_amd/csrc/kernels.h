@@ -42,6 +42,18 @@ struct BandForwardArgs {
 
 hipError_t launch_band_forward(const BandForwardArgs& a, ElemType et, hipStream_t stream);
 
+// The paper's LLSA forward with La + 1 channels: q, k, v, out are
+// [La+1][B][T][H][d], lse [La+1][B][H][T] (required).
+struct LlsaPaperArgs {
+  const void *q, *k, *v;
+  void* out;
+  float* lse;
+  int B, T, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& a, ElemType et, hipStream_t stream);
+
 struct SaBackwardArgs {
   const void *q, *k, *v, *out, *dout;
   const float* lse;

@@ -85,21 +85,22 @@ def sa_inputs(B: int, T: int, H: int, d: int, seed: int, *, dtype: str = "bf16",
 
 def llsa_inputs(B: int, T: int, H: int, d: int, seed: int, *, dtype: str = "bf16",
                 scale="rsqrt_d", peak: float = 1.0, lengths: LengthSpec = "full",
-                pad_value: float = 0.0, with_dout: bool = False) -> dict:
-    """Two-branch q, k, v as float32 CPU tensors ``[2][B][T][H][d]``
-    (index 0 = causal branch, 1 = look-ahead branch); ``lengths`` int32 ``[B]``;
-    with ``with_dout`` also the gradient of both outputs, ``dout`` N(0, 1)
-    ``[2][B][T][H][d]``, drawn after the lengths (so q, k, v and the lengths
-    do not depend on it)."""
+                pad_value: float = 0.0, with_dout: bool = False, channels: int = 2) -> dict:
+    """Multi-branch q, k, v as float32 CPU tensors ``[channels][B][T][H][d]``
+    (two branches by default: index 0 = causal branch, 1 = look-ahead branch;
+    ``channels = La + 1`` for the paper's channel form); ``lengths`` int32
+    ``[B]``; with ``with_dout`` also the gradient of every output, ``dout``
+    N(0, 1) of the same shape, drawn after the lengths (so q, k, v and the
+    lengths do not depend on it)."""
     g = torch.Generator(device="cpu").manual_seed(int(seed))
     s = _scale(scale, d) * float(peak)
-    q = torch.randn(2, B, T, H, d, generator=g) * s
-    k = torch.randn(2, B, T, H, d, generator=g) * s
-    v = torch.randn(2, B, T, H, d, generator=g) * s
+    q = torch.randn(channels, B, T, H, d, generator=g) * s
+    k = torch.randn(channels, B, T, H, d, generator=g) * s
+    v = torch.randn(channels, B, T, H, d, generator=g) * s
     ln = _draw_lengths(g, B, T, lengths)
     out = {"q": q, "k": k, "v": v}
     if with_dout:
-        out["dout"] = torch.randn(2, B, T, H, d, generator=g)
+        out["dout"] = torch.randn(channels, B, T, H, d, generator=g)
     for name in list(out):
         out[name] = _pad(_round(out[name], dtype), ln, pad_value, 2)
     out["lengths"] = ln

@@ -29,7 +29,8 @@ def lib():
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("sa_forward", "sa_backward", "llsa_forward", "llsa_backward", "sa_stream_step",
+    for n in ("sa_forward", "sa_backward", "llsa_forward", "llsa_paper_forward", "llsa_backward",
+              "sa_stream_step",
               "sa_last_error", "sa_abi_version"):
         assert n in names
 
@@ -98,6 +99,21 @@ def test_llsa_backward_validation(lib):
     assert lib.llsa_backward(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 200, 2, 64,
                              70, 20, None, bd.SA_BF16, None) == bd.SA_ERR_UNSUPPORTED  # window too wide
     assert "too wide" in lib.sa_last_error().decode()
+
+
+def test_llsa_paper_forward_validation(lib):
+    def lp(lse=FAKE, out=FAKE, B=2, Lb=2, La=3, d=64, dtype=bd.SA_BF16):
+        return lib.llsa_paper_forward(FAKE, FAKE, FAKE, out, lse, B, 8, 2, d, Lb, La, None, dtype,
+                                      None)
+    assert lp(B=0) == bd.SA_OK
+    assert lp(lse=None) == bd.SA_ERR_NULL
+    assert lp(out=None) == bd.SA_ERR_NULL
+    assert lp(out=FAKE_ODD) == bd.SA_ERR_INVALID
+    assert lp(La=-1) == bd.SA_ERR_INVALID
+    assert lp(La=65) == bd.SA_ERR_INVALID                      # above SA_LLSA_PAPER_MAX_LA
+    assert "exceeds 64" in lib.sa_last_error().decode()
+    assert lp(d=16) == bd.SA_ERR_UNSUPPORTED
+    assert lp(dtype=7) == bd.SA_ERR_UNSUPPORTED
 
 
 def test_stream_validation(lib):
