@@ -143,6 +143,29 @@ int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, f
                        const int32_t* lengths, int dtype, void* stream);
 
 /*
+ * Backward of llsa_paper_forward: gradients of a loss l with respect to q, k,
+ * v of every channel given dout = dl/dout of every output channel. It is the
+ * adjoint of the forward's gather (Eq. 16 of the paper prints only the value
+ * part): every output row contributes as in sa_backward (Eq. 7-13) over its
+ * window, each key/value row receiving the sum over the rows that read it,
+ * through the same channel map. Channel La's keys and values gather the
+ * band parts of all La + 1 outputs; channel c < La's keys and values are read
+ * by one query per output channel (on a diagonal).
+ *
+ * q, k, v, out, dout : [La+1][B][T][H][d] inputs; out is llsa_paper_forward's
+ * lse                : float [La+1][B][H][T] from llsa_paper_forward (required)
+ * dq, dk, dv         : [La+1][B][T][H][d] outputs (padding frames written as 0)
+ * Supported: dtype SA_BF16, La <= SA_LLSA_PAPER_MAX_LA, and Lb + La <= 64
+ * (208 at d = 32), or Lb + La <= 80 when La <= 15 at d = 64; other windows
+ * return SA_ERR_UNSUPPORTED. La = 0 is the SA backward with the window
+ * t-Lb .. t.
+ */
+int llsa_paper_backward(const void* q, const void* k, const void* v, const void* out,
+                        const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                        int B, int T, int H, int d, int Lb, int La,
+                        const int32_t* lengths, int dtype, void* stream);
+
+/*
  * Two-branch LLSA backward: gradients of a loss l with respect to q, k, v of
  * both branches given dout = dl/dout of both outputs, for llsa_forward with
  * the same arguments. It is the adjoint of llsa_forward's gather (the paper's

@@ -238,6 +238,14 @@ def llsa_paper(q, k, v, Lb: int, La: int, lengths=None, convention: str = "text"
     return llsa_forward(q, k, v, chans, chans, chans, Lb, La, lengths, convention, threads)
 
 
+def llsa_paper_backward(q, k, v, dy, Lb: int, La: int, lengths=None, convention: str = "text",
+                        threads: int = 0):
+    """Gradient of :func:`llsa_paper` for ``dy [La+1][B][T][H][d]``; returns
+    ``(dq, dk, dv)``, each ``[La+1][B][T][H][d]``."""
+    chans = list(range(La + 1))
+    return llsa_backward(q, k, v, dy, chans, chans, chans, Lb, La, lengths, convention, threads)
+
+
 class StreamOracle:
     """Per-stream ring buffers driven one frame at a time (SA streaming step).
 

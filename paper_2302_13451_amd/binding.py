@@ -38,6 +38,8 @@ _SIGNATURES = {
                     _i, _vp],
     "llsa_forward": [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp],
     "llsa_paper_forward": [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp],
+    "llsa_paper_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                            _vp, _i, _vp],
     "llsa_backward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp,
                       _i, _vp],
     "sa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _vp,
@@ -203,6 +205,30 @@ def llsa_paper_forward(q, k, v, Lb: int, La: int, lengths=None, out=None, lse=No
                                              T, H, d, int(Lb), int(La), _ptr(lengths), code,
                                              _stream(q.device, stream)))
     return out, lse
+
+
+def llsa_paper_backward(q, k, v, out, lse, dout, Lb: int, La: int, lengths=None, dq=None,
+                        dk=None, dv=None, *, stream=None):
+    """Backward of llsa_paper_forward. Every tensor is [La+1][B][T][H][d],
+    lse [La+1][B][H][T] from the forward. Returns (dq, dk, dv)."""
+    C, B, T, H, d = q.shape
+    if C != La + 1:
+        raise SAError(SA_ERR_INVALID, "paper LLSA tensors must have La + 1 = %d channels" % (La + 1))
+    for n, t in (("q", q), ("k", k), ("v", v), ("out", out), ("dout", dout)):
+        _require(t, n, (C, B, T, H, d), q.dtype, q.device)
+    _require(lse, "lse", (C, B, H, T), torch.float32, q.device)
+    code = _dtype_code(q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _require(t, n, (C, B, T, H, d), q.dtype, q.device)
+    lengths = _lengths(lengths, B, q.device)
+    _check(load_library().llsa_paper_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                              _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), B, T, H,
+                                              d, int(Lb), int(La), _ptr(lengths), code,
+                                              _stream(q.device, stream)))
+    return dq, dk, dv
 
 
 def llsa_backward(q, k, v, out, lse, dout, Lb: int, La: int, lengths=None, dq=None, dk=None,

@@ -1381,6 +1381,263 @@ bool llsa_bwd_geometry(int d, int Lb, int La, LlsaBwdDev& a) {
 
 }  // namespace
 
+namespace {
+
+// Band part of the backward of the paper's (A+1)-channel LLSA (Eq. 14/15 in
+// the convention of Fig. 4, A = La): output channel c of frame t reads the
+// frames tau <= t + c - A of its window, t + c - A - Lb .. t + c - A, from
+// channel A. That segment's gradients are the SA backward's (Eq. 7-13) with
+// the output's final lse and D_t = dout_t . out_t, so
+//   dq[c] (band part) = query role of segment c,
+//   dk[A], dv[A]      = sum over c of the key role of segment c.
+// The frames from channels 0 .. A-1 (one per channel, on a diagonal) are the
+// diagonal pass's (llsa_paper.hip), which adds its part to dq[c].
+struct PaperBwdDev {
+  const uint16_t *q, *o, *dout, *k, *v;  // channel 0 of [A+1][B][T][H][d]
+  const float* lse;                      // channel 0 of [A+1][B][H][T]
+  uint16_t *dq, *dk, *dv;
+  size_t cstride, lstride;  // elements per channel of the tensors, of lse
+  int A, Lb;
+  int B, T, H, ntiles;
+  const int32_t* lengths;
+  float scale, scale_log2, log2_scale;
+};
+
+// One workgroup of 16 waves per (sequence, head, 64-frame tile). LDS holds the
+// key and value bands of channel A (origin f0 - A - Lb, staged once) and the
+// query and dout bands (origin f0) of two output channels at a time, with -D
+// and lse log2(e) of both. The outputs are taken in pairs (2p, 2p + 1): waves
+// 0-3 / 4-7 take the query role of the pair's first / second output, waves
+// 8-11 / 12-15 the key role, accumulating over the pairs; at the end waves
+// 12-15 hand their sums to waves 8-11, which store dk[A] and dv[A].
+template <int D>
+__global__ __launch_bounds__(1024) void llsa_paper_bwd_band_kernel(PaperBwdDev a) {
+  constexpr int NT = 1024;
+  constexpr int SEG = Seg<D>::kRows;
+  constexpr int NS = D / 32, NB = D / 16;
+  constexpr int NB16 = SEG / 16;
+  constexpr int BPW = (2 * NB16 + 15) / 16;
+  static_assert(SEG % 16 == 0, "the D product covers the band in 16-row blocks");
+  static_assert(4 * 64 * 2 * NB * 4 * 2 <= 6 * SEG * D, "the key-role hand-over fits the bands");
+  __shared__ __attribute__((aligned(128))) uint16_t s_band[6 * SEG * D];
+  __shared__ __attribute__((aligned(16))) float s_stat[4 * SEG];
+  // bands: q, dout of slot 0; q, dout of slot 1; k, v of channel A
+  auto band = [&](int x) { return s_band + x * SEG * D; };
+  auto s_qb = [&](int j) { return band(2 * j); };
+  auto s_db = [&](int j) { return band(2 * j + 1); };
+
+  int bh, tile;
+  if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int T = a.T, H = a.H, A = a.A;
+  const int len = clamp_len_uniform(a.lengths, b, T);
+  const int f0 = tile * kC;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, g = lane >> 4;
+  const size_t cs = a.cstride;
+
+  if (f0 >= len) {  // padding tile
+    for (int c = 0; c <= A; ++c) zero_rows<D, NT>(a.dq + c * cs, nullptr, b, h, T, H, f0, min(f0 + kC, T), tid);
+    zero_rows<D, NT>(a.dk + A * cs, a.dv + A * cs, b, h, T, H, f0, min(f0 + kC, T), tid);
+    return;
+  }
+  const size_t slice = row_index(b, 0, h, T, H, D);
+  const int fs = H * D;
+  const int koff = -(A + a.Lb);  // key band origin relative to f0 (the query bands start at f0)
+  const int kbase = f0 + koff;
+  const int kblo = max(0, -kbase), kbhi = min(SEG, len - kbase);
+  const int qbhi = min(SEG, len - f0);
+  seg_issue_rows<D, 16>(band(4), a.k + A * cs + slice, fs, kbase, kblo, kbhi, w, lane);
+  seg_issue_rows<D, 16>(band(5), a.v + A * cs + slice, fs, kbase, kblo, kbhi, w, lane);
+
+  const int wq = w & 3, role = w >> 2;  // 0, 1: query role of slot role; 2, 3: key role of slot role - 2
+  const int r0 = f0 + 16 * wq;
+  const bool valid = r0 + col < len;
+  const int nrows = min(16, T - r0);
+  const int npairs = A / 2 + 1;
+  // stages the query bands and statistics of pair p; every wave runs it, with
+  // the same barriers, in either role's loop
+  auto stage_pair = [&](int p) {
+    const int c0 = 2 * p;
+    const bool two = c0 + 1 <= A;
+    if (p > 0) __syncthreads();  // every wave is done with the previous pair's bands
+    for (int j = 0; j < (two ? 2 : 1); ++j) {
+      seg_issue_rows<D, 16>(s_qb(j), a.q + (c0 + j) * cs + slice, fs, f0, 0, qbhi, w, lane);
+      seg_issue_rows<D, 16>(s_db(j), a.dout + (c0 + j) * cs + slice, fs, f0, 0, qbhi, w, lane);
+    }
+    // out rows of both query bands as the B operand of the D products (zero
+    // outside the sequence): wave w takes the 16-row blocks w, w + 16, ...
+    bf16x8 of[BPW][NS];
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int blk = w + 16 * i;
+      const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
+      const int fr = f0 + 16 * rb + col;
+      const bool in = blk < 2 * NB16 && (jb == 0 || two) && fr < len;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        of[i][s] = bf16x8{};
+        if (in) of[i][s] = __builtin_bit_cast(bf16x8, ld16(a.o + (c0 + jb) * cs + slice + (fr * fs + 32 * s + 8 * g)));
+      }
+    }
+    float lsev = 0.f;
+    const int lj = tid >= SEG ? 1 : 0, lr = tid - lj * SEG;
+    const int lfr = f0 + lr;
+    const bool lin = tid < 2 * SEG && (lj == 0 || two) && lfr < len;
+    if (lin) lsev = a.lse[(c0 + lj) * a.lstride + (static_cast<size_t>(b) * H + h) * T + lfr];
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (p == 0) {  // rows outside the sequence stay zero: no later load writes them
+      if (kblo > 0) {
+        seg_zero_rows<D, NT>(band(4), 0, min(kblo, SEG), tid);
+        seg_zero_rows<D, NT>(band(5), 0, min(kblo, SEG), tid);
+      }
+      if (kbhi < SEG) {
+        seg_zero_rows<D, NT>(band(4), max(kbhi, 0), SEG, tid);
+        seg_zero_rows<D, NT>(band(5), max(kbhi, 0), SEG, tid);
+      }
+      if (qbhi < SEG)
+        for (int x = 0; x < 4; ++x) seg_zero_rows<D, NT>(band(x), qbhi, SEG, tid);
+      __syncthreads();
+    }
+    if (tid < 2 * SEG) s_stat[2 * SEG * lj + SEG + lr] = lin ? lsev * kLog2e : __builtin_huge_valf();
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int blk = w + 16 * i;
+      if (blk < 2 * NB16) {
+        const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
+        f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(seg_row8<D>(s_db(jb), 16 * rb + col, 32 * s + 8 * g), of[i][s],
+                                                       dd, 0, 0, 0);
+        const int e = col & 3;
+        const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
+        if ((col >> 2) == g) s_stat[2 * SEG * jb + 16 * rb + col] = -dg;
+      }
+    }
+    __syncthreads();
+  };
+  const int j = role & 1;
+  auto bands_of = [&]() {
+    return BwdBands<D, SEG>{s_qb(j), s_db(j), band(4), band(5), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
+                            f0, kbase, 0};
+  };
+  // segment c: window t + lo .. t + hi with lo = c - A - Lb, hi = c - A (the
+  // role functions' Lb = -lo, La = hi); an odd channel count leaves the last
+  // pair's second slot empty
+  f32x4* s_red = reinterpret_cast<f32x4*>(s_band);
+  const int ri = wq * 64 + lane;
+  if (role < 2) {
+    const int c_own = 16 * wq + col;  // query band row of frame r0 + col
+    const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
+    for (int p = 0; p < npairs; ++p) {
+      stage_pair(p);
+      const int c = 2 * p + j;
+      if (c > A) continue;
+      const int lo = c - A - a.Lb, hi = c - A;
+      f32x4 aq[NB];
+      const int rel = lo - koff;  // key band row of the first key of query f0 (= c)
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      bwd_query_role<D, SEG, false, false>(bands_of(), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own, c_own, r0, wq,
+                                           len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
+      store_rows_direct<D>(a.dq + c * cs + slice, fs, r0, nrows, aq, 1.f, valid, lane);
+    }
+    __syncthreads();  // the key roles' hand-over (two barriers)
+    __syncthreads();
+  } else {
+    const int c_own = 16 * wq + col - koff;  // key band row of frame r0 + col
+    const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
+    f32x4 adv[NB], adk[NB];
+    auto key_role = [&](int c, auto acc) {
+      const int lo = c - A - a.Lb, hi = c - A;
+      const int rel = -hi;  // query band row of the first query that sees key f0 (= A - c)
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      bwd_key_role<D, SEG, false, decltype(acc)::value>(bands_of(), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own,
+                                                        r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk, sbs);
+    };
+    stage_pair(0);  // the first pair's slots both hold an output (A >= 1)
+    key_role(j, std::false_type{});
+    for (int p = 1; p < npairs; ++p) {
+      stage_pair(p);
+      const int c = 2 * p + j;
+      if (c <= A) key_role(c, std::true_type{});
+    }
+    // waves 12-15 hand their sums to waves 8-11 (A >= 1: both slots of the
+    // first pair hold an output, so both sets are initialised)
+    __syncthreads();
+    if (role == 3) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        s_red[(2 * i) * 256 + ri] = adv[i];
+        s_red[(2 * i + 1) * 256 + ri] = adk[i];
+      }
+    }
+    __syncthreads();
+    if (role == 2) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        adv[i] += s_red[(2 * i) * 256 + ri];
+        adk[i] += s_red[(2 * i + 1) * 256 + ri];
+      }
+      store_rows_direct<D>(a.dv + A * cs + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+      store_rows_direct<D>(a.dk + A * cs + slice, fs, r0, nrows, adk, a.scale, valid, lane);
+    }
+  }
+}
+
+}  // namespace
+
+bool llsa_paper_backward_fits(int d, int Lb, int La) {
+  if (La < 1) return false;
+  const int seg_rows = d == 64 ? Seg<64>::kRows : Seg<32>::kRows;
+  // every row a wave reads lies in its band: 48 + sbs + 32 nblk rows from the
+  // band's origin, and the key role's own rows 64 + A + Lb
+  auto fits = [&](long long rel) {
+    const long long nb = (16LL + Lb + (rel & 15) + kSub - 1) / kSub;
+    return 48LL + (rel & ~15LL) + kSub * nb <= seg_rows;
+  };
+  for (int c = 0; c <= La; ++c)
+    if (!fits(c) || !fits(La - c)) return false;
+  return 64LL + La + Lb <= seg_rows;
+}
+
+hipError_t launch_llsa_paper_backward_band(const LlsaPaperBwdArgs& x, hipStream_t stream) {
+  if (!llsa_paper_backward_fits(x.d, x.Lb, x.La)) return hipErrorNotSupported;
+  PaperBwdDev a{};
+  a.q = static_cast<const uint16_t*>(x.q);
+  a.o = static_cast<const uint16_t*>(x.out);
+  a.dout = static_cast<const uint16_t*>(x.dout);
+  a.k = static_cast<const uint16_t*>(x.k);
+  a.v = static_cast<const uint16_t*>(x.v);
+  a.lse = x.lse;
+  a.dq = static_cast<uint16_t*>(x.dq);
+  a.dk = static_cast<uint16_t*>(x.dk);
+  a.dv = static_cast<uint16_t*>(x.dv);
+  a.cstride = static_cast<size_t>(x.B) * x.T * x.H * x.d;
+  a.lstride = static_cast<size_t>(x.B) * x.H * x.T;
+  a.A = x.La;
+  a.Lb = x.Lb;
+  a.B = x.B;
+  a.T = x.T;
+  a.H = x.H;
+  a.ntiles = (x.T + kC - 1) / kC;
+  a.lengths = x.lengths;
+  a.scale = 1.f / sqrtf(static_cast<float>(x.d));
+  a.scale_log2 = kLog2e * a.scale;
+  a.log2_scale = -0.5f * log2f(static_cast<float>(x.d));
+  const int grid = xcd_slice_grid(x.B * x.H, a.ntiles);
+  if (x.d == 64)
+    hipLaunchKernelGGL(llsa_paper_bwd_band_kernel<64>, dim3(grid), dim3(1024), 0, stream, a);
+  else
+    hipLaunchKernelGGL(llsa_paper_bwd_band_kernel<32>, dim3(grid), dim3(1024), 0, stream, a);
+  return hipGetLastError();
+}
+
 bool llsa_backward_fits(int d, int Lb, int La) {
   LlsaBwdDev a{};
   return llsa_bwd_geometry(d, Lb, La, a);

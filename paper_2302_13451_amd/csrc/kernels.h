@@ -54,6 +54,23 @@ struct LlsaPaperArgs {
 
 hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& a, ElemType et, hipStream_t stream);
 
+// Backward of the paper's LLSA forward (bf16): every tensor [La+1][B][T][H][d],
+// lse [La+1][B][H][T] from the forward.
+struct LlsaPaperBwdArgs {
+  const void *q, *k, *v, *out, *dout;
+  const float* lse;
+  void *dq, *dk, *dv;
+  int B, T, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+// The band part (keys from channel La): writes dq[c] (band part only), dk[La],
+// dv[La], and zeros of every padding row of those.
+hipError_t launch_llsa_paper_backward_band(const LlsaPaperBwdArgs& a, hipStream_t stream);
+bool llsa_paper_backward_fits(int d, int Lb, int La);
+// The whole backward: the band part, then the diagonal frames' part.
+hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& a, ElemType et, hipStream_t stream);
+
 struct SaBackwardArgs {
   const void *q, *k, *v, *out, *dout;
   const float* lse;

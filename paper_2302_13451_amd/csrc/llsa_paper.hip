@@ -123,7 +123,144 @@ __global__ __launch_bounds__(256) void llsa_paper_merge_kernel(PaperMergeDev a) 
   }
 }
 
+// Diagonal part of the backward (bf16 tensors). With P = exp(s - lse) over
+// the whole window and D_t = dout_t . out_t, every (query, key) pair adds
+//   dq += scale dS k,  dk += scale dS q,  dv += P dout,  dS = P (dout . v - D_t)
+// (Eq. 7-13). The diagonal pairs are (c, t) with the key of channel c' < A at
+// tau = t + c - c'. Rows of the first kind, (c, b, t, h), add their diagonal
+// sum to the band part already in dq[c]; rows of the second kind,
+// (c', b, tau, h) for c' < A, gather dk[c'] and dv[c'] over the A + 1 queries
+// (c, tau + c' - c) that see them (channels c' < A take no band keys).
+struct PaperDiagDev {
+  const uint16_t *q, *o, *dout, *k, *v;
+  const float* lse;
+  uint16_t *dq, *dk, *dv;
+  int B, T, H, La;
+  const int32_t* lengths;
+  float scale;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void llsa_paper_bwd_diag_kernel(PaperDiagDev a) {
+  constexpr int LPR = D / 4;
+  const int sub = threadIdx.x % LPR;
+  const int A = a.La;
+  const long long per_ch = static_cast<long long>(a.B) * a.T * a.H;
+  const long long nq = (A + 1) * per_ch;  // rows of the first kind
+  const long long nrows = nq + A * per_ch;
+  const size_t cstride = static_cast<size_t>(per_ch) * D;
+  const size_t lstride = static_cast<size_t>(per_ch);
+  for (long long r = (static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x) / LPR; r < nrows;
+       r += static_cast<long long>(gridDim.x) * blockDim.x / LPR) {
+    const bool query_kind = r < nq;
+    const long long rr = query_kind ? r : r - nq;
+    const int h = static_cast<int>(rr % a.H);
+    const int t = static_cast<int>((rr / a.H) % a.T);
+    const int b = static_cast<int>((rr / (static_cast<long long>(a.H) * a.T)) % a.B);
+    const int c = static_cast<int>(rr / per_ch);
+    int len = a.T;
+    if (a.lengths) {
+      len = a.lengths[b];
+      len = len < 0 ? 0 : (len > a.T ? a.T : len);
+    }
+    const size_t own = c * cstride + row_index(b, t, h, a.T, a.H, D) + 4 * sub;
+    if (query_kind) {
+      if (t >= len) continue;  // padding row: the band pass zeroed it
+      const float lse = a.lse[c * lstride + (static_cast<size_t>(b) * a.H + h) * a.T + t];
+      float qf[4], df[4], of[4], acc[4] = {0.f, 0.f, 0.f, 0.f};
+      load4f<uint16_t>(a.q + own, qf);
+      load4f<uint16_t>(a.dout + own, df);
+      load4f<uint16_t>(a.o + own, of);
+      const float dn = row_sum<LPR>(df[0] * of[0] + df[1] * of[1] + df[2] * of[2] + df[3] * of[3]);
+      for (int cp = 0; cp < A; ++cp) {
+        const int tau = t + c - cp;
+        if (tau < 0 || tau >= len) continue;
+        const size_t kr = cp * cstride + row_index(b, tau, h, a.T, a.H, D) + 4 * sub;
+        float kf[4], vf[4];
+        load4f<uint16_t>(a.k + kr, kf);
+        load4f<uint16_t>(a.v + kr, vf);
+        const float s = row_sum<LPR>(qf[0] * kf[0] + qf[1] * kf[1] + qf[2] * kf[2] + qf[3] * kf[3]) * a.scale;
+        const float dp = row_sum<LPR>(df[0] * vf[0] + df[1] * vf[1] + df[2] * vf[2] + df[3] * vf[3]);
+        const float ds = __expf(s - lse) * (dp - dn);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] += ds * kf[i];
+      }
+      float dq[4];
+      load4f<uint16_t>(a.dq + own, dq);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dq[i] += a.scale * acc[i];
+      store4f<uint16_t>(a.dq + own, dq);
+    } else {
+      float dk[4] = {0.f, 0.f, 0.f, 0.f}, dv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (t < len) {  // padding rows are written as zeros
+        float kf[4], vf[4];
+        load4f<uint16_t>(a.k + own, kf);
+        load4f<uint16_t>(a.v + own, vf);
+        for (int cq = 0; cq <= A; ++cq) {
+          const int tq = t + c - cq;  // the query of output cq that reads this key
+          if (tq < 0 || tq >= len) continue;
+          const size_t qr = cq * cstride + row_index(b, tq, h, a.T, a.H, D) + 4 * sub;
+          const float lse = a.lse[cq * lstride + (static_cast<size_t>(b) * a.H + h) * a.T + tq];
+          float qf[4], df[4], of[4];
+          load4f<uint16_t>(a.q + qr, qf);
+          load4f<uint16_t>(a.dout + qr, df);
+          load4f<uint16_t>(a.o + qr, of);
+          const float s = row_sum<LPR>(qf[0] * kf[0] + qf[1] * kf[1] + qf[2] * kf[2] + qf[3] * kf[3]) * a.scale;
+          const float dn = row_sum<LPR>(df[0] * of[0] + df[1] * of[1] + df[2] * of[2] + df[3] * of[3]);
+          const float dp = row_sum<LPR>(df[0] * vf[0] + df[1] * vf[1] + df[2] * vf[2] + df[3] * vf[3]);
+          const float pw = __expf(s - lse);
+          const float ds = pw * (dp - dn);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            dv[i] += pw * df[i];
+            dk[i] += ds * qf[i];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dk[i] *= a.scale;
+      }
+      store4f<uint16_t>(a.dk + own, dk);
+      store4f<uint16_t>(a.dv + own, dv);
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hipStream_t stream) {
+  if (et != kBF16) return hipErrorNotSupported;
+  if (x.La == 0) {  // one channel: SA with the window t - Lb .. t
+    const SaBackwardArgs s{x.q, x.k, x.v, x.out, x.dout, x.lse, x.dq, x.dk, x.dv,
+                           x.B, x.T, x.H, x.d, x.Lb, 0, x.lengths};
+    return launch_sa_backward(s, et, stream);
+  }
+  hipError_t e = launch_llsa_paper_backward_band(x, stream);
+  if (e != hipSuccess) return e;
+  PaperDiagDev m{};
+  m.q = static_cast<const uint16_t*>(x.q);
+  m.o = static_cast<const uint16_t*>(x.out);
+  m.dout = static_cast<const uint16_t*>(x.dout);
+  m.k = static_cast<const uint16_t*>(x.k);
+  m.v = static_cast<const uint16_t*>(x.v);
+  m.lse = x.lse;
+  m.dq = static_cast<uint16_t*>(x.dq);
+  m.dk = static_cast<uint16_t*>(x.dk);
+  m.dv = static_cast<uint16_t*>(x.dv);
+  m.B = x.B;
+  m.T = x.T;
+  m.H = x.H;
+  m.La = x.La;
+  m.lengths = x.lengths;
+  m.scale = 1.f / sqrtf(static_cast<float>(x.d));
+  const long long rows = static_cast<long long>(2 * x.La + 1) * x.B * x.T * x.H;
+  const long long blocks = (rows * (x.d / 4) + 255) / 256;
+  const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
+  if (x.d == 64)
+    hipLaunchKernelGGL(llsa_paper_bwd_diag_kernel<64>, dim3(grid), dim3(256), 0, stream, m);
+  else
+    hipLaunchKernelGGL(llsa_paper_bwd_diag_kernel<32>, dim3(grid), dim3(256), 0, stream, m);
+  return hipGetLastError();
+}
 
 hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStream_t stream) {
   const int A = x.La;

@@ -30,7 +30,7 @@ def lib():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("sa_forward", "sa_backward", "llsa_forward", "llsa_paper_forward", "llsa_backward",
-              "sa_stream_step",
+              "llsa_paper_backward", "sa_stream_step",
               "sa_last_error", "sa_abi_version"):
         assert n in names
 
@@ -114,6 +114,21 @@ def test_llsa_paper_forward_validation(lib):
     assert "exceeds 64" in lib.sa_last_error().decode()
     assert lp(d=16) == bd.SA_ERR_UNSUPPORTED
     assert lp(dtype=7) == bd.SA_ERR_UNSUPPORTED
+
+
+def test_llsa_paper_backward_validation(lib):
+    def lb(lse=FAKE, dv=FAKE, B=2, Lb=2, La=1, d=64, dtype=bd.SA_BF16, T=8):
+        return lib.llsa_paper_backward(FAKE, FAKE, FAKE, FAKE, lse, FAKE, FAKE, FAKE, dv, B, T, 2,
+                                       d, Lb, La, None, dtype, None)
+    assert lb(B=0) == bd.SA_OK
+    assert lb(lse=None) == bd.SA_ERR_NULL
+    assert lb(dv=None) == bd.SA_ERR_NULL
+    assert lb(dv=FAKE_ODD) == bd.SA_ERR_INVALID
+    assert lb(La=65) == bd.SA_ERR_INVALID
+    assert lb(d=16) == bd.SA_ERR_UNSUPPORTED
+    assert lb(dtype=bd.SA_F32) == bd.SA_ERR_UNSUPPORTED       # bfloat16 only
+    assert lb(T=200, Lb=70, La=20) == bd.SA_ERR_UNSUPPORTED   # window too wide
+    assert "too wide" in lib.sa_last_error().decode()
 
 
 def test_stream_validation(lib):

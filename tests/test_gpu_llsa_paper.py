@@ -102,3 +102,86 @@ def test_llsa_paper_rejects_bad_arguments():
     big = torch.zeros(66, 1, 4, 1, 64, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(bd.SAError):
         bd.llsa_paper_forward(big, big, big, 4, 65)  # La beyond the maximum
+
+
+# ---------------------------------------------------------------------------
+# backward
+
+
+def run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
+    print("llsa paper backward case B=%d T=%d H=%d d=%d Lb=%d La=%d seed=%d" % (
+        B, T, H, d, Lb, La, seed), flush=True)
+    x = llsa_inputs(B, T, H, d, seed, dtype="bf16", scale=scale, lengths=lengths, pad_value=pad,
+                    with_dout=True, channels=La + 1)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].cuda()
+    out, lse = bd.llsa_paper_forward(q, k, v, Lb, La, ln)
+    dq, dk, dv = bd.llsa_paper_backward(q, k, v, out, lse, do, Lb, La, ln)
+    torch.cuda.synchronize()
+    clean = {n: np.nan_to_num(f64(x[n] if n != "dout" else do.cpu())) for n in ("q", "k", "v", "dout")}
+    ref = oracle_mod.llsa_paper_backward(clean["q"], clean["k"], clean["v"], clean["dout"], Lb, La,
+                                         x["lengths"].numpy())
+    return (f64(dq), f64(dk), f64(dv)), ref, x["lengths"].tolist()
+
+
+def check_bwd(got, ref):
+    zero_atol = 1e-5 * float(np.max(np.abs(ref[2])))
+    for name, g, r in zip(("dq", "dk", "dv"), got, ref):
+        for c in range(g.shape[0]):
+            assert_close(g[c], r[c], "bf16", "%s channel %d" % (name, c), elementwise=False,
+                         zero_atol=zero_atol)
+
+
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
+    (2, 150, 2, 64, 30, 1, (40, 150)),   # the paper's two-channel module
+    (2, 130, 2, 32, 21, 3, (1, 130)),
+    (2, 190, 2, 64, 64, 8, (50, 190)),   # nine channels, the widest band at La = 8
+    (2, 120, 2, 64, 37, 4, (60, 120)),   # odd channel count: the last pair has one output
+    (1, 90, 2, 64, 0, 5, "full"),        # band of one frame
+    (2, 100, 1, 64, 17, 0, (30, 100)),   # one channel: the SA backward
+    (2, 160, 2, 64, 24, 16, (60, 160)),
+    (2, 140, 1, 64, 13, 33, (50, 140)),  # pairs past the first 16 rows of the bands
+    (2, 150, 1, 32, 150, 50, (70, 150)),
+    (3, 9, 2, 64, 5, 12, (0, 9, 4)),     # look-ahead longer than the sequences
+    (66, 40, 1, 32, 10, 2, (0, 40)),
+])
+@pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
+def test_llsa_paper_backward_parity(oracle_mod, B, T, H, d, Lb, La, lengths, scale):
+    got, ref, _ = run_bwd(oracle_mod, B, T, H, d, Lb, La, 52, lengths, scale)
+    check_bwd(got, ref)
+
+
+def test_llsa_paper_backward_config4_shape(oracle_mod):
+    """bf16, B=4, T=800, H=12, d=64, Lb=64, La=8 (nine channels), lengths
+    U[400, 800]."""
+    got, ref, _ = run_bwd(oracle_mod, 4, 800, 12, 64, 64, 8, 6, (400, 800))
+    check_bwd(got, ref)
+
+
+def test_llsa_paper_backward_padded_frames_are_never_read(oracle_mod):
+    got, ref, lengths = run_bwd(oracle_mod, 3, 180, 2, 64, 30, 6, 53, (40, 179), pad=float("nan"))
+    check_bwd(got, ref)
+    for g in got:
+        for b, L in enumerate(lengths):
+            assert (g[:, b, L:] == 0).all()
+
+
+def test_llsa_paper_backward_one_channel_is_sa_backward():
+    """La = 0: bit-identical to sa_backward with the window t-Lb .. t."""
+    x = llsa_inputs(2, 140, 2, 64, 54, dtype="bf16", lengths=(60, 140), with_dout=True,
+                    channels=1)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].cuda()
+    out, lse = bd.llsa_paper_forward(q, k, v, 33, 0, ln)
+    got = bd.llsa_paper_backward(q, k, v, out, lse, do, 33, 0, ln)
+    ref = bd.sa_backward(q[0], k[0], v[0], out[0], lse[0], do[0], 33, 0, ln)
+    for g, r in zip(got, ref):
+        assert torch.equal(g[0], r)
+
+
+def test_llsa_paper_backward_rejects_unsupported_windows():
+    x = llsa_inputs(1, 200, 1, 64, 55, dtype="bf16", with_dout=True, channels=21)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    out, lse = bd.llsa_paper_forward(q, k, v, 70, 20)
+    with pytest.raises(bd.SAError):
+        bd.llsa_paper_backward(q, k, v, out, lse, do, 70, 20)
