@@ -11,6 +11,9 @@ its inputs in the 256 MB Infinity Cache.
 The same run also times, on their own workloads:
   * llsa_forward and llsa_backward, two-branch, same shapes (rows "llsa",
     "llsa_backward");
+  * llsa_paper_forward and llsa_paper_backward, the paper's channel form with
+    La + 1 = 9 channels, same shapes (rows "llsa_paper",
+    "llsa_paper_backward");
   * sa_stream_step, 64 streams x 1000 steps, ring of 64 + 8 + 1 frames, eager
     and replayed from a HIP graph (row "stream");
   * masked full attention in PyTorch (dense T x T scores, band mask) as the
@@ -237,6 +240,66 @@ def bench_llsa(steps, warmup):
         "algorithmic_bytes": byts,
         "useful_flops": flops,
     }
+
+
+def bench_llsa_paper(steps, warmup):
+    """The paper's (La+1)-channel LLSA forward and backward on the LLSA
+    workload's shapes (nine channels at La = 8)."""
+    w = WORKLOAD
+    C = w["La"] + 1
+    x = llsa_inputs(w["B"], w["T"], w["H"], w["d"], 6, dtype="bf16", lengths=w["lengths"],
+                    with_dout=True, channels=C)
+    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v", "dout")}
+    lengths = x["lengths"].cuda()
+    sets = []
+    for i in range(N_SETS):
+        s = {n: (t if i == 0 else t.clone()) for n, t in base.items()}
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty(C, w["B"], w["H"], w["T"], dtype=torch.float32, device="cuda")
+        for n in ("dq", "dk", "dv"):
+            s[n] = torch.empty_like(s["q"])
+        sets.append(s)
+
+    def fwd(s):
+        bd.llsa_paper_forward(s["q"], s["k"], s["v"], w["Lb"], w["La"], lengths, out=s["out"],
+                              lse=s["lse"])
+
+    def bwd(s):
+        bd.llsa_paper_backward(s["q"], s["k"], s["v"], s["out"], s["lse"], s["dout"], w["Lb"],
+                               w["La"], lengths, dq=s["dq"], dk=s["dk"], dv=s["dv"])
+
+    for i in range(max(warmup, N_SETS)):
+        fwd(sets[i % N_SETS])
+    torch.cuda.synchronize()
+    ms = launch_ms(fwd, sets, steps)
+    for i in range(warmup):
+        bwd(sets[i % N_SETS])
+    torch.cuda.synchronize()
+    bms = launch_ms(bwd, sets, steps)
+    L = x["lengths"].tolist()
+    rows = {}
+    for name, t, byts, flops, traffic in (
+            ("forward", ms, acc.llsa_paper_forward_bytes(L, w["H"], w["d"], w["La"]),
+             acc.llsa_paper_forward_flops(L, w["H"], w["d"], w["Lb"], w["La"]),
+             load_traffic("llsa_paper_fwd_traffic.json", source_sha("band_fwd.hip", "llsa_paper.hip"))),
+            ("backward", bms, acc.llsa_paper_backward_bytes(L, w["H"], w["d"], w["La"]),
+             acc.llsa_paper_backward_flops(L, w["H"], w["d"], w["Lb"], w["La"]),
+             load_traffic("llsa_paper_bwd_traffic.json", source_sha("band_bwd.hip", "llsa_paper.hip")))):
+        gbs = byts / (t * 1e-3) / 1e9
+        rows[name] = {
+            "workload": "LLSA %s, paper form with %d channels, bf16, B=16, T=800, H=12, d=64, "
+                        "Lb=64, La=8, lengths U[400,800]" % (name, C),
+            "ms_per_call": t,
+            "frames_per_s": sum(L) / (t * 1e-3),
+            "useful_tflops": flops / (t * 1e-3) / 1e12,
+            "algorithmic_gbs": gbs,
+            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": gbs / HBM_PEAK_GBS, "traffic": traffic,
+                         "per": "call (all launches of one call)"},
+            "algorithmic_bytes": byts,
+            "useful_flops": flops,
+        }
+    return rows["forward"], rows["backward"]
 
 
 def bench_stream():
@@ -549,6 +612,8 @@ def main():
     if not args.no_extras:
         log("LLSA forward and backward")
         line["llsa_backward"], line["llsa"] = bench_llsa(max(20, args.steps // 2), 5)
+        log("LLSA in the paper's channel form, forward and backward")
+        line["llsa_paper"], line["llsa_paper_backward"] = bench_llsa_paper(20, 3)
         log("streaming step")
         line["stream"] = bench_stream()
         log("masked full attention in PyTorch")

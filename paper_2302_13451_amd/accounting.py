@@ -77,6 +77,21 @@ def llsa_backward_flops(lengths, H: int, d: int, Lb: int, La: int) -> int:
     return 8 * d * H * (c + l)
 
 
+def llsa_paper_width_sums(lengths: Iterable[int], Lb: int, La: int):
+    """Pair counts of the (La+1)-channel LLSA, one per output channel c: the
+    window t+c-La-Lb .. t+c clipped to [0, len)."""
+    lengths = list(lengths)
+    return [window_width_sum(lengths, La + Lb - c, c) for c in range(La + 1)]
+
+
+def llsa_paper_forward_flops(lengths, H: int, d: int, Lb: int, La: int) -> int:
+    return 4 * d * H * sum(llsa_paper_width_sums(lengths, Lb, La))
+
+
+def llsa_paper_backward_flops(lengths, H: int, d: int, Lb: int, La: int) -> int:
+    return 8 * d * H * sum(llsa_paper_width_sums(lengths, Lb, La))
+
+
 def valid_frames(lengths) -> int:
     return sum(int(L) for L in lengths)
 
@@ -108,6 +123,17 @@ def llsa_backward_bytes(lengths, H: int, d: int, dtype: str = "bf16") -> int:
     f = valid_frames(lengths)
     e = ELEM_BYTES[dtype]
     return 16 * f * H * d * e + 2 * 4 * f * H
+
+
+def llsa_paper_forward_bytes(lengths, H: int, d: int, La: int, dtype: str = "bf16") -> int:
+    """Every channel's q, k, v read and out and lse written once per valid
+    frame: La + 1 times the SA forward's bytes."""
+    return (La + 1) * sa_forward_bytes(lengths, H, d, dtype)
+
+
+def llsa_paper_backward_bytes(lengths, H: int, d: int, La: int, dtype: str = "bf16") -> int:
+    """La + 1 times the SA backward's bytes."""
+    return (La + 1) * sa_backward_bytes(lengths, H, d, dtype)
 
 
 def sa_training_tensor_bytes(T: int, H: int, d: int, dtype: str = "bf16") -> int:

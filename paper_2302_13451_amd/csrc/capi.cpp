@@ -204,8 +204,8 @@ int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, f
   if (B == 0 || T == 0 || H == 0) return SA_OK;
   if (!lse) return fail(SA_ERR_NULL, "%s: lse is required", fn);
   if (int rc = check_ptrs(fn, {q, k, v, out}, {lse}, {lengths})) return rc;
-  if (static_cast<long long>(La + 1) * B * T * H > (1LL << 31) - 1)
-    return fail(SA_ERR_INVALID, "%s: (La+1)*B*T*H exceeds 2^31-1", fn);
+  if (static_cast<long long>(La + 1) * B * (T + La) * H > (1LL << 31) - 1)
+    return fail(SA_ERR_INVALID, "%s: (La+1)*B*(T+La)*H exceeds 2^31-1", fn);
   Lb = Lb < T ? Lb : T;  // La stays: it fixes the channel count
   sa::LlsaPaperArgs a{};
   a.q = q;
@@ -236,8 +236,8 @@ int llsa_paper_backward(const void* q, const void* k, const void* v, const void*
   if (B == 0 || T == 0 || H == 0) return SA_OK;
   if (!lse) return fail(SA_ERR_NULL, "%s: lse (from llsa_paper_forward) is required", fn);
   if (int rc = check_ptrs(fn, {q, k, v, out, dout, dq, dk, dv}, {lse}, {lengths})) return rc;
-  if (static_cast<long long>(2 * La + 1) * B * T * H > (1LL << 31) - 1)
-    return fail(SA_ERR_INVALID, "%s: (2La+1)*B*T*H exceeds 2^31-1", fn);
+  if (static_cast<long long>(2 * La + 1) * B * (T + La) * H > (1LL << 31) - 1)
+    return fail(SA_ERR_INVALID, "%s: (2La+1)*B*(T+La)*H exceeds 2^31-1", fn);
   Lb = Lb < T ? Lb : T;
   if (La > 0 && !sa::llsa_paper_backward_fits(d, Lb, La))
     return fail(SA_ERR_UNSUPPORTED, "%s: window Lb = %d, La = %d too wide for d = %d", fn, Lb, La, d);

@@ -58,13 +58,16 @@ __device__ __forceinline__ float row_sum(float x) {
   return x;
 }
 
-// One row (output channel c, sequence b, frame t, head h) per LPR = D / 4
-// lanes, four features per lane.
+// Rows are taken in anti-diagonal groups: the A + 1 rows (c, t = s - c),
+// c = 0 .. A, of one (sequence b, s, head h) read the same A diagonal frames
+// (c', s - c'), so a group's consecutive rows find them in the caches. One row
+// per LPR = D / 4 lanes, four features per lane.
 template <typename E, int D>
 __global__ __launch_bounds__(256) void llsa_paper_merge_kernel(PaperMergeDev a) {
   constexpr int LPR = D / 4;
   const int sub = threadIdx.x % LPR;
-  const long long nrows = static_cast<long long>(a.La + 1) * a.B * a.T * a.H;
+  const int G = a.La + 1, S = a.T + a.La;  // rows per group, anti-diagonals per sequence
+  const long long nrows = static_cast<long long>(G) * a.B * S * a.H;
   const size_t cstride = static_cast<size_t>(a.B) * a.T * a.H * D;
   const E* q = static_cast<const E*>(a.q);
   const E* k = static_cast<const E*>(a.k);
@@ -72,48 +75,66 @@ __global__ __launch_bounds__(256) void llsa_paper_merge_kernel(PaperMergeDev a) 
   E* out = static_cast<E*>(a.out);
   for (long long r = (static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x) / LPR; r < nrows;
        r += static_cast<long long>(gridDim.x) * blockDim.x / LPR) {
-    const int h = static_cast<int>(r % a.H);
-    const int t = static_cast<int>((r / a.H) % a.T);
-    const int b = static_cast<int>((r / (static_cast<long long>(a.H) * a.T)) % a.B);
-    const int c = static_cast<int>(r / (static_cast<long long>(a.H) * a.T * a.B));
+    const int c = static_cast<int>(r % G);
+    const long long grp = r / G;
+    const int h = static_cast<int>(grp % a.H);
+    const int sd = static_cast<int>((grp / a.H) % S);
+    const int b = static_cast<int>(grp / (static_cast<long long>(a.H) * S));
+    const int t = sd - c;
     int len = a.T;
     if (a.lengths) {
       len = a.lengths[b];
       len = len < 0 ? 0 : (len > a.T ? a.T : len);
     }
-    if (t >= len) continue;  // padding row: the band forward wrote it
+    if (t < 0 || t >= len) continue;  // no such frame, or a padding row (the band forward wrote it)
     float* lp = a.lse + ((static_cast<size_t>(c) * a.B + b) * a.H + h) * a.T + t;
     const float lb = *lp;  // natural log; -inf: the band part is empty
     const size_t row = c * cstride + row_index(b, t, h, a.T, a.H, D) + 4 * sub;
     float qf[4], yb[4];
     load4f<E>(q + row, qf);
     load4f<E>(out + row, yb);
-    // scores of the diagonal frames (natural-log scale)
-    float m = lb;
-    for (int cp = 0; cp < a.La; ++cp) {
-      const int tau = t + c - cp;
-      if (tau < 0 || tau >= len) continue;
-      float kf[4];
-      load4f<E>(k + cp * cstride + row_index(b, tau, h, a.T, a.H, D) + 4 * sub, kf);
-      const float s = row_sum<LPR>(qf[0] * kf[0] + qf[1] * kf[1] + qf[2] * kf[2] + qf[3] * kf[3]) * a.scale;
-      m = fmaxf(m, s);
-    }
-    const float wb = lb == kNegInf ? 0.f : __expf(lb - m);
-    float acc[4], den = wb;
+    // online softmax over the band part (weight exp(lb - m) on its normalised
+    // output) and the diagonal frames, CH of them per round of loads; a frame
+    // outside the sequence (or past channel A - 1) reads row (0, t) instead
+    // and gets weight 0
+    constexpr int CH = 4;
+    float m = lb, den = lb == kNegInf ? 0.f : 1.f, acc[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = wb == 0.f ? 0.f : wb * yb[i];  // yb is NaN for an empty band
-    for (int cp = 0; cp < a.La; ++cp) {
-      const int tau = t + c - cp;
-      if (tau < 0 || tau >= len) continue;
-      const size_t kr = cp * cstride + row_index(b, tau, h, a.T, a.H, D) + 4 * sub;
-      float kf[4], vf[4];
-      load4f<E>(k + kr, kf);
-      load4f<E>(v + kr, vf);
-      const float s = row_sum<LPR>(qf[0] * kf[0] + qf[1] * kf[1] + qf[2] * kf[2] + qf[3] * kf[3]) * a.scale;
-      const float w = __expf(s - m);
-      den += w;
+    for (int i = 0; i < 4; ++i) acc[i] = den == 0.f ? 0.f : yb[i];  // yb is NaN for an empty band
+    for (int c0 = 0; c0 < a.La; c0 += CH) {
+      float kf[CH][4], vf[CH][4], sc[CH];
+      bool ok[CH];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] += w * vf[i];
+      for (int j = 0; j < CH; ++j) {
+        const int cp = c0 + j, tau = t + c - cp;
+        ok[j] = cp < a.La && tau >= 0 && tau < len;
+        const size_t kr = (ok[j] ? cp * cstride + row_index(b, tau, h, a.T, a.H, D)
+                                 : row_index(b, t, h, a.T, a.H, D)) + 4 * sub;
+        load4f<E>(k + kr, kf[j]);
+        load4f<E>(v + kr, vf[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < CH; ++j)
+        sc[j] = row_sum<LPR>(qf[0] * kf[j][0] + qf[1] * kf[j][1] + qf[2] * kf[j][2] + qf[3] * kf[j][3]) * a.scale;
+      float mn = m;
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        sc[j] = ok[j] ? sc[j] : kNegInf;
+        mn = fmaxf(mn, sc[j]);
+      }
+      if (mn == kNegInf) continue;  // nothing seen yet
+      const float f = __expf(m - mn);  // 0 while m = -inf
+      den *= f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] *= f;
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        const float w = __expf(sc[j] - mn);
+        den += w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] += w * vf[j][i];
+      }
+      m = mn;
     }
     const float inv = 1.f / den;
 #pragma unroll
@@ -131,6 +152,10 @@ __global__ __launch_bounds__(256) void llsa_paper_merge_kernel(PaperMergeDev a) 
 // sum to the band part already in dq[c]; rows of the second kind,
 // (c', b, tau, h) for c' < A, gather dk[c'] and dv[c'] over the A + 1 queries
 // (c, tau + c' - c) that see them (channels c' < A take no band keys).
+// Both kinds are taken in anti-diagonal groups: for one (b, s, h) the query
+// rows (c, s - c), c = 0 .. A, and the key rows (c', s - c'), c' < A, are
+// exactly the pairs of one dense (A+1) x A block, so the group's 2A + 1
+// consecutive rows share every load through the caches.
 struct PaperDiagDev {
   const uint16_t *q, *o, *dout, *k, *v;
   const float* lse;
@@ -145,19 +170,22 @@ __global__ __launch_bounds__(256) void llsa_paper_bwd_diag_kernel(PaperDiagDev a
   constexpr int LPR = D / 4;
   const int sub = threadIdx.x % LPR;
   const int A = a.La;
+  const int G = 2 * A + 1, S = a.T + A;  // rows per group, anti-diagonals per sequence
   const long long per_ch = static_cast<long long>(a.B) * a.T * a.H;
-  const long long nq = (A + 1) * per_ch;  // rows of the first kind
-  const long long nrows = nq + A * per_ch;
+  const long long nrows = static_cast<long long>(G) * a.B * S * a.H;
   const size_t cstride = static_cast<size_t>(per_ch) * D;
   const size_t lstride = static_cast<size_t>(per_ch);
   for (long long r = (static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x) / LPR; r < nrows;
        r += static_cast<long long>(gridDim.x) * blockDim.x / LPR) {
-    const bool query_kind = r < nq;
-    const long long rr = query_kind ? r : r - nq;
-    const int h = static_cast<int>(rr % a.H);
-    const int t = static_cast<int>((rr / a.H) % a.T);
-    const int b = static_cast<int>((rr / (static_cast<long long>(a.H) * a.T)) % a.B);
-    const int c = static_cast<int>(rr / per_ch);
+    const int gi = static_cast<int>(r % G);  // row within the group
+    const long long grp = r / G;
+    const int h = static_cast<int>(grp % a.H);
+    const int sd = static_cast<int>((grp / a.H) % S);
+    const int b = static_cast<int>(grp / (static_cast<long long>(a.H) * S));
+    const bool query_kind = gi <= A;
+    const int c = query_kind ? gi : gi - A - 1;
+    const int t = sd - c;
+    if (t < 0 || t >= a.T) continue;  // no such frame
     int len = a.T;
     if (a.lengths) {
       len = a.lengths[b];
@@ -172,18 +200,30 @@ __global__ __launch_bounds__(256) void llsa_paper_bwd_diag_kernel(PaperDiagDev a
       load4f<uint16_t>(a.dout + own, df);
       load4f<uint16_t>(a.o + own, of);
       const float dn = row_sum<LPR>(df[0] * of[0] + df[1] * of[1] + df[2] * of[2] + df[3] * of[3]);
-      for (int cp = 0; cp < A; ++cp) {
-        const int tau = t + c - cp;
-        if (tau < 0 || tau >= len) continue;
-        const size_t kr = cp * cstride + row_index(b, tau, h, a.T, a.H, D) + 4 * sub;
-        float kf[4], vf[4];
-        load4f<uint16_t>(a.k + kr, kf);
-        load4f<uint16_t>(a.v + kr, vf);
-        const float s = row_sum<LPR>(qf[0] * kf[0] + qf[1] * kf[1] + qf[2] * kf[2] + qf[3] * kf[3]) * a.scale;
-        const float dp = row_sum<LPR>(df[0] * vf[0] + df[1] * vf[1] + df[2] * vf[2] + df[3] * vf[3]);
-        const float ds = __expf(s - lse) * (dp - dn);
+      constexpr int CH = 4;  // diagonal frames per round of loads (see the forward merge)
+      for (int c0 = 0; c0 < A; c0 += CH) {
+        float kf[CH][4], vf[CH][4], sc[CH], dp[CH];
+        bool ok[CH];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] += ds * kf[i];
+        for (int j = 0; j < CH; ++j) {
+          const int cp = c0 + j, tau = t + c - cp;
+          ok[j] = cp < A && tau >= 0 && tau < len;
+          const size_t kr = (ok[j] ? cp * cstride + row_index(b, tau, h, a.T, a.H, D)
+                                   : row_index(b, t, h, a.T, a.H, D)) + 4 * sub;
+          load4f<uint16_t>(a.k + kr, kf[j]);
+          load4f<uint16_t>(a.v + kr, vf[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          sc[j] = row_sum<LPR>(qf[0] * kf[j][0] + qf[1] * kf[j][1] + qf[2] * kf[j][2] + qf[3] * kf[j][3]) * a.scale;
+          dp[j] = row_sum<LPR>(df[0] * vf[j][0] + df[1] * vf[j][1] + df[2] * vf[j][2] + df[3] * vf[j][3]);
+        }
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          const float ds = ok[j] ? __expf(sc[j] - lse) * (dp[j] - dn) : 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] += ds * kf[j][i];
+        }
       }
       float dq[4];
       load4f<uint16_t>(a.dq + own, dq);
@@ -252,7 +292,7 @@ hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hi
   m.La = x.La;
   m.lengths = x.lengths;
   m.scale = 1.f / sqrtf(static_cast<float>(x.d));
-  const long long rows = static_cast<long long>(2 * x.La + 1) * x.B * x.T * x.H;
+  const long long rows = static_cast<long long>(2 * x.La + 1) * x.B * (x.T + x.La) * x.H;
   const long long blocks = (rows * (x.d / 4) + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
   if (x.d == 64)
@@ -286,7 +326,7 @@ hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStr
   }
   if (A == 0) return hipSuccess;  // one channel: the band is the whole window
   PaperMergeDev m{x.q, x.k, x.v, x.out, x.lse, x.B, x.T, x.H, A, x.lengths, 1.f / sqrtf(static_cast<float>(x.d))};
-  const long long rows = static_cast<long long>(A + 1) * x.B * x.T * x.H;
+  const long long rows = static_cast<long long>(A + 1) * x.B * (x.T + A) * x.H;
   const long long threads = rows * (x.d / 4);
   const long long blocks = (threads + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);

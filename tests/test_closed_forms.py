@@ -69,3 +69,17 @@ def test_byte_accounting():
     f = 1200
     assert acc.sa_forward_bytes(lengths, 12, 64) == 4 * f * 12 * 64 * 2 + 4 * f * 12
     assert acc.sa_backward_bytes(lengths, 12, 64) == 8 * f * 12 * 64 * 2 + 4 * f * 12
+
+
+def test_llsa_paper_width_sums_brute_force():
+    """Pairs of the (La+1)-channel LLSA per channel, counted frame by frame:
+    channel c of frame t reads t+c-La-Lb .. t+c clipped to [0, len)."""
+    lengths = [0, 1, 7, 30, 64]
+    for Lb, La in ((0, 1), (5, 3), (12, 8), (40, 2)):
+        got = acc.llsa_paper_width_sums(lengths, Lb, La)
+        for c in range(La + 1):
+            want = sum(len([tau for tau in range(t + c - La - Lb, t + c + 1) if 0 <= tau < L])
+                       for L in lengths for t in range(L))
+            assert got[c] == want, (Lb, La, c)
+    # with two channels the paper's module is the two-branch one
+    assert acc.llsa_paper_width_sums(lengths, 9, 1) == list(acc.llsa_width_sums(lengths, 9, 1))
