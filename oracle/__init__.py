@@ -70,8 +70,10 @@ def _load():
                                          _DP, i, i, i, i, i, i, _IP, i]
     lib.oracle_sa_stream_step.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, i, _IP, _IP,
                                           i, i, i, i, i, _IP]
+    lib.oracle_llsa_stream_step.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, _DP, _DP, _DP,
+                                            _DP, _DP, i, _IP, _IP, _IP, i, i, i, i, i, _IP]
     for fn in (lib.oracle_sa_forward, lib.oracle_sa_backward, lib.oracle_llsa_forward,
-               lib.oracle_llsa_backward, lib.oracle_sa_stream_step):
+               lib.oracle_llsa_backward, lib.oracle_sa_stream_step, lib.oracle_llsa_stream_step):
         fn.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -280,3 +282,39 @@ class StreamOracle:
             self.d, self.Lb, self.La, _ip(self.lengths))
         _check(rc, "oracle_sa_stream_step")
         return out, emitted
+
+
+class LlsaStreamOracle:
+    """Two-branch LLSA streaming step: per-stream key/value rings of the
+    causal branch C and the look-ahead branch L, driven one step at a time.
+    At step u a stream takes branch C's frame u and branch L's frame u - La
+    and emits the causal output of frame u and the look-ahead output of frame
+    u - La. ``R`` must be at least ``Lb + La + 1``."""
+
+    def __init__(self, S: int, H: int, d: int, Lb: int, La: int, R: int, lengths=None):
+        if R < Lb + La + 1:
+            raise ValueError("the rings must hold at least Lb + La + 1 frames")
+        self.S, self.H, self.d, self.Lb, self.La, self.R = S, H, d, Lb, La, R
+        self.rings = [np.zeros((S, R, H, d), dtype=np.float64) for _ in range(4)]
+        self.step_ctr = np.zeros((S,), dtype=np.int32)
+        self.lengths = _lengths(lengths, S)
+
+    def step(self, qc, kc, vc, ql, kl, vl):
+        """Feed branch C's frame u and branch L's frame u - La of every stream
+        (``[S][H][d]`` each); returns ``(out_c, emitted_c, out_l, emitted_l)``
+        with ``emitted[s] = -1`` where stream s emitted nothing."""
+        xs = [_f64(x) for x in (qc, kc, vc, ql, kl, vl)]
+        shape = (self.S, self.H, self.d)
+        for x in xs:
+            if x.shape != shape:
+                raise ValueError("frames must have shape %s" % (shape,))
+        out_c = np.empty(shape, dtype=np.float64)
+        out_l = np.empty(shape, dtype=np.float64)
+        em_c = np.empty((self.S,), dtype=np.int32)
+        em_l = np.empty((self.S,), dtype=np.int32)
+        rc = _load().oracle_llsa_stream_step(
+            *[_dp(x) for x in xs], _dp(out_c), _dp(out_l), *[_dp(r) for r in self.rings], self.R,
+            _ip(self.step_ctr), _ip(em_c), _ip(em_l), self.S, self.H, self.d, self.Lb, self.La,
+            _ip(self.lengths))
+        _check(rc, "oracle_llsa_stream_step")
+        return out_c, em_c, out_l, em_l

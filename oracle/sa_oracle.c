@@ -21,6 +21,8 @@
  *   - LLSA backward: the exact adjoint of that forward, row by row as for
  *     SA (the paper's Eq. 16 covers only the values).
  *   - SA streaming step: a literal simulation of per-stream ring buffers.
+ *   - Two-branch LLSA streaming step: the same simulation with the rings of
+ *     both branches, branch L's frames arriving La steps after branch C's.
  *
  * Readings of the paper taken here (Sec. "Streaming Attention" is silent on
  * them):
@@ -531,6 +533,106 @@ int oracle_sa_stream_step(const double* q, const double* k, const double* v, dou
     } else {
       memset(os, 0, sizeof(double) * hd);
       if (emitted) emitted[s] = -1;
+    }
+    step[s] = (int32_t)(u + 1);
+  }
+  free(kr); free(vr); free(a);
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Two-branch LLSA streaming step (infer_llsa)                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The two-branch LLSA of oracle_llsa_forward (channels 0 .. A-1 held by the
+ * causal branch C, channel A by the look-ahead branch L; the causal output
+ * reads window [t - A - B, t], the look-ahead output [t - B, t + A], frame
+ * tau from branch L when tau <= t - A, resp. tau <= t) driven one step at a
+ * time. Frame versions of branch C are available when their frame arrives,
+ * those of branch L A frames later (as in a stack of such layers, where
+ * branch L of a layer is the look-ahead output of the one below).
+ *
+ * State per stream s: step counter u = step[s]; key/value rings of branch C
+ * (kc_ring, vc_ring) and of branch L (kl_ring, vl_ring), [s][R][H][d] each.
+ * One call:
+ *   1. if 0 <= u < len_s, branch C's frame u (qc, kc, vc: [S][H][d]) arrives:
+ *      its key and value go to slot u mod R of the C rings;
+ *   2. if 0 <= t = u - A < len_s, branch L's frame t (ql, kl, vl) arrives:
+ *      its key and value go to slot t mod R of the L rings;
+ *   3. if frame u arrived in 1, out_c[s] receives the causal output of frame
+ *      u (query qc) over frames max(0, u - A - B) .. u, and emitted_c[s] = u;
+ *      otherwise out_c[s] is zero and emitted_c[s] = -1;
+ *   4. if frame t arrived in 2, out_l[s] receives the look-ahead output of
+ *      frame t (query ql) over frames max(0, t - B) .. min(len_s - 1, t + A),
+ *      and emitted_l[s] = t; otherwise zero and -1;
+ *   5. step[s] = u + 1.
+ * Both windows are read from the rings only.
+ */
+int oracle_llsa_stream_step(const double* qc, const double* kc, const double* vc,
+                            const double* ql, const double* kl, const double* vl,
+                            double* out_c, double* out_l, double* kc_ring, double* vc_ring,
+                            double* kl_ring, double* vl_ring, int R, int32_t* step,
+                            int32_t* emitted_c, int32_t* emitted_l, int S, int H, int d, int Lb,
+                            int La, const int32_t* lengths) {
+  if (S < 0 || H < 0 || d <= 0 || Lb < 0 || La < 0) return ORC_ERR_INVALID;
+  if ((long)R < (long)Lb + La + 1) return ORC_ERR_INVALID;
+  if (S == 0 || H == 0) return ORC_OK;
+  if (!qc || !kc || !vc || !ql || !kl || !vl || !out_c || !out_l || !kc_ring || !vc_ring ||
+      !kl_ring || !vl_ring || !step)
+    return ORC_ERR_INVALID;
+  const size_t hd = (size_t)H * d;
+  const double** kr = (const double**)malloc(sizeof(double*) * (size_t)R);
+  const double** vr = (const double**)malloc(sizeof(double*) * (size_t)R);
+  double* a = (double*)malloc(sizeof(double) * (size_t)R);
+  if (!kr || !vr || !a) {
+    free(kr); free(vr); free(a);
+    return ORC_ERR_NOMEM;
+  }
+  for (int s = 0; s < S; ++s) {
+    const long u = step[s];
+    const long len = lengths ? (lengths[s] < 0 ? 0 : lengths[s]) : (long)INT32_MAX;
+    double* kcr = kc_ring + (size_t)s * R * hd;
+    double* vcr = vc_ring + (size_t)s * R * hd;
+    double* klr = kl_ring + (size_t)s * R * hd;
+    double* vlr = vl_ring + (size_t)s * R * hd;
+    const long t = u - La;
+    const int got_c = u >= 0 && u < len;
+    const int got_l = t >= 0 && t < len;
+    if (got_c) {
+      memcpy(kcr + (size_t)(u % R) * hd, kc + (size_t)s * hd, sizeof(double) * hd);
+      memcpy(vcr + (size_t)(u % R) * hd, vc + (size_t)s * hd, sizeof(double) * hd);
+    }
+    if (got_l) {
+      memcpy(klr + (size_t)(t % R) * hd, kl + (size_t)s * hd, sizeof(double) * hd);
+      memcpy(vlr + (size_t)(t % R) * hd, vl + (size_t)s * hd, sizeof(double) * hd);
+    }
+    /* output o = 0: causal output of frame u; o = 1: look-ahead output of frame t */
+    for (int o = 0; o < 2; ++o) {
+      const int due = o == 0 ? got_c : got_l;
+      double* os = (o == 0 ? out_c : out_l) + (size_t)s * hd;
+      int32_t* em = o == 0 ? emitted_c : emitted_l;
+      if (!due) {
+        memset(os, 0, sizeof(double) * hd);
+        if (em) em[s] = -1;
+        continue;
+      }
+      const long f = o == 0 ? u : t;             /* the emitted frame */
+      const long lo = o == 0 ? lmax(0, f - La - Lb) : lmax(0, f - Lb);
+      const long hi = o == 0 ? f : lmin(len - 1, f + La);
+      const long split = o == 0 ? f - La : f;    /* frames <= split come from branch L */
+      const double* qrow = (o == 0 ? qc : ql) + (size_t)s * hd;
+      const int W = (int)(hi - lo + 1);
+      for (int h = 0; h < H; ++h) {
+        for (int j = 0; j < W; ++j) {
+          const long tau = lo + j;
+          const size_t off = (size_t)(tau % R) * hd + (size_t)h * d;
+          kr[j] = (tau <= split ? klr : kcr) + off;
+          vr[j] = (tau <= split ? vlr : vcr) + off;
+        }
+        attend_row(qrow + (size_t)h * d, kr, vr, W, d, a, os + (size_t)h * d);
+      }
+      if (em) em[s] = (int32_t)f;
     }
     step[s] = (int32_t)(u + 1);
   }
