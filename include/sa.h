@@ -222,6 +222,54 @@ int sa_stream_step(const void* q, const void* k, const void* v, void* out,
                    int S, int H, int d, int Lb, int La,
                    const int32_t* lengths, int dtype, void* stream);
 
+/*
+ * One step of streaming two-branch LLSA inference (infer_llsa) for S
+ * independent streams: the module of llsa_forward (Eq. 14/15, channels
+ * 0 .. La-1 held by branch C, channel La by branch L) driven frame by frame.
+ * Frame versions of branch C exist when their frame arrives; those of branch
+ * L La steps later (in a stack of such layers, branch L of a layer is the
+ * look-ahead output of the layer below, which needs La frames of future).
+ * Per stream s with step counter u = step[s], and t = u - La:
+ *   1. if 0 <= u < lengths[s], branch C's frame u (qc, kc, vc [s]) arrives:
+ *      its key and value go to slot u mod R of kc_ring and vc_ring;
+ *   2. if 0 <= t < lengths[s], branch L's frame t (ql, kl, vl [s]) arrives:
+ *      its key and value go to slot t mod R of kl_ring and vl_ring;
+ *   3. if frame u arrived, out_c[s] receives the causal output of frame u
+ *      (query qc) over frames max(0, u-La-Lb) .. u and emitted_c[s] = u;
+ *      otherwise out_c[s] is zero and emitted_c[s] = -1;
+ *   4. if frame t arrived, out_l[s] receives the look-ahead output of frame
+ *      t (query ql) over frames max(0, t-Lb) .. min(len-1, t+La) and
+ *      emitted_l[s] = t; otherwise zero and -1;
+ *   5. step[s] = u + 1 (advanced on the device).
+ * In both windows frame tau is read from branch L when tau <= t and from
+ * branch C otherwise. Running steps u = 0 .. L+La-1 emits exactly
+ * llsa_forward's rows: the causal ones as their frame arrives, the
+ * look-ahead ones La steps later. Chaining layers (out_c of step u as the
+ * next layer's qc/kc/vc source for frame u, out_l as its branch-L source for
+ * frame t) keeps the top layer's look-ahead latency at La frames for any
+ * depth. A stream whose counter starts negative joins -u steps later.
+ *
+ * qc, kc, vc : [S][H][d] branch C's frame u of every stream (read only)
+ * ql, kl, vl : [S][H][d] branch L's frame u - La of every stream (read only)
+ * out_c      : [S][H][d] causal output of frame u
+ * out_l      : [S][H][d] look-ahead output of frame u - La
+ * kc_ring, vc_ring, kl_ring, vl_ring : [S][R][H][d] caller-owned rings,
+ *              R >= Lb+La+1
+ * step       : device int32 [S], read and advanced
+ * emitted_c, emitted_l : device int32 [S] (nullable)
+ * lengths    : device int32 [S] (nullable: open-ended streams)
+ * Lb + La + 1 must not exceed SA_STREAM_MAX_WINDOW. Calls that share rings
+ * or counters must be ordered on one stream; a call may be captured in a
+ * HIP graph and replayed.
+ */
+int llsa_stream_step(const void* qc, const void* kc, const void* vc,
+                     const void* ql, const void* kl, const void* vl,
+                     void* out_c, void* out_l,
+                     void* kc_ring, void* vc_ring, void* kl_ring, void* vl_ring, int R,
+                     int32_t* step, int32_t* emitted_c, int32_t* emitted_l,
+                     int S, int H, int d, int Lb, int La,
+                     const int32_t* lengths, int dtype, void* stream);
+
 /* Message for the last non-zero status returned to the calling thread. */
 const char* sa_last_error(void);
 

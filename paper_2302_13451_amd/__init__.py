@@ -9,7 +9,9 @@ use of one of its names).
 
 _BINDING_NAMES = {
     "SA_BF16", "SA_F32", "SAError", "library_path", "load_library", "sa_forward",
-    "sa_backward", "llsa_forward", "sa_stream_step", "StreamState",
+    "sa_backward", "llsa_forward", "llsa_backward", "llsa_paper_forward",
+    "llsa_paper_backward", "sa_stream_step", "StreamState", "llsa_stream_step",
+    "LlsaStreamState",
 }
 
 

@@ -44,6 +44,8 @@ _SIGNATURES = {
                       _i, _vp],
     "sa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _vp,
                        _i, _vp],
+    "llsa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp,
+                         _vp, _vp, _i, _i, _i, _i, _i, _vp, _i, _vp],
     "sa_last_error": [],
     "sa_abi_version": [],
 }
@@ -290,3 +292,45 @@ def sa_stream_step(state: StreamState, q, k, v, out=None, *, stream=None):
         _ptr(state.v_ring), state.R, _ptr(state.step_ctr), _ptr(state.emitted), S, H, d,
         state.Lb, state.La, _ptr(state.lengths), code, _stream(dev, stream)))
     return out, state.emitted
+
+
+class LlsaStreamState:
+    """Caller-owned rings and counters of ``llsa_stream_step`` for S streams:
+    key/value rings of branch C and of branch L (allocated here with torch;
+    the library never allocates)."""
+
+    def __init__(self, S: int, H: int, d: int, Lb: int, La: int, R: Optional[int] = None,
+                 lengths=None, dtype=torch.bfloat16, device="cuda"):
+        self.S, self.H, self.d, self.Lb, self.La = S, H, d, Lb, La
+        self.R = R if R is not None else Lb + La + 1
+        self.rings = [torch.zeros((S, self.R, H, d), dtype=dtype, device=device)
+                      for _ in range(4)]  # k, v of branch C; k, v of branch L
+        self.step_ctr = torch.zeros((S,), dtype=torch.int32, device=device)
+        self.emitted_c = torch.full((S,), -1, dtype=torch.int32, device=device)
+        self.emitted_l = torch.full((S,), -1, dtype=torch.int32, device=device)
+        self.lengths = None if lengths is None else torch.as_tensor(
+            lengths, dtype=torch.int32).to(device)
+
+
+def llsa_stream_step(state: LlsaStreamState, qc, kc, vc, ql, kl, vl, out_c=None, out_l=None, *,
+                     stream=None):
+    """One streaming step: branch C's frame u (qc, kc, vc) and branch L's
+    frame u - La (ql, kl, vl), each [S][H][d]. Returns (out_c, emitted_c,
+    out_l, emitted_l): the causal output of frame u and the look-ahead output
+    of frame u - La; emitted = -1 where nothing was emitted."""
+    S, H, d = state.S, state.H, state.d
+    dt = state.rings[0].dtype
+    dev = state.rings[0].device
+    for n, t in (("qc", qc), ("kc", kc), ("vc", vc), ("ql", ql), ("kl", kl), ("vl", vl)):
+        _require(t, n, (S, H, d), dt, dev)
+    out_c = torch.empty_like(qc) if out_c is None else out_c
+    out_l = torch.empty_like(qc) if out_l is None else out_l
+    _require(out_c, "out_c", (S, H, d), dt, dev)
+    _require(out_l, "out_l", (S, H, d), dt, dev)
+    code = _dtype_code(state.rings[0])
+    _check(load_library().llsa_stream_step(
+        _ptr(qc), _ptr(kc), _ptr(vc), _ptr(ql), _ptr(kl), _ptr(vl), _ptr(out_c), _ptr(out_l),
+        *[_ptr(r) for r in state.rings], state.R, _ptr(state.step_ctr), _ptr(state.emitted_c),
+        _ptr(state.emitted_l), S, H, d, state.Lb, state.La, _ptr(state.lengths), code,
+        _stream(dev, stream)))
+    return out_c, state.emitted_c, out_l, state.emitted_l

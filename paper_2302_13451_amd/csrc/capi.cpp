@@ -338,4 +338,54 @@ int sa_stream_step(const void* q, const void* k, const void* v, void* out, void*
                       fn);
 }
 
+int llsa_stream_step(const void* qc, const void* kc, const void* vc, const void* ql,
+                     const void* kl, const void* vl, void* out_c, void* out_l, void* kc_ring,
+                     void* vc_ring, void* kl_ring, void* vl_ring, int R, int32_t* step,
+                     int32_t* emitted_c, int32_t* emitted_l, int S, int H, int d, int Lb, int La,
+                     const int32_t* lengths, int dtype, void* stream) {
+  const char* fn = "llsa_stream_step";
+  if (S < 0 || H < 0) return fail(SA_ERR_INVALID, "%s: negative size (S=%d, H=%d)", fn, S, H);
+  if (Lb < 0 || La < 0)
+    return fail(SA_ERR_INVALID, "%s: negative look-back/look-ahead (Lb=%d, La=%d)", fn, Lb, La);
+  if (dtype != SA_F32 && dtype != SA_BF16)
+    return fail(SA_ERR_UNSUPPORTED, "%s: unsupported dtype %d", fn, dtype);
+  if (d != 32 && d != 64) return fail(SA_ERR_UNSUPPORTED, "%s: unsupported head dim %d", fn, d);
+  const long long W = static_cast<long long>(Lb) + La + 1;
+  if (W > SA_STREAM_MAX_WINDOW)
+    return fail(SA_ERR_INVALID, "%s: window Lb+La+1 = %lld exceeds %d", fn, W,
+                SA_STREAM_MAX_WINDOW);
+  if (R < W) return fail(SA_ERR_INVALID, "%s: ring of %d frames is smaller than the window %lld", fn, R, W);
+  if (S == 0 || H == 0) return SA_OK;
+  if (int rc = check_ptrs(fn, {qc, kc, vc, ql, kl, vl, out_c, out_l, kc_ring, vc_ring, kl_ring, vl_ring},
+                            {step}, {emitted_c, emitted_l, lengths}))
+    return rc;
+  if (static_cast<long long>(S) * R * H * d > (1LL << 40))
+    return fail(SA_ERR_INVALID, "%s: ring too large", fn);
+  sa::LlsaStreamStepArgs a{};
+  a.qc = qc;
+  a.kc = kc;
+  a.vc = vc;
+  a.ql = ql;
+  a.kl = kl;
+  a.vl = vl;
+  a.out_c = out_c;
+  a.out_l = out_l;
+  a.kc_ring = kc_ring;
+  a.vc_ring = vc_ring;
+  a.kl_ring = kl_ring;
+  a.vl_ring = vl_ring;
+  a.R = R;
+  a.step = step;
+  a.emitted_c = emitted_c;
+  a.emitted_l = emitted_l;
+  a.S = S;
+  a.H = H;
+  a.d = d;
+  a.Lb = Lb;
+  a.La = La;
+  a.lengths = lengths;
+  return check_launch(
+      sa::launch_llsa_stream_step(a, elem(dtype), static_cast<hipStream_t>(stream)), fn);
+}
+
 }  // extern "C"

@@ -110,4 +110,17 @@ struct StreamStepArgs {
 
 hipError_t launch_stream_step(const StreamStepArgs& a, ElemType et, hipStream_t stream);
 
+struct LlsaStreamStepArgs {
+  const void *qc, *kc, *vc, *ql, *kl, *vl;
+  void *out_c, *out_l;
+  void *kc_ring, *vc_ring, *kl_ring, *vl_ring;
+  int R;
+  int32_t* step;
+  int32_t *emitted_c, *emitted_l;
+  int S, H, d, Lb, La;
+  const int32_t* lengths;
+};
+
+hipError_t launch_llsa_stream_step(const LlsaStreamStepArgs& a, ElemType et, hipStream_t stream);
+
 }  // namespace sa

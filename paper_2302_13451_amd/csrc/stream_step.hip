@@ -80,6 +80,70 @@ struct DevStream {
   float scale_log2;
 };
 
+// Attention of one query row (one head) over the W frames lo .. lo + W - 1 by
+// one wave: krow(tau) and vrow(tau) give frame tau's key and value rows, wts
+// holds the wave's W score slots, orow receives the output row.
+template <typename E, int D, typename KRow, typename VRow>
+__device__ __forceinline__ void attend_wave(const E* qrow, KRow krow, VRow vrow, int lo, int W, float scale_log2,
+                                            float* wts, E* orow, int lane) {
+  constexpr int EPC = 16 / sizeof(E);
+  constexpr int CH = D / EPC;
+  constexpr int NKG = 64 / CH;
+  auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
+  float qv[D];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) unpack16<E>(chunk(qrow, c), qv + c * EPC);
+
+  // scores: one key per lane
+  float mloc = kNegInf;
+  for (int j = lane; j < W; j += 64) {
+    const E* kr = krow(lo + j);
+    float z = 0.f;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      float kf[EPC];
+      unpack16<E>(chunk(kr, c), kf);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) z += qv[c * EPC + e] * kf[e];
+    }
+    z *= scale_log2;
+    wts[j] = z;
+    mloc = fmaxf(mloc, z);
+  }
+  const float m = wave_max(mloc);
+  float lpart = 0.f;
+  for (int j = lane; j < W; j += 64) {
+    const float pw = fast_exp2(wts[j] - m);
+    wts[j] = pw;
+    lpart += pw;
+  }
+  const float inv = 1.f / wave_sum(lpart);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // weighted sum: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
+  const int dc = lane % CH, kg = lane / CH;
+  float acc[EPC];
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+  for (int j = kg; j < W; j += NKG) {
+    float vf[EPC];
+    unpack16<E>(chunk(vrow(lo + j), dc), vf);
+    const float pw = wts[j];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] += pw * vf[e];
+  }
+#pragma unroll
+  for (int o = CH; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] += __shfl_xor(acc[e], o);
+  if (kg == 0) *reinterpret_cast<uint4*>(orow + dc * EPC) = pack16<E>(acc, inv);
+  // the next head reuses wts: finish these reads first
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <typename E, int D>
 __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a) {
   constexpr int EPC = 16 / sizeof(E);   // elements per 16-byte chunk
@@ -132,65 +196,151 @@ __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a
     auto krow = [&](int tau) { return (tau == u ? kin : kring + static_cast<size_t>(tau % R) * HD) + ho; };
     auto vrow = [&](int tau) { return (tau == u ? vin : vring + static_cast<size_t>(tau % R) * HD) + ho; };
     const E* qrow = (La == 0 ? qin : qring + static_cast<size_t>(t % QR) * HD) + ho;
-    float qv[D];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) unpack16<E>(chunk(qrow, c), qv + c * EPC);
-
-    // scores: one key per lane
-    float mloc = kNegInf;
-    for (int j = lane; j < W; j += 64) {
-      const E* kr = krow(lo + j);
-      float z = 0.f;
-#pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        float kf[EPC];
-        unpack16<E>(chunk(kr, c), kf);
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) z += qv[c * EPC + e] * kf[e];
-      }
-      z *= a.scale_log2;
-      wts[j] = z;
-      mloc = fmaxf(mloc, z);
-    }
-    const float m = wave_max(mloc);
-    float lpart = 0.f;
-    for (int j = lane; j < W; j += 64) {
-      const float pw = fast_exp2(wts[j] - m);
-      wts[j] = pw;
-      lpart += pw;
-    }
-    const float inv = 1.f / wave_sum(lpart);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // weighted sum: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
-    const int dc = lane % CH, kg = lane / CH;
-    float acc[EPC];
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-    for (int j = kg; j < W; j += NKG) {
-      float vf[EPC];
-      unpack16<E>(chunk(vrow(lo + j), dc), vf);
-      const float pw = wts[j];
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[e] += pw * vf[e];
-    }
-#pragma unroll
-    for (int o = CH; o < 64; o <<= 1)
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[e] += __shfl_xor(acc[e], o);
-    if (kg == 0) *reinterpret_cast<uint4*>(out + ho + dc * EPC) = pack16<E>(acc, inv);
-    // the next head reuses wts: finish these reads first
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    attend_wave<E, D>(qrow, krow, vrow, lo, W, a.scale_log2, wts, out + ho, lane);
   }
   if (threadIdx.x == 0 && a.emitted) a.emitted[s] = emit ? t : -1;
   __syncthreads();  // every wave has read step[s]
   if (threadIdx.x == 0) a.step[s] = u + 1;
 }
 
+// One step of streaming two-branch LLSA inference (infer_llsa). At step u a
+// stream takes branch C's frame u and branch L's frame t = u - La (in a stack,
+// the causal and look-ahead outputs the layer below emitted at this step) and
+// emits the causal output of frame u and the look-ahead output of frame t.
+// Both windows are the frames u - La - Lb .. u (clipped to the sequence), frame
+// tau taken from branch L when tau <= t and from branch C otherwise (Eq. 14/15
+// with channels 0 .. La-1 held by C and channel La by L), so the two outputs
+// differ only in their query. Layout and work split as in stream_step_kernel,
+// the two outputs one after the other per head.
+struct DevLlsaStream {
+  const void *qc, *kc, *vc, *ql, *kl, *vl;
+  void *out_c, *out_l;
+  void *kc_ring, *vc_ring, *kl_ring, *vl_ring;
+  int R;
+  int32_t* step;
+  int32_t *emitted_c, *emitted_l;
+  int S, H, Lb, La;
+  int wmax;  // Lb + La + 1: score slots per wave
+  const int32_t* lengths;
+  float scale_log2;
+};
+
+template <typename E, int D>
+__global__ __launch_bounds__(64 * kMaxWaves) void llsa_stream_step_kernel(DevLlsaStream a) {
+  constexpr int EPC = 16 / sizeof(E);
+  constexpr int CH = D / EPC;
+  static_assert(CH * EPC == D && 4 * CH <= 64, "row must split into 16-byte chunks");
+  extern __shared__ float wts_all[];
+  const int s = blockIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  float* wts = wts_all + w * a.wmax;
+  const int H = a.H, La = a.La, R = a.R;
+  const size_t HD = static_cast<size_t>(H) * D;
+
+  const int u = a.step[s];
+  int len = a.lengths ? a.lengths[s] : 0x7fffffff;
+  len = len < 0 ? 0 : len;
+  const bool got_c = u >= 0 && u < len;  // branch C's frame u arrives; its causal output is due
+  const long long tl = static_cast<long long>(u) - La;
+  const bool got_l = tl >= 0 && tl < len;  // branch L's frame t arrives; its look-ahead output is due
+  const int t = static_cast<int>(got_l ? tl : 0);
+
+  auto in = [&](const void* p) { return static_cast<const E*>(p) + s * HD; };
+  auto ring = [&](void* p) { return static_cast<E*>(p) + static_cast<size_t>(s) * R * HD; };
+  const E *qc = in(a.qc), *kc = in(a.kc), *vc = in(a.vc), *ql = in(a.ql), *kl = in(a.kl), *vl = in(a.vl);
+  E *kcr = ring(a.kc_ring), *vcr = ring(a.vc_ring), *klr = ring(a.kl_ring), *vlr = ring(a.vl_ring);
+  E* out_c = static_cast<E*>(a.out_c) + s * HD;
+  E* out_l = static_cast<E*>(a.out_l) + s * HD;
+  auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
+  const long long split = static_cast<long long>(u) - La;  // frames <= split come from branch L
+  // every due output reads frames lo .. hi
+  const int lo = static_cast<int>(max(0LL, split - a.Lb));
+  const int hi = min(len - 1, u);
+
+  for (int h = w; h < H; h += nw) {
+    const size_t ho = static_cast<size_t>(h) * D;
+    // store the new frames: lanes 0 .. 2 CH - 1 branch C's key and value,
+    // lanes 2 CH .. 4 CH - 1 branch L's
+    if (lane < 4 * CH) {
+      const int which = lane / CH, c = lane % CH;
+      const bool br_l = which >= 2;
+      if (br_l ? got_l : got_c) {
+        const E* src = which == 0 ? kc : which == 1 ? vc : which == 2 ? kl : vl;
+        E* dst = (which == 0 ? kcr : which == 1 ? vcr : which == 2 ? klr : vlr) +
+                 static_cast<size_t>((br_l ? t : u) % R) * HD;
+        *reinterpret_cast<uint4*>(dst + ho + c * EPC) = chunk(src + ho, c);
+      }
+    }
+    // frame tau's rows; the frames that arrived in this step are still in the inputs
+    auto krow = [&](int tau) {
+      return (tau <= split ? (tau == t ? kl : klr + static_cast<size_t>(tau % R) * HD)
+                           : (tau == u ? kc : kcr + static_cast<size_t>(tau % R) * HD)) + ho;
+    };
+    auto vrow = [&](int tau) {
+      return (tau <= split ? (tau == t ? vl : vlr + static_cast<size_t>(tau % R) * HD)
+                           : (tau == u ? vc : vcr + static_cast<size_t>(tau % R) * HD)) + ho;
+    };
+    for (int o = 0; o < 2; ++o) {
+      E* orow = (o == 0 ? out_c : out_l) + ho;
+      if (!(o == 0 ? got_c : got_l)) {
+        if (lane < CH) *reinterpret_cast<uint4*>(orow + lane * EPC) = make_uint4(0, 0, 0, 0);
+        continue;
+      }
+      attend_wave<E, D>((o == 0 ? qc : ql) + ho, krow, vrow, lo, hi - lo + 1, a.scale_log2, wts, orow, lane);
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (a.emitted_c) a.emitted_c[s] = got_c ? u : -1;
+    if (a.emitted_l) a.emitted_l[s] = got_l ? t : -1;
+  }
+  __syncthreads();  // every wave has read step[s]
+  if (threadIdx.x == 0) a.step[s] = u + 1;
+}
+
 }  // namespace
+
+hipError_t launch_llsa_stream_step(const LlsaStreamStepArgs& a, ElemType et, hipStream_t stream) {
+  DevLlsaStream d;
+  d.qc = a.qc;
+  d.kc = a.kc;
+  d.vc = a.vc;
+  d.ql = a.ql;
+  d.kl = a.kl;
+  d.vl = a.vl;
+  d.out_c = a.out_c;
+  d.out_l = a.out_l;
+  d.kc_ring = a.kc_ring;
+  d.vc_ring = a.vc_ring;
+  d.kl_ring = a.kl_ring;
+  d.vl_ring = a.vl_ring;
+  d.R = a.R;
+  d.step = a.step;
+  d.emitted_c = a.emitted_c;
+  d.emitted_l = a.emitted_l;
+  d.S = a.S;
+  d.H = a.H;
+  d.Lb = a.Lb;
+  d.La = a.La;
+  d.lengths = a.lengths;
+  d.wmax = a.Lb + a.La + 1;
+  d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
+  const int nw = a.H < kMaxWaves ? a.H : kMaxWaves;
+  const dim3 grid(a.S), block(64 * nw);
+  const size_t lds = static_cast<size_t>(nw) * d.wmax * sizeof(float);
+  if (et == kBF16) {
+    if (a.d == 64)
+      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 64>), grid, block, lds, stream, d);
+    else
+      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 32>), grid, block, lds, stream, d);
+  } else {
+    if (a.d == 64)
+      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 64>), grid, block, lds, stream, d);
+    else
+      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 32>), grid, block, lds, stream, d);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_stream_step(const StreamStepArgs& a, ElemType et, hipStream_t stream) {
   DevStream d;

@@ -30,7 +30,7 @@ def lib():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("sa_forward", "sa_backward", "llsa_forward", "llsa_paper_forward", "llsa_backward",
-              "llsa_paper_backward", "sa_stream_step",
+              "llsa_paper_backward", "sa_stream_step", "llsa_stream_step",
               "sa_last_error", "sa_abi_version"):
         assert n in names
 
@@ -142,6 +142,22 @@ def test_stream_validation(lib):
     assert st(step=None) == bd.SA_ERR_NULL
     assert st(step=ctypes.c_void_p(0x10002)) == bd.SA_ERR_INVALID
     assert st(q=None) == bd.SA_ERR_NULL
+    assert st(S=-1) == bd.SA_ERR_INVALID
+    assert st(d=16) == bd.SA_ERR_UNSUPPORTED
+
+
+def test_llsa_stream_validation(lib):
+    def st(R=11, S=4, Lb=8, La=2, step=FAKE, kl=FAKE, d=64):
+        return lib.llsa_stream_step(FAKE, FAKE, FAKE, FAKE, kl, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    FAKE, FAKE, R, step, None, None, S, 2, d, Lb, La, None,
+                                    bd.SA_BF16, None)
+    assert st(R=10) == bd.SA_ERR_INVALID        # ring smaller than Lb + La + 1
+    assert "smaller than the window" in lib.sa_last_error().decode()
+    assert st(Lb=1000, La=100, R=2000) == bd.SA_ERR_INVALID
+    assert st(S=0) == bd.SA_OK
+    assert st(step=None) == bd.SA_ERR_NULL
+    assert st(kl=None) == bd.SA_ERR_NULL
+    assert st(kl=FAKE_ODD) == bd.SA_ERR_INVALID
     assert st(S=-1) == bd.SA_ERR_INVALID
     assert st(d=16) == bd.SA_ERR_UNSUPPORTED
 
