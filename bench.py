@@ -15,7 +15,10 @@ The same run also times, on their own workloads:
     La + 1 = 9 channels, same shapes (rows "llsa_paper",
     "llsa_paper_backward");
   * sa_stream_step, 64 streams x 1000 steps, ring of 64 + 8 + 1 frames, eager
-    and replayed from a HIP graph (row "stream");
+    and replayed from a HIP graph (row "stream"), and llsa_stream_step on the
+    same shapes (row "llsa_stream");
+  * the algorithmic latency of a 12-layer streaming stack, SA against LLSA
+    (row "stream_latency");
   * masked full attention in PyTorch (dense T x T scores, band mask) as the
     GPU baseline the paper argues against (row "masked_attention_torch");
   * the CPU oracle on the host cores (``cpu_baseline``).
@@ -362,7 +365,7 @@ def bench_stream():
     widths = [Lb + La + 1] * S
     byts = acc.stream_step_bytes(widths, S, H, d)
     flops = acc.stream_step_flops(widths, H, d)
-    mean_step = t.mean_ms()
+    mean_step = lat[len(lat) // 2]  # median: a rare host hiccup skews the mean
     return {
         "workload": "SA streaming step bf16, 64 streams x 1000 steps, H=12, d=64, ring 64 past + "
                     "8 look-ahead + current",
@@ -376,6 +379,117 @@ def bench_stream():
         "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
         "note": "ring is L2/MALL resident; the step is launch-bound",
     }
+
+
+def bench_llsa_stream():
+    """llsa_stream_step on the streaming shapes: 64 streams, H=12, d=64, Lb=64,
+    La=8, open-ended, every stream emitting both outputs every step after the
+    first La steps."""
+    c = STREAM
+    S, H, d, Lb, La, steps = c["S"], c["H"], c["d"], c["Lb"], c["La"], c["steps"]
+    x = stream_inputs(steps, S, H, d, c["seed"], dtype="bf16")
+    y = stream_inputs(steps, S, H, d, c["seed"] + 1, dtype="bf16")
+    fc = [x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v")]
+    fl = [y[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v")]
+    oc = torch.empty(S, H, d, dtype=torch.bfloat16, device="cuda")
+    ol = torch.empty_like(oc)
+
+    def step(st, u):
+        bd.llsa_stream_step(st, fc[0][u], fc[1][u], fc[2][u], fl[0][u], fl[1][u], fl[2][u],
+                            out_c=oc, out_l=ol)
+
+    st = bd.LlsaStreamState(S, H, d, Lb, La)
+    for u in range(20):
+        step(st, u)
+    st = bd.LlsaStreamState(S, H, d, Lb, La)
+    torch.cuda.synchronize()
+    t = EventTimer()
+    for u in range(steps):
+        e = t.start()
+        step(st, u)
+        t.stop(e)
+    torch.cuda.synchronize()
+    lat = sorted(t.all_ms())
+    # graph: capture 100 steps, replay them (the counters advance on the device)
+    n_cap = 100
+    st = bd.LlsaStreamState(S, H, d, Lb, La)
+    bufs = [torch.empty(n_cap, S, H, d, dtype=torch.bfloat16, device="cuda") for _ in range(6)]
+    side = bd.LlsaStreamState(S, H, d, Lb, La)
+    step(side, 0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n_cap):
+            bd.llsa_stream_step(st, *[b[i] for b in bufs], out_c=oc, out_l=ol)
+    torch.cuda.synchronize()
+    g_ms = 0.0
+    for r in range(steps // n_cap):
+        sl = slice(r * n_cap, (r + 1) * n_cap)
+        for b, src in zip(bufs, fc + fl):
+            b.copy_(src[sl])
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        graph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        g_ms += s0.elapsed_time(s1)
+    widths = [Lb + La + 1] * S
+    byts = acc.llsa_stream_step_bytes(widths, S, H, d)
+    flops = acc.llsa_stream_step_flops(widths, H, d)
+    mean_step = lat[len(lat) // 2]  # median: a rare host hiccup skews the mean
+    return {
+        "workload": "LLSA (two-branch) streaming step bf16, 64 streams x 1000 steps, H=12, d=64, "
+                    "rings of 64 past + 8 look-ahead + current frames per branch",
+        "graph_steps_per_s": (steps // n_cap * n_cap) / (g_ms * 1e-3),
+        "graph_frames_per_s": S * (steps // n_cap * n_cap) / (g_ms * 1e-3),
+        "step_latency_ms_p50": lat[len(lat) // 2],
+        "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
+        "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
+        "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
+        "note": "two outputs per stream and step; the rings are L2/MALL resident; launch-bound",
+    }
+
+
+STACK = dict(layers=12, S=64, H=12, d=64, Lb=64, La=8, T=200, frame_ms=20.0, seed=9)
+
+
+def bench_stream_latency():
+    """Algorithmic latency of a 12-layer streaming stack (Tab. 3): the step at
+    which the top layer emits each frame, SA against LLSA, and the wall time
+    of one step of the whole stack."""
+    from paper_2302_13451_amd.streaming import StackedStream
+
+    c = STACK
+    L, S, H, d, Lb, La, T = c["layers"], c["S"], c["H"], c["d"], c["Lb"], c["La"], c["T"]
+    g = torch.Generator(device="cpu").manual_seed(c["seed"])
+    W = [torch.randn(3, H * d, H * d, generator=g) / math.sqrt(H * d) for _ in range(L)]
+    x = torch.randn(T, S, H, d, generator=g).to(torch.bfloat16).cuda()
+    res = {"workload": "%d-layer streaming stack, %d streams of %d frames, H=%d, d=%d, Lb=%d, "
+                       "La=%d, bf16, random projections; %g ms per frame"
+                       % (L, S, T, H, d, Lb, La, c["frame_ms"])}
+    for kind in ("sa", "llsa"):
+        model = StackedStream(kind, W, S, H, d, Lb, La, lengths=[T] * S)
+        t = EventTimer()
+        lag = []
+        for n in range(T + L * La):
+            e = t.start()
+            _, em = model.step(x[n] if n < T else None)
+            t.stop(e)
+            f = int(em[0])
+            if f >= 0:
+                lag.append(n - f)
+        torch.cuda.synchronize()
+        ms = sorted(t.all_ms())
+        frames = max(lag)
+        res[kind] = {
+            "algorithmic_latency_frames": frames,
+            "algorithmic_latency_s": frames * c["frame_ms"] * 1e-3,
+            "latency_constant_over_frames": min(lag) == frames and len(lag) == T,
+            "stack_step_ms_p50": ms[len(ms) // 2],
+            "stack_step_ms_p99": ms[min(len(ms) - 1, int(0.99 * len(ms)))],
+        }
+    return res
 
 
 def bench_masked_attention(steps=5):
@@ -616,6 +730,10 @@ def main():
         line["llsa_paper"], line["llsa_paper_backward"] = bench_llsa_paper(20, 3)
         log("streaming step")
         line["stream"] = bench_stream()
+        log("LLSA streaming step")
+        line["llsa_stream"] = bench_llsa_stream()
+        log("12-layer streaming stack latency")
+        line["stream_latency"] = bench_stream_latency()
         log("masked full attention in PyTorch")
         try:
             line["masked_attention_torch"] = bench_masked_attention()

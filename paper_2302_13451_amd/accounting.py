@@ -162,3 +162,21 @@ def stream_step_bytes(window_widths: Iterable[int], appended: int, H: int, d: in
 
 def stream_step_flops(window_widths: Iterable[int], H: int, d: int) -> int:
     return 4 * d * stream_step_pairs(window_widths, H)
+
+
+def llsa_stream_step_bytes(window_widths: Iterable[int], appended: int, H: int, d: int,
+                           dtype: str = "bf16") -> int:
+    """One two-branch LLSA streaming step: each emitting stream reads its two
+    queries and the keys and values of the shared window and writes its two
+    output rows; each accepting stream reads the new key and value of both
+    branches and writes them into the rings."""
+    e = ELEM_BYTES[dtype]
+    widths = [int(w) for w in window_widths]
+    row = H * d * e
+    return (4 * len(widths) * row + 2 * sum(widths) * row  # queries + outputs + window
+            + appended * 8 * row)                         # two branches' k, v in and out
+
+
+def llsa_stream_step_flops(window_widths: Iterable[int], H: int, d: int) -> int:
+    """Two outputs (causal and look-ahead) over each emitting stream's window."""
+    return 2 * 4 * d * stream_step_pairs(window_widths, H)
