@@ -305,6 +305,15 @@ def bench_llsa_paper(steps, warmup):
     return rows["forward"], rows["backward"]
 
 
+def stream_roofline(byts, step_ms):
+    """Algorithmic bytes of one streaming step over its median duration,
+    against HBM (the step's working set is cache resident and a launch costs
+    about 2.5 us, so this fraction stays small)."""
+    gbs = byts / (step_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "per": "step (one launch)"}
+
+
 def bench_stream():
     c = STREAM
     S, H, d, Lb, La, steps = c["S"], c["H"], c["d"], c["Lb"], c["La"], c["steps"]
@@ -377,6 +386,7 @@ def bench_stream():
         "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
         "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
         "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
+        "roofline": stream_roofline(byts, mean_step),
         "note": "ring is L2/MALL resident; the step is launch-bound",
     }
 
@@ -447,6 +457,7 @@ def bench_llsa_stream():
         "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
         "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
         "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
+        "roofline": stream_roofline(byts, mean_step),
         "note": "two outputs per stream and step; the rings are L2/MALL resident; launch-bound",
     }
 

@@ -45,22 +45,12 @@ __device__ __forceinline__ void load4<float>(const float* p, float* x) {
   const float4 v = *reinterpret_cast<const float4*>(p);
   x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
 }
-template <>
-__device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float* x) {
-  const uint2 v = *reinterpret_cast<const uint2*>(p);
-  x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xffff0000u);
-  x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xffff0000u);
-}
 
 template <typename E>
 __device__ __forceinline__ void store4(E* p, const float* x);
 template <>
 __device__ __forceinline__ void store4<float>(float* p, const float* x) {
   *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
-}
-template <>
-__device__ __forceinline__ void store4<uint16_t>(uint16_t* p, const float* x) {
-  *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
 }
 
 template <typename E, int D>
