@@ -265,6 +265,252 @@ __global__ __launch_bounds__(256) void llsa_paper_bwd_diag_kernel(PaperDiagDev a
   }
 }
 
+// ---------------------------------------------------------------------------
+// MFMA forms of the two diagonal passes (bfloat16, La <= 15). One anti-diagonal
+// group (b, s, h) is a dense block of at most 16 queries (channel c, frame
+// s - c, c = 0 .. A) against at most 15 keys (channel c', frame s - c',
+// c' < A), so one wave takes one group: lane (col, g) loads the rows of query
+// col and of key col (16-byte pieces 8g .. 8g + 7 of each 32-feature slice),
+// which are at the same time the A-operand rows and the B-operand columns of
+// v_mfma_f32_16x16x32_bf16. The score tile comes out as S^T (lane (i, g)
+// holds S[i][4g + e]) or S (lane (j, g) holds S[4g + e][j]); its four values
+// per lane become the B operand of the next product with the contraction
+// index k = 8g + e for e < 4 and zeros at k = 8g + 4 .. 8g + 7, and the A
+// operand of that product (a row tile transposed: lane (f, g) holds
+// X[4g + e][f]) is read from the rows staged in LDS (stride D + 4 elements,
+// which keeps the four row groups of a transposed read on distinct banks).
+// Every row is read from memory once per group.
+
+constexpr int kDiagWaves = 4;  // waves per workgroup, one group each
+constexpr int kMaxMfmaLa = 15;  // A + 1 queries and A keys fit one 16 x 16 tile
+
+template <int D>
+__device__ __forceinline__ bf16x8 ld_row8(const uint16_t* p, bool ok) {
+  return ok ? __builtin_bit_cast(bf16x8, ld16(p)) : bf16x8{};
+}
+
+// Stages a row piece (8 elements at column c) into an LDS row tile of stride
+// D + 4 (8-byte aligned rows).
+template <int D>
+__device__ __forceinline__ void stage8(uint16_t* tile, int row, int c, bf16x8 x) {
+  const u32x4 u = __builtin_bit_cast(u32x4, x);
+  uint16_t* p = tile + row * (D + 4) + c;
+  st8(p, u32x2{u[0], u[1]});
+  st8(p + 4, u32x2{u[2], u[3]});
+}
+
+// A operand of a product that contracts over the 16 rows of an LDS tile:
+// lane (f, g) receives X[4g + e][f0 + f] for e < 4 and zeros at e >= 4.
+template <int D>
+__device__ __forceinline__ bf16x8 tile_tr(const uint16_t* tile, int f0, int col, int g) {
+  bf16x8 r{};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = __builtin_bit_cast(__bf16, tile[(4 * g + e) * (D + 4) + f0 + col]);
+  return r;
+}
+
+// Four values of a score-shaped tile as the B operand (k = 8g + e, e < 4).
+__device__ __forceinline__ bf16x8 as_b4(const float* x) {
+  bf16x8 r{};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = static_cast<__bf16>(x[e]);
+  return r;
+}
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_merge_mfma_kernel(PaperMergeDev a) {
+  constexpr int NS = D / 32, NF = D / 16;
+  __shared__ __attribute__((aligned(16))) uint16_t s_tile[kDiagWaves][16 * (D + 4)];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = lane & 15, g = lane >> 4;
+  uint16_t* sv = s_tile[w];
+  const int A = a.La, S = a.T + A, T = a.T, H = a.H;
+  const long long ngroups = static_cast<long long>(a.B) * S * H;
+  const size_t cs = static_cast<size_t>(a.B) * T * H * D;
+  const size_t ls = static_cast<size_t>(a.B) * H * T;
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+  const uint16_t* k = static_cast<const uint16_t*>(a.k);
+  const uint16_t* v = static_cast<const uint16_t*>(a.v);
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  const float scale = a.scale;
+  for (long long gi = static_cast<long long>(blockIdx.x) * kDiagWaves + w; gi < ngroups;
+       gi += static_cast<long long>(gridDim.x) * kDiagWaves) {
+    const int h = static_cast<int>(gi % H);
+    const int sd = static_cast<int>((gi / H) % S);
+    const int b = static_cast<int>(gi / (static_cast<long long>(H) * S));
+    int len = T;
+    if (a.lengths) {
+      len = a.lengths[b];
+      len = len < 0 ? 0 : (len > T ? T : len);
+    }
+    const int tc = sd - col;  // frame of query col and of key col
+    const bool qv = col <= A && tc >= 0 && tc < len;
+    const bool kv = col < A && tc >= 0 && tc < len;
+    const size_t qrow = col * cs + row_index(b, tc, h, T, H, D);
+    bf16x8 qa[NS], ka[NS], va[NS];
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      qa[s2] = ld_row8<D>(q + qrow + 32 * s2 + 8 * g, qv);
+      ka[s2] = ld_row8<D>(k + qrow + 32 * s2 + 8 * g, kv);
+      va[s2] = ld_row8<D>(v + qrow + 32 * s2 + 8 * g, kv);
+    }
+    float* lp = a.lse + col * ls + (static_cast<size_t>(b) * H + h) * T + tc;
+    const float lb = qv ? *lp : kNegInf;
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) stage8<D>(sv, col, 32 * s2 + 8 * g, va[s2]);
+    f32x4 st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[s2], qa[s2], st, 0, 0, 0);
+    // lane (i = col, g): scores of query i against keys j = 4g + e
+    float sc[4], m = lb;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = 4 * g + e, tj = sd - j;
+      const bool ok = qv && j < A && tj >= 0 && tj < len;
+      sc[e] = ok ? st[e] * scale : kNegInf;
+      m = fmaxf(m, sc[e]);
+    }
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    float p[4], ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      p[e] = sc[e] == kNegInf ? 0.f : __expf(sc[e] - m);
+      ps += p[e];
+    }
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    const float wb = lb == kNegInf ? 0.f : __expf(lb - m);  // the band part's weight
+    const float den = wb + ps;
+    const bf16x8 pb = as_b4(p);
+    wave_sync();
+#pragma unroll
+    for (int fb = 0; fb < NF; ++fb) {
+      const f32x4 y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sv, 16 * fb, col, g), pb,
+                                                             f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+      if (qv) {  // lane (i, g) holds features 16 fb + 4g .. + 3 of query i
+        uint16_t* o = out + qrow + 16 * fb + 4 * g;
+        const u32x2 yb = *reinterpret_cast<const u32x2*>(o);
+        const float inv = 1.f / den;
+        float r[4];
+        const float bv[4] = {__uint_as_float(yb[0] << 16), __uint_as_float(yb[0] & 0xffff0000u),
+                             __uint_as_float(yb[1] << 16), __uint_as_float(yb[1] & 0xffff0000u)};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = (wb == 0.f ? y[e] : wb * bv[e] + y[e]) * inv;  // bv is NaN for an empty band
+        st8(o, u32x2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])});
+      }
+    }
+    if (qv && g == 0) *lp = m + __logf(den);
+    wave_sync();  // the tile is rewritten by the next group
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kernel(PaperDiagDev a) {
+  constexpr int NS = D / 32, NF = D / 16, TS = 16 * (D + 4);
+  __shared__ __attribute__((aligned(16))) uint16_t s_tile[kDiagWaves][3 * TS];  // q, k, dout rows
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = lane & 15, g = lane >> 4;
+  uint16_t* sq = s_tile[w];
+  uint16_t* sk = sq + TS;
+  uint16_t* sdo = sk + TS;
+  const int A = a.La, S = a.T + A, T = a.T, H = a.H;
+  const long long ngroups = static_cast<long long>(a.B) * S * H;
+  const size_t cs = static_cast<size_t>(a.B) * T * H * D;
+  const size_t ls = static_cast<size_t>(a.B) * H * T;
+  const float scale = a.scale;
+  for (long long gi = static_cast<long long>(blockIdx.x) * kDiagWaves + w; gi < ngroups;
+       gi += static_cast<long long>(gridDim.x) * kDiagWaves) {
+    const int h = static_cast<int>(gi % H);
+    const int sd = static_cast<int>((gi / H) % S);
+    const int b = static_cast<int>(gi / (static_cast<long long>(H) * S));
+    int len = T;
+    if (a.lengths) {
+      len = a.lengths[b];
+      len = len < 0 ? 0 : (len > T ? T : len);
+    }
+    const int tc = sd - col;  // frame of query col and of key col
+    const bool qv = col <= A && tc >= 0 && tc < len;
+    const bool kv = col < A && tc >= 0 && tc < len;
+    const size_t row = col * cs + row_index(b, tc, h, T, H, D);
+    bf16x8 qa[NS], da[NS], ka[NS], va[NS];
+    float dn = 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      const int c0 = 32 * s2 + 8 * g;
+      qa[s2] = ld_row8<D>(a.q + row + c0, qv);
+      da[s2] = ld_row8<D>(a.dout + row + c0, qv);
+      ka[s2] = ld_row8<D>(a.k + row + c0, kv);
+      va[s2] = ld_row8<D>(a.v + row + c0, kv);
+      dn = dot_bf16x8(da[s2], ld_row8<D>(a.o + row + c0, qv), dn);
+    }
+    dn += __shfl_xor(dn, 16, 64);
+    dn += __shfl_xor(dn, 32, 64);  // D of query col
+    const float lse = qv ? a.lse[col * ls + (static_cast<size_t>(b) * H + h) * T + tc] : 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      stage8<D>(sq, col, 32 * s2 + 8 * g, qa[s2]);
+      stage8<D>(sk, col, 32 * s2 + 8 * g, ka[s2]);
+      stage8<D>(sdo, col, 32 * s2 + 8 * g, da[s2]);
+    }
+    f32x4 st = {0.f, 0.f, 0.f, 0.f}, dpt = st, sq4 = st, dp = st;
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[s2], qa[s2], st, 0, 0, 0);   // S^T
+      dpt = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[s2], da[s2], dpt, 0, 0, 0); // dP^T
+      sq4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s2], ka[s2], sq4, 0, 0, 0); // S
+      dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(da[s2], va[s2], dp, 0, 0, 0);   // dP
+    }
+    // S^T layout, lane (i = col, g): pairs (i, j = 4g + e); S layout, lane
+    // (j = col, g): pairs (i = 4g + e, j)
+    float dst[4], ds[4], pw[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 4 * g + e, tr = sd - r;
+      const bool rq = r <= A && tr >= 0 && tr < len;  // query r
+      const bool rk = r < A && tr >= 0 && tr < len;   // key r
+      const float lse_r = __shfl(lse, r, 64), dn_r = __shfl(dn, r, 64);
+      const float p_t = qv && rk ? __expf(st[e] * scale - lse) : 0.f;
+      dst[e] = p_t * (dpt[e] - dn);
+      pw[e] = rq && kv ? __expf(sq4[e] * scale - lse_r) : 0.f;
+      ds[e] = pw[e] * (dp[e] - dn_r);
+    }
+    const bf16x8 bdst = as_b4(dst), bds = as_b4(ds), bp = as_b4(pw);
+    wave_sync();
+    const bool kout = col < A && tc >= 0 && tc < T;  // a key row of this group (zeros past the length)
+#pragma unroll
+    for (int fb = 0; fb < NF; ++fb) {
+      const int f0 = 16 * fb;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      const f32x4 gq = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sk, f0, col, g), bdst, z, 0, 0, 0);
+      const f32x4 gk = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sq, f0, col, g), bds, z, 0, 0, 0);
+      const f32x4 gv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sdo, f0, col, g), bp, z, 0, 0, 0);
+      const size_t off = row + f0 + 4 * g;  // features f0 + 4g .. + 3 of row col
+      if (qv) {
+        uint16_t* p = a.dq + off;
+        const u32x2 o = *reinterpret_cast<const u32x2*>(p);
+        const float r0 = __uint_as_float(o[0] << 16) + scale * gq[0];
+        const float r1 = __uint_as_float(o[0] & 0xffff0000u) + scale * gq[1];
+        const float r2 = __uint_as_float(o[1] << 16) + scale * gq[2];
+        const float r3 = __uint_as_float(o[1] & 0xffff0000u) + scale * gq[3];
+        st8(p, u32x2{pack_bf16x2(r0, r1), pack_bf16x2(r2, r3)});
+      }
+      if (kout) {
+        st8(a.dk + off, kv ? u32x2{pack_bf16x2(scale * gk[0], scale * gk[1]), pack_bf16x2(scale * gk[2], scale * gk[3])}
+                           : u32x2{0u, 0u});
+        st8(a.dv + off, kv ? u32x2{pack_bf16x2(gv[0], gv[1]), pack_bf16x2(gv[2], gv[3])} : u32x2{0u, 0u});
+      }
+    }
+    wave_sync();  // the tiles are rewritten by the next group
+  }
+}
+
 }  // namespace
 
 hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hipStream_t stream) {
@@ -292,6 +538,16 @@ hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hi
   m.La = x.La;
   m.lengths = x.lengths;
   m.scale = 1.f / sqrtf(static_cast<float>(x.d));
+  if (x.La <= kMaxMfmaLa) {  // one wave per anti-diagonal group
+    const long long groups = static_cast<long long>(x.B) * (x.T + x.La) * x.H;
+    const long long blocks = (groups + kDiagWaves - 1) / kDiagWaves;
+    const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
+    if (x.d == 64)
+      hipLaunchKernelGGL(llsa_paper_bwd_diag_mfma_kernel<64>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    else
+      hipLaunchKernelGGL(llsa_paper_bwd_diag_mfma_kernel<32>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    return hipGetLastError();
+  }
   const long long rows = static_cast<long long>(2 * x.La + 1) * x.B * (x.T + x.La) * x.H;
   const long long blocks = (rows * (x.d / 4) + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
@@ -326,6 +582,16 @@ hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStr
   }
   if (A == 0) return hipSuccess;  // one channel: the band is the whole window
   PaperMergeDev m{x.q, x.k, x.v, x.out, x.lse, x.B, x.T, x.H, A, x.lengths, 1.f / sqrtf(static_cast<float>(x.d))};
+  if (et == kBF16 && A <= kMaxMfmaLa) {  // one wave per anti-diagonal group
+    const long long groups = static_cast<long long>(x.B) * (x.T + A) * x.H;
+    const long long blocks = (groups + kDiagWaves - 1) / kDiagWaves;
+    const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
+    if (x.d == 64)
+      hipLaunchKernelGGL(llsa_paper_merge_mfma_kernel<64>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    else
+      hipLaunchKernelGGL(llsa_paper_merge_mfma_kernel<32>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    return hipGetLastError();
+  }
   const long long rows = static_cast<long long>(A + 1) * x.B * (x.T + A) * x.H;
   const long long threads = rows * (x.d / 4);
   const long long blocks = (threads + 255) / 256;
