@@ -43,6 +43,8 @@ def check(out, lse, yr, lr, dtype):
     (2, 100, 1, 64, 17, 0, (30, 100)),   # one channel: plain causal SA
     (3, 9, 2, 64, 5, 12, (0, 9, 4)),     # look-ahead longer than the sequences
     (66, 40, 1, 32, 10, 2, (0, 40)),
+    (2, 110, 2, 64, 30, 15, (40, 110)),  # the widest look-ahead of the one-tile diagonal pass
+    (2, 110, 2, 32, 30, 16, (40, 110)),  # and one past it
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_paper_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):
@@ -144,6 +146,8 @@ def check_bwd(got, ref):
     (2, 150, 1, 32, 150, 50, (70, 150)),
     (3, 9, 2, 64, 5, 12, (0, 9, 4)),     # look-ahead longer than the sequences
     (66, 40, 1, 32, 10, 2, (0, 40)),
+    (2, 110, 2, 64, 40, 15, (40, 110)),  # the widest look-ahead of the one-tile diagonal pass
+    (2, 110, 2, 32, 40, 16, (40, 110)),  # and one past it
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_paper_backward_parity(oracle_mod, B, T, H, d, Lb, La, lengths, scale):
