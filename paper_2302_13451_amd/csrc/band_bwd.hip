@@ -1154,8 +1154,11 @@ struct LlsaBwdDev {
 // the key and value bands of both branches and the query and dout bands of
 // both outputs (SEG rows each, frames outside the sequence zero-filled), and
 // -D and lse log2(e) of both query bands. Waves 0-3 / 4-7 take the query role
-// of output 0 / 1 (both segments), waves 8-11 / 12-15 the key role of branch
-// 0 / 1 (both outputs); each wave owns 16 rows and stores them.
+// of output 0 / 1 (both segments). Branch L's key role (two long segments) is
+// split by output: waves 8-11 take branch C's key role (both outputs) and then
+// branch L's output-0 segment, waves 12-15 branch L's output-1 segment, and
+// the two halves of branch L's sums meet in LDS once every wave is done with
+// the bands. Each gradient row is stored by one wave.
 template <int D>
 __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
   constexpr int NT = 1024;
@@ -1293,30 +1296,54 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
                                           r0, wq, len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
     }
     store_rows_direct<D>(a.dq[j] + slice, fs, r0, nrows, aq, 1.f, valid, lane);
+    __syncthreads();  // the key roles' hand-over (two barriers)
+    __syncthreads();
   } else {
-    const int i = role - 2;
+    // branch L's key role is split by output: waves 8-11 take branch C (both
+    // outputs, stored) and then branch L's output-0 segment, waves 12-15 its
+    // output-1 segment, and hand their sum to waves 8-11 at the end
     f32x4 adv[NB], adk[NB];
-    const int c_own = 16 * wq + col - a.koff[i];  // key band row of frame r0 + col
-    const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
-    const bool any = i == 1 || has_c;
-    if (any) {
+    auto key_role = [&](int j, int i, auto acc) {
+      const int c_own = 16 * wq + col - a.koff[i];  // key band row of frame r0 + col
+      const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
+      const int lo = a.lo[j][i], hi = a.hi[j][i];
+      const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
+      const int sbs = rel & ~15;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      bwd_key_role<D, SEG, false, decltype(acc)::value>(bands_of(j, i), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own,
+                                                        r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk, sbs);
+    };
+    if (role == 2) {
+      if (has_c) {
+        key_role(0, 0, std::false_type{});
+        key_role(1, 0, std::true_type{});
+      }
+      store_rows_direct<D>(a.dv[0] + slice, fs, r0, nrows, adv, 1.f, valid && has_c, lane);
+      store_rows_direct<D>(a.dk[0] + slice, fs, r0, nrows, adk, a.scale, valid && has_c, lane);
+      key_role(0, 1, std::false_type{});
+    } else {
+      key_role(1, 1, std::false_type{});
+    }
+    __syncthreads();  // every wave is done with the bands: their space takes the hand-over
+    f32x4* s_red = reinterpret_cast<f32x4*>(s_band);
+    const int ri = wq * 64 + lane;
+    if (role == 3) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int lo = a.lo[j][i], hi = a.hi[j][i];
-        const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
-        const int sbs = rel & ~15;
-        const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
-        const SubBlockAddr<D, SEG> sa(lane, 16 * wq + sbs);
-        if (j == 0)
-          bwd_key_role<D, SEG, false, false>(bands_of(j, i), sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
-                                             lane, adv, adk, sbs);
-        else
-          bwd_key_role<D, SEG, false, true>(bands_of(j, i), sa, own, r0, wq, len, -lo, hi, nblk, a.scale_log2,
-                                            lane, adv, adk, sbs);
+      for (int x = 0; x < NB; ++x) {
+        s_red[(2 * x) * 256 + ri] = adv[x];
+        s_red[(2 * x + 1) * 256 + ri] = adk[x];
       }
     }
-    store_rows_direct<D>(a.dv[i] + slice, fs, r0, nrows, adv, 1.f, valid && any, lane);
-    store_rows_direct<D>(a.dk[i] + slice, fs, r0, nrows, adk, a.scale, valid && any, lane);
+    __syncthreads();
+    if (role == 2) {
+#pragma unroll
+      for (int x = 0; x < NB; ++x) {
+        adv[x] += s_red[(2 * x) * 256 + ri];
+        adk[x] += s_red[(2 * x + 1) * 256 + ri];
+      }
+      store_rows_direct<D>(a.dv[1] + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+      store_rows_direct<D>(a.dk[1] + slice, fs, r0, nrows, adk, a.scale, valid, lane);
+    }
   }
 }
 
