@@ -462,7 +462,7 @@ def bench_llsa_stream():
     }
 
 
-STACK = dict(layers=12, S=64, H=12, d=64, Lb=64, La=8, T=200, frame_ms=20.0, seed=9)
+STACK = dict(layers=12, S=64, H=12, d=64, Lb=64, La=(8, 16), T=200, frame_ms=20.0, seed=9)
 
 
 def bench_stream_latency():
@@ -472,34 +472,35 @@ def bench_stream_latency():
     from paper_2302_13451_amd.streaming import StackedStream
 
     c = STACK
-    L, S, H, d, Lb, La, T = c["layers"], c["S"], c["H"], c["d"], c["Lb"], c["La"], c["T"]
+    L, S, H, d, Lb, T = c["layers"], c["S"], c["H"], c["d"], c["Lb"], c["T"]
     g = torch.Generator(device="cpu").manual_seed(c["seed"])
     W = [torch.randn(3, H * d, H * d, generator=g) / math.sqrt(H * d) for _ in range(L)]
     x = torch.randn(T, S, H, d, generator=g).to(torch.bfloat16).cuda()
     res = {"workload": "%d-layer streaming stack, %d streams of %d frames, H=%d, d=%d, Lb=%d, "
-                       "La=%d, bf16, random projections; %g ms per frame"
-                       % (L, S, T, H, d, Lb, La, c["frame_ms"])}
-    for kind in ("sa", "llsa"):
-        model = StackedStream(kind, W, S, H, d, Lb, La, lengths=[T] * S)
-        t = EventTimer()
-        lag = []
-        for n in range(T + L * La):
-            e = t.start()
-            _, em = model.step(x[n] if n < T else None)
-            t.stop(e)
-            f = int(em[0])
-            if f >= 0:
-                lag.append(n - f)
-        torch.cuda.synchronize()
-        ms = sorted(t.all_ms())
-        frames = max(lag)
-        res[kind] = {
-            "algorithmic_latency_frames": frames,
-            "algorithmic_latency_s": frames * c["frame_ms"] * 1e-3,
-            "latency_constant_over_frames": min(lag) == frames and len(lag) == T,
-            "stack_step_ms_p50": ms[len(ms) // 2],
-            "stack_step_ms_p99": ms[min(len(ms) - 1, int(0.99 * len(ms)))],
-        }
+                       "La=%s, bf16, random projections; %g ms per frame"
+                       % (L, S, T, H, d, Lb, "/".join(str(a) for a in c["La"]), c["frame_ms"])}
+    for La in c["La"]:
+        for kind in ("sa", "llsa"):
+            model = StackedStream(kind, W, S, H, d, Lb, La, lengths=[T] * S)
+            t = EventTimer()
+            lag = []
+            for n in range(T + L * La):
+                e = t.start()
+                _, em = model.step(x[n] if n < T else None)
+                t.stop(e)
+                f = int(em[0])
+                if f >= 0:
+                    lag.append(n - f)
+            torch.cuda.synchronize()
+            ms = sorted(t.all_ms())
+            frames = max(lag)
+            res["%s_La%d" % (kind, La)] = {
+                "algorithmic_latency_frames": frames,
+                "algorithmic_latency_s": frames * c["frame_ms"] * 1e-3,
+                "latency_constant_over_frames": min(lag) == frames and len(lag) == T,
+                "stack_step_ms_p50": ms[len(ms) // 2],
+                "stack_step_ms_p99": ms[min(len(ms) - 1, int(0.99 * len(ms)))],
+            }
     return res
 
 
