@@ -1,0 +1,76 @@
+"""Every batch entry point at the smallest shapes: one-frame and two-frame
+sequences, empty sequences, windows far longer than the sequence, against the
+fp64 oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2302_13451_amd import binding as bd
+from paper_2302_13451_amd.inputs import llsa_inputs, sa_inputs
+from parity import assert_close, assert_lse_close, f64, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+CASES = [(1, 1, [1]), (2, 2, [2, 1]), (3, 3, [0, 3, 1]), (1, 5, [5])]
+
+
+@pytest.mark.parametrize("B,T,lengths", CASES)
+@pytest.mark.parametrize("Lb,La", [(0, 0), (3, 0), (0, 2), (7, 9)])
+def test_sa_tiny(oracle_mod, B, T, lengths, Lb, La):
+    print("tiny sa B=%d T=%d Lb=%d La=%d" % (B, T, Lb, La), flush=True)
+    H, d = 2, 64
+    x = sa_inputs(B, T, H, d, 71, dtype="bf16", lengths=lengths)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].cuda()
+    out, lse = bd.sa_forward(q, k, v, Lb, La, ln)
+    dq, dk, dv = bd.sa_backward(q, k, v, out, lse, do, Lb, La, ln)
+    torch.cuda.synchronize()
+    xn = {n: f64(x[n]) for n in ("q", "k", "v", "dout")}
+    y, l = oracle_mod.sa_forward(xn["q"], xn["k"], xn["v"], Lb, La, lengths)
+    g = oracle_mod.sa_backward(xn["q"], xn["k"], xn["v"], f64(do.cpu()), Lb, La, lengths)
+    assert_close(f64(out), y, "bf16", "out")
+    assert_lse_close(lse.cpu().numpy(), l, "bf16")
+    for got, ref, n in zip((dq, dk, dv), g, ("dq", "dk", "dv")):
+        assert_close(f64(got), ref, "bf16", n, elementwise=False, zero_atol=1e-6)
+
+
+@pytest.mark.parametrize("B,T,lengths", CASES)
+@pytest.mark.parametrize("Lb,La", [(0, 1), (3, 0), (7, 9)])
+def test_llsa_tiny(oracle_mod, B, T, lengths, Lb, La):
+    print("tiny llsa B=%d T=%d Lb=%d La=%d" % (B, T, Lb, La), flush=True)
+    H, d = 2, 64
+    x = llsa_inputs(B, T, H, d, 72, dtype="bf16", lengths=lengths, with_dout=True)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].cuda()
+    out, lse = bd.llsa_forward(q, k, v, Lb, La, ln)
+    dq, dk, dv = bd.llsa_backward(q, k, v, out, lse, do, Lb, La, ln)
+    torch.cuda.synchronize()
+    xn = {n: f64(x[n]) for n in ("q", "k", "v", "dout")}
+    y, l = oracle_mod.llsa_two_branch(xn["q"], xn["k"], xn["v"], Lb, La, lengths)
+    g = oracle_mod.llsa_two_branch_backward(xn["q"], xn["k"], xn["v"], xn["dout"], Lb, La, lengths)
+    assert_close(f64(out), y, "bf16", "out")
+    assert_lse_close(lse.cpu().numpy(), l, "bf16")
+    for got, ref, n in zip((dq, dk, dv), g, ("dq", "dk", "dv")):
+        assert_close(f64(got), ref, "bf16", n, elementwise=False, zero_atol=1e-6)
+
+
+@pytest.mark.parametrize("B,T,lengths", CASES)
+@pytest.mark.parametrize("Lb,La", [(0, 1), (3, 2), (7, 9)])
+def test_llsa_paper_tiny(oracle_mod, B, T, lengths, Lb, La):
+    print("tiny llsa paper B=%d T=%d Lb=%d La=%d" % (B, T, Lb, La), flush=True)
+    H, d = 2, 64
+    x = llsa_inputs(B, T, H, d, 73, dtype="bf16", lengths=lengths, with_dout=True,
+                    channels=La + 1)
+    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].cuda()
+    out, lse = bd.llsa_paper_forward(q, k, v, Lb, La, ln)
+    dq, dk, dv = bd.llsa_paper_backward(q, k, v, out, lse, do, Lb, La, ln)
+    torch.cuda.synchronize()
+    xn = {n: f64(x[n]) for n in ("q", "k", "v", "dout")}
+    y, l = oracle_mod.llsa_paper(xn["q"], xn["k"], xn["v"], Lb, La, lengths)
+    g = oracle_mod.llsa_paper_backward(xn["q"], xn["k"], xn["v"], xn["dout"], Lb, La, lengths)
+    assert_close(f64(out), y, "bf16", "out")
+    assert_lse_close(lse.cpu().numpy(), l, "bf16")
+    for got, ref, n in zip((dq, dk, dv), g, ("dq", "dk", "dv")):
+        assert_close(f64(got), ref, "bf16", n, elementwise=False, zero_atol=1e-6)
