@@ -24,6 +24,14 @@ namespace sa {
 namespace {
 
 constexpr int kMaxWaves = 16;
+// waves of the LLSA step (its per-lane state allows three per SIMD)
+constexpr int kLlsaWaves = 12;
+// LDS floats per wave of the LLSA step: one query row, two score slots per
+// window frame, rounded up so every wave's query starts 16-byte aligned
+template <int D>
+__host__ __device__ constexpr int llsa_wave_floats(int wmax) {
+  return D + (2 * wmax + 3) / 4 * 4;
+}
 
 template <typename E>
 __device__ __forceinline__ void unpack16(const uint4& x, float* f);
@@ -144,6 +152,112 @@ __device__ __forceinline__ void attend_wave(const E* qrow, KRow krow, VRow vrow,
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Two query rows (one head) over the same W frames in one pass: each key and
+// value row is read once for both. on0 / on1 select the queries that are due.
+// Query 0 is held in registers, query 1 in the wave's LDS slots qs (D floats,
+// 16-byte aligned, read as broadcasts); wts holds 2W score slots (the first W
+// for query 0).
+template <typename E, int D, typename KRow, typename VRow>
+__device__ __forceinline__ void attend_wave2(const E* q0, const E* q1, bool on0, bool on1, KRow krow, VRow vrow,
+                                             int lo, int W, float scale_log2, float* qs, float* wts, E* o0, E* o1,
+                                             int lane) {
+  constexpr int EPC = 16 / sizeof(E);
+  constexpr int CH = D / EPC;
+  constexpr int NKG = 64 / CH;
+  auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
+  float qa[D];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    if (on0) unpack16<E>(chunk(q0, c), qa + c * EPC);
+    else
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) qa[c * EPC + e] = 0.f;
+  }
+  if (lane < CH) {  // query 1 into LDS, one 16-byte chunk per lane
+    float f[EPC];
+    if (on1) unpack16<E>(chunk(q1, lane), f);
+    else
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) f[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPC; e += 4)
+      *reinterpret_cast<f32x4*>(qs + lane * EPC + e) = f32x4{f[e], f[e + 1], f[e + 2], f[e + 3]};
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // scores: one key per lane, both queries
+  float m0 = kNegInf, m1 = kNegInf;
+  for (int j = lane; j < W; j += 64) {
+    const E* kr = krow(lo + j);
+    float z0 = 0.f, z1 = 0.f;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      float kf[EPC];
+      unpack16<E>(chunk(kr, c), kf);
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4) {
+        const f32x4 qb = *reinterpret_cast<const f32x4*>(qs + c * EPC + e);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          z0 += qa[c * EPC + e + i] * kf[e + i];
+          z1 += qb[i] * kf[e + i];
+        }
+      }
+    }
+    z0 *= scale_log2;
+    z1 *= scale_log2;
+    wts[j] = z0;
+    wts[W + j] = z1;
+    m0 = fmaxf(m0, z0);
+    m1 = fmaxf(m1, z1);
+  }
+  m0 = wave_max(m0);
+  m1 = wave_max(m1);
+  float l0 = 0.f, l1 = 0.f;
+  for (int j = lane; j < W; j += 64) {
+    const float p0 = fast_exp2(wts[j] - m0), p1 = fast_exp2(wts[W + j] - m1);
+    wts[j] = p0;
+    wts[W + j] = p1;
+    l0 += p0;
+    l1 += p1;
+  }
+  const float inv0 = 1.f / wave_sum(l0), inv1 = 1.f / wave_sum(l1);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // weighted sums: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
+  const int dc = lane % CH, kg = lane / CH;
+  float a0[EPC], a1[EPC];
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) a0[e] = a1[e] = 0.f;
+  for (int j = kg; j < W; j += NKG) {
+    float vf[EPC];
+    unpack16<E>(chunk(vrow(lo + j), dc), vf);
+    const float p0 = wts[j], p1 = wts[W + j];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      a0[e] += p0 * vf[e];
+      a1[e] += p1 * vf[e];
+    }
+  }
+#pragma unroll
+  for (int o = CH; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      a0[e] += __shfl_xor(a0[e], o);
+      a1[e] += __shfl_xor(a1[e], o);
+    }
+  if (kg == 0) {
+    *reinterpret_cast<uint4*>(o0 + dc * EPC) = on0 ? pack16<E>(a0, inv0) : make_uint4(0, 0, 0, 0);
+    *reinterpret_cast<uint4*>(o1 + dc * EPC) = on1 ? pack16<E>(a1, inv1) : make_uint4(0, 0, 0, 0);
+  }
+  // the next head reuses wts: finish these reads first
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <typename E, int D>
 __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a) {
   constexpr int EPC = 16 / sizeof(E);   // elements per 16-byte chunk
@@ -210,8 +324,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a
 // Both windows are the frames u - La - Lb .. u (clipped to the sequence), frame
 // tau taken from branch L when tau <= t and from branch C otherwise (Eq. 14/15
 // with channels 0 .. La-1 held by C and channel La by L), so the two outputs
-// differ only in their query. Layout and work split as in stream_step_kernel,
-// the two outputs one after the other per head.
+// differ only in their query. Layout and work split as in stream_step_kernel;
+// per head one pass over the window computes both outputs (attend_wave2).
 struct DevLlsaStream {
   const void *qc, *kc, *vc, *ql, *kl, *vl;
   void *out_c, *out_l;
@@ -226,7 +340,7 @@ struct DevLlsaStream {
 };
 
 template <typename E, int D>
-__global__ __launch_bounds__(64 * kMaxWaves) void llsa_stream_step_kernel(DevLlsaStream a) {
+__global__ __launch_bounds__(64 * kLlsaWaves) void llsa_stream_step_kernel(DevLlsaStream a) {
   constexpr int EPC = 16 / sizeof(E);
   constexpr int CH = D / EPC;
   static_assert(CH * EPC == D && 4 * CH <= 64, "row must split into 16-byte chunks");
@@ -234,7 +348,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void llsa_stream_step_kernel(DevLls
   const int s = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
-  float* wts = wts_all + w * a.wmax;
+  float* qs = wts_all + w * llsa_wave_floats<D>(a.wmax);  // query 1, then the score slots
+  float* wts = qs + D;
   const int H = a.H, La = a.La, R = a.R;
   const size_t HD = static_cast<size_t>(H) * D;
 
@@ -281,14 +396,15 @@ __global__ __launch_bounds__(64 * kMaxWaves) void llsa_stream_step_kernel(DevLls
       return (tau <= split ? (tau == t ? vl : vlr + static_cast<size_t>(tau % R) * HD)
                            : (tau == u ? vc : vcr + static_cast<size_t>(tau % R) * HD)) + ho;
     };
-    for (int o = 0; o < 2; ++o) {
-      E* orow = (o == 0 ? out_c : out_l) + ho;
-      if (!(o == 0 ? got_c : got_l)) {
-        if (lane < CH) *reinterpret_cast<uint4*>(orow + lane * EPC) = make_uint4(0, 0, 0, 0);
-        continue;
+    if (!got_c && !got_l) {
+      if (lane < CH) {
+        *reinterpret_cast<uint4*>(out_c + ho + lane * EPC) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(out_l + ho + lane * EPC) = make_uint4(0, 0, 0, 0);
       }
-      attend_wave<E, D>((o == 0 ? qc : ql) + ho, krow, vrow, lo, hi - lo + 1, a.scale_log2, wts, orow, lane);
+      continue;
     }
+    attend_wave2<E, D>(qc + ho, ql + ho, got_c, got_l, krow, vrow, lo, hi - lo + 1, a.scale_log2, qs, wts,
+                       out_c + ho, out_l + ho, lane);
   }
   if (threadIdx.x == 0) {
     if (a.emitted_c) a.emitted_c[s] = got_c ? u : -1;
@@ -325,9 +441,13 @@ hipError_t launch_llsa_stream_step(const LlsaStreamStepArgs& a, ElemType et, hip
   d.lengths = a.lengths;
   d.wmax = a.Lb + a.La + 1;
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
-  const int nw = a.H < kMaxWaves ? a.H : kMaxWaves;
+  // per wave a query row and two score slots per window frame, within 64 KB
+  const int per_wave = a.d == 64 ? llsa_wave_floats<64>(d.wmax) : llsa_wave_floats<32>(d.wmax);
+  int nw = a.H < kLlsaWaves ? a.H : kLlsaWaves;
+  const int fit = static_cast<int>((64 * 1024) / (sizeof(float) * static_cast<size_t>(per_wave)));
+  nw = nw < fit ? nw : fit;
   const dim3 grid(a.S), block(64 * nw);
-  const size_t lds = static_cast<size_t>(nw) * d.wmax * sizeof(float);
+  const size_t lds = static_cast<size_t>(nw) * per_wave * sizeof(float);
   if (et == kBF16) {
     if (a.d == 64)
       hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 64>), grid, block, lds, stream, d);
