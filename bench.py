@@ -665,6 +665,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the SA forward+backward step")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip the streaming-stack latency row (its many small launches crowd "
+                         "kernel traces)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 512 MiB (counter calibration)")
     ap.add_argument("--memory-experiment", action="store_true",
@@ -744,8 +747,9 @@ def main():
         line["stream"] = bench_stream()
         log("LLSA streaming step")
         line["llsa_stream"] = bench_llsa_stream()
-        log("12-layer streaming stack latency")
-        line["stream_latency"] = bench_stream_latency()
+        if not args.no_stack:
+            log("12-layer streaming stack latency")
+            line["stream_latency"] = bench_stream_latency()
         log("masked full attention in PyTorch")
         try:
             line["masked_attention_torch"] = bench_masked_attention()
