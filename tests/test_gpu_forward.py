@@ -1,7 +1,6 @@
 """GPU parity of sa_forward against the fp64 oracle on identical (rounded)
 inputs, plus the exact band-bookkeeping probes. Runs through the C ABI."""
 
-import math
 
 import numpy as np
 import pytest

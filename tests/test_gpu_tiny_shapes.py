@@ -2,7 +2,6 @@
 sequences, empty sequences, windows far longer than the sequence, against the
 fp64 oracle."""
 
-import numpy as np
 import pytest
 import torch
 
