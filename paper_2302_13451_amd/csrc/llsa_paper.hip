@@ -22,6 +22,7 @@ struct PaperMergeDev {
   int B, T, H, La;
   const int32_t* lengths;
   float scale;
+  int Lb;  // used by the fused forward only
 };
 
 template <typename E>
@@ -411,6 +412,162 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_merge_mfma_kernel(
   }
 }
 
+// The whole forward in one pass (bfloat16, La <= 15, Lb < 16 kMaxBandBlocks):
+// within an anti-diagonal group (b, s, h) every query (c, s - c) reads the same
+// band, frames s - A - Lb .. s - A of channel A, besides the diagonal keys
+// (c', s - c'), c' < A. So a group is one dense block of A + 1 queries against
+// Lb + 1 band keys (in 16-key blocks) and A diagonal keys, with one softmax.
+// A workgroup takes 64 consecutive anti-diagonals of one (sequence, head) and
+// stages the union of their bands (64 + Lb rows of channel A's keys and
+// values) in LDS once; its waves take every fourth anti-diagonal. Layouts as
+// in the merge kernel: scores S^T per 16-key block (lane (i, g) holds query i
+// against keys 4g .. 4g + 3); key rows are read as A-operand rows (stride
+// D + 8: 16-byte aligned), value rows transposed (stride D + 4). Writes every
+// row (c, t), t < T, of out and lse (zeros / -inf past the sequence's end).
+constexpr int kMaxBandBlocks = 5;
+constexpr int kFusedRows = 64 + 16 * kMaxBandBlocks;  // staged band rows (64 + Lb <= this)
+
+template <int D>
+__global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_fwd_fused_kernel(PaperMergeDev a) {
+  constexpr int NS = D / 32, NF = D / 16, NKB = kMaxBandBlocks, KS = D + 8, VS = D + 4;
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[kFusedRows * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[kFusedRows * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t s_tile[kDiagWaves][16 * VS];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int col = lane & 15, g = lane >> 4;
+  uint16_t* sv = s_tile[w];
+  const int A = a.La, Lb = a.Lb, T = a.T, H = a.H, S = T + A;
+  const int nchunk = (S + 63) / 64;
+  const int nkb = (Lb + 16) / 16;  // 16-key blocks of the band
+  const long long items = static_cast<long long>(a.B) * H * nchunk;
+  const size_t cs = static_cast<size_t>(a.B) * T * H * D;
+  const size_t ls = static_cast<size_t>(a.B) * H * T;
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+  const uint16_t* k = static_cast<const uint16_t*>(a.k);
+  const uint16_t* v = static_cast<const uint16_t*>(a.v);
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  const float scale = a.scale;
+  constexpr int CPR = D / 8;  // 16-byte pieces per row
+  for (long long it = blockIdx.x; it < items; it += gridDim.x) {
+    const int h = static_cast<int>(it % H);
+    const int chunk = static_cast<int>((it / H) % nchunk);
+    const int b = static_cast<int>(it / (static_cast<long long>(H) * nchunk));
+    int len = T;
+    if (a.lengths) {
+      len = a.lengths[b];
+      len = len < 0 ? 0 : (len > T ? T : len);
+    }
+    const int s0 = chunk * 64;
+    const int fb0 = s0 - A - Lb;  // frame of staged row 0
+    const size_t achan = static_cast<size_t>(A) * cs;
+    __syncthreads();  // every wave is done with the previous item's band
+    // every row a block may read is staged (finite values: a masked key's
+    // value still enters the product with weight 0)
+    for (int e = tid; e < kFusedRows * CPR; e += 64 * kDiagWaves) {
+      const int r = e / CPR, c8 = 8 * (e % CPR), fr = fb0 + r;
+      const bool ok = fr >= 0 && fr < len;
+      const size_t off = achan + row_index(b, fr, h, T, H, D) + c8;
+      const u32x4 kk = ok ? ld16(k + off) : kZero16, vv = ok ? ld16(v + off) : kZero16;
+      st16(s_k + r * KS + c8, kk);
+      st8(s_v + r * VS + c8, u32x2{vv[0], vv[1]});
+      st8(s_v + r * VS + c8 + 4, u32x2{vv[2], vv[3]});
+    }
+    __syncthreads();
+    const int s1 = min(s0 + 64, S);
+    for (int sd = s0 + w; sd < s1; sd += kDiagWaves) {
+      const int tc = sd - col;  // frame of query col and of diagonal key col
+      const bool qrow = col <= A && tc >= 0 && tc < T;  // a row this group writes
+      const bool qv = qrow && tc < len;
+      const bool kv = col < A && tc >= 0 && tc < len;
+      const size_t crow = col * cs + row_index(b, tc, h, T, H, D);
+      bf16x8 qa[NS];
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) qa[s2] = ld_row8<D>(q + crow + 32 * s2 + 8 * g, qv);
+      const int tb0 = sd - A - Lb;  // frame of band key 0
+      const int rb0 = sd - s0;      // its staged row
+      // scores: band blocks 0 .. NKB-1, then the diagonal block NKB
+      float sc[NKB + 1][4];
+      float m = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        if (kb < nkb) {
+          const uint16_t* kr = s_k + (rb0 + 16 * kb + col) * KS + 8 * g;
+          f32x4 st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s2 = 0; s2 < NS; ++s2)
+            st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ld16(kr + 32 * s2)), qa[s2], st,
+                                                         0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int j = 16 * kb + 4 * g + e, te = tb0 + j;
+            const bool ok = qv && j <= Lb && te >= 0 && te < len;
+            sc[kb][e] = ok ? st[e] * scale : kNegInf;
+            m = fmaxf(m, sc[kb][e]);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sc[kb][e] = kNegInf;
+        }
+      }
+      bf16x8 dv[NS];
+      {
+        f32x4 st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s2 = 0; s2 < NS; ++s2) {
+          dv[s2] = ld_row8<D>(v + crow + 32 * s2 + 8 * g, kv);
+          st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ld_row8<D>(k + crow + 32 * s2 + 8 * g, kv), qa[s2], st, 0, 0,
+                                                       0);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = 4 * g + e, tj = sd - j;
+          const bool ok = qv && j < A && tj >= 0 && tj < len;
+          sc[NKB][e] = ok ? st[e] * scale : kNegInf;
+          m = fmaxf(m, sc[NKB][e]);
+        }
+      }
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      float ps = 0.f;
+#pragma unroll
+      for (int kb = 0; kb <= NKB; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sc[kb][e] = sc[kb][e] == kNegInf ? 0.f : __expf(sc[kb][e] - m);
+          ps += sc[kb][e];
+        }
+      ps += __shfl_xor(ps, 16, 64);
+      ps += __shfl_xor(ps, 32, 64);
+      // values: O^T += V^T P^T per block (band rows from the staged band, the
+      // diagonal rows through the wave's tile)
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) stage8<D>(sv, col, 32 * s2 + 8 * g, dv[s2]);
+      wave_sync();
+      f32x4 acc[NF];
+#pragma unroll
+      for (int fb = 0; fb < NF; ++fb) acc[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb <= NKB; ++kb) {
+        if (kb < NKB && kb >= nkb) continue;
+        const uint16_t* tile = kb < NKB ? s_v + (rb0 + 16 * kb) * VS : sv;
+        const bf16x8 pb = as_b4(sc[kb]);
+#pragma unroll
+        for (int fb = 0; fb < NF; ++fb)
+          acc[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(tile, 16 * fb, col, g), pb, acc[fb], 0, 0, 0);
+      }
+      wave_sync();  // the tile is rewritten by the next group
+      if (qrow) {  // lane (i, g) holds features 16 fb + 4g .. + 3 of query i
+        const float inv = qv ? 1.f / ps : 0.f;
+#pragma unroll
+        for (int fb = 0; fb < NF; ++fb)
+          st8(out + crow + 16 * fb + 4 * g,
+              u32x2{pack_bf16x2(acc[fb][0] * inv, acc[fb][1] * inv), pack_bf16x2(acc[fb][2] * inv, acc[fb][3] * inv)});
+        if (g == 0) a.lse[col * ls + (static_cast<size_t>(b) * H + h) * T + tc] = qv ? m + __logf(ps) : kNegInf;
+      }
+    }
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kernel(PaperDiagDev a) {
   constexpr int NS = D / 32, NF = D / 16, TS = 16 * (D + 4);
@@ -560,6 +717,17 @@ hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hi
 
 hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStream_t stream) {
   const int A = x.La;
+  if (et == kBF16 && A >= 1 && A <= kMaxMfmaLa && x.Lb < 16 * kMaxBandBlocks) {  // one pass
+    PaperMergeDev m{x.q, x.k, x.v, x.out, x.lse, x.B, x.T, x.H, A, x.lengths,
+                    1.f / sqrtf(static_cast<float>(x.d)), x.Lb};
+    const long long items = static_cast<long long>(x.B) * x.H * ((x.T + A + 63) / 64);
+    const int grid = static_cast<int>(items < 65536 ? items : 65536);
+    if (x.d == 64)
+      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<64>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    else
+      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<32>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+    return hipGetLastError();
+  }
   const size_t cstride = static_cast<size_t>(x.B) * x.T * x.H * x.d * (et == kBF16 ? 2 : 4);
   const size_t lstride = static_cast<size_t>(x.B) * x.H * x.T;
   auto at = [&](const void* p, int c) { return static_cast<const char*>(p) + c * cstride; };
@@ -581,7 +749,8 @@ hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStr
     if (e != hipSuccess) return e;
   }
   if (A == 0) return hipSuccess;  // one channel: the band is the whole window
-  PaperMergeDev m{x.q, x.k, x.v, x.out, x.lse, x.B, x.T, x.H, A, x.lengths, 1.f / sqrtf(static_cast<float>(x.d))};
+  PaperMergeDev m{x.q, x.k, x.v, x.out, x.lse, x.B, x.T, x.H, A, x.lengths, 1.f / sqrtf(static_cast<float>(x.d)),
+                  x.Lb};
   if (et == kBF16 && A <= kMaxMfmaLa) {  // one wave per anti-diagonal group
     const long long groups = static_cast<long long>(x.B) * (x.T + A) * x.H;
     const long long blocks = (groups + kDiagWaves - 1) / kDiagWaves;
