@@ -419,20 +419,21 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_merge_mfma_kernel(
 // Lb + 1 band keys (in 16-key blocks) and A diagonal keys, with one softmax.
 // A workgroup takes 64 consecutive anti-diagonals of one (sequence, head) and
 // stages the union of their bands (64 + Lb rows of channel A's keys and
-// values) in LDS once; its waves take every fourth anti-diagonal. Layouts as
+// values) in LDS once; its eight waves take every eighth anti-diagonal. Layouts as
 // in the merge kernel: scores S^T per 16-key block (lane (i, g) holds query i
 // against keys 4g .. 4g + 3); key rows are read as A-operand rows (stride
 // D + 8: 16-byte aligned), value rows transposed (stride D + 4). Writes every
 // row (c, t), t < T, of out and lse (zeros / -inf past the sequence's end).
 constexpr int kMaxBandBlocks = 5;
 constexpr int kFusedRows = 64 + 16 * kMaxBandBlocks;  // staged band rows (64 + Lb <= this)
+constexpr int kFusedWaves = 8;  // waves per workgroup of the one-pass forward
 
 template <int D>
-__global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_fwd_fused_kernel(PaperMergeDev a) {
+__global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(PaperMergeDev a) {
   constexpr int NS = D / 32, NF = D / 16, NKB = kMaxBandBlocks, KS = D + 8, VS = D + 4;
   __shared__ __attribute__((aligned(16))) uint16_t s_k[kFusedRows * KS];
   __shared__ __attribute__((aligned(16))) uint16_t s_v[kFusedRows * VS];
-  __shared__ __attribute__((aligned(16))) uint16_t s_tile[kDiagWaves][16 * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t s_tile[kFusedWaves][16 * VS];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int col = lane & 15, g = lane >> 4;
   uint16_t* sv = s_tile[w];
@@ -463,7 +464,7 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_fwd_fused_kernel(P
     __syncthreads();  // every wave is done with the previous item's band
     // every row a block may read is staged (finite values: a masked key's
     // value still enters the product with weight 0)
-    for (int e = tid; e < kFusedRows * CPR; e += 64 * kDiagWaves) {
+    for (int e = tid; e < kFusedRows * CPR; e += 64 * kFusedWaves) {
       const int r = e / CPR, c8 = 8 * (e % CPR), fr = fb0 + r;
       const bool ok = fr >= 0 && fr < len;
       const size_t off = achan + row_index(b, fr, h, T, H, D) + c8;
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_fwd_fused_kernel(P
     }
     __syncthreads();
     const int s1 = min(s0 + 64, S);
-    for (int sd = s0 + w; sd < s1; sd += kDiagWaves) {
+    for (int sd = s0 + w; sd < s1; sd += kFusedWaves) {
       const int tc = sd - col;  // frame of query col and of diagonal key col
       const bool qrow = col <= A && tc >= 0 && tc < T;  // a row this group writes
       const bool qv = qrow && tc < len;
@@ -723,9 +724,9 @@ hipError_t launch_llsa_paper_forward(const LlsaPaperArgs& x, ElemType et, hipStr
     const long long items = static_cast<long long>(x.B) * x.H * ((x.T + A + 63) / 64);
     const int grid = static_cast<int>(items < 65536 ? items : 65536);
     if (x.d == 64)
-      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<64>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<64>, dim3(grid), dim3(64 * kFusedWaves), 0, stream, m);
     else
-      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<32>, dim3(grid), dim3(64 * kDiagWaves), 0, stream, m);
+      hipLaunchKernelGGL(llsa_paper_fwd_fused_kernel<32>, dim3(grid), dim3(64 * kFusedWaves), 0, stream, m);
     return hipGetLastError();
   }
   const size_t cstride = static_cast<size_t>(x.B) * x.T * x.H * x.d * (et == kBF16 ? 2 : 4);
