@@ -63,10 +63,11 @@ def _load():
     lib = ctypes.CDLL(_LIB_PATH)
     i = ctypes.c_int
     lib.oracle_sa_forward.argtypes = [_DP, _DP, _DP, _DP, _DP, i, i, i, i, i, i, _IP, i]
-    lib.oracle_sa_backward.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, i, i, i, i, i, i, _IP, i]
+    lib.oracle_sa_backward.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, _DP, i, i, i, i, i, i, _IP,
+                                       i]
     lib.oracle_llsa_forward.argtypes = [_DP, _DP, _DP, i, _IP, i, _IP, _IP, i, _DP, _DP,
                                         i, i, i, i, i, i, _IP, i]
-    lib.oracle_llsa_backward.argtypes = [_DP, _DP, _DP, _DP, i, _IP, i, _IP, _IP, i, _DP, _DP,
+    lib.oracle_llsa_backward.argtypes = [_DP, _DP, _DP, _DP, _DP, i, _IP, i, _IP, _IP, i, _DP, _DP,
                                          _DP, i, i, i, i, i, i, _IP, i]
     lib.oracle_sa_stream_step.argtypes = [_DP, _DP, _DP, _DP, _DP, _DP, _DP, i, _IP, _IP,
                                           i, i, i, i, i, _IP]
@@ -124,16 +125,27 @@ def sa_forward(q, k, v, Lb: int, La: int, lengths=None, threads: int = 0):
     return y, lse
 
 
-def sa_backward(q, k, v, dy, Lb: int, La: int, lengths=None, threads: int = 0):
-    """SA backward (Eq. 7-13). Returns ``(dq, dk, dv)``, each ``[B][T][H][d]``."""
+def sa_backward(q, k, v, dy, Lb: int, La: int, lengths=None, threads: int = 0, y=None):
+    """SA backward (Eq. 7-13). Returns ``(dq, dk, dv)``, each ``[B][T][H][d]``.
+
+    ``y`` (optional, ``[B][T][H][d]``): a supplied forward output. Without it
+    the gradient is exact (explicit softmax Jacobian); with it the term
+    ``sum_i a_i g_i = dy_n . y_n`` of the Jacobian product takes ``y_n`` from
+    the supplied output, which is what a backward given a stored (rounded)
+    output computes."""
     q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
     B, T, H, d = q.shape
     for x in (k, v, dy):
         if x.shape != q.shape:
             raise ValueError("q, k, v, dy must share one shape")
+    if y is not None:
+        y = _f64(y)
+        if y.shape != q.shape:
+            raise ValueError("y must have the shape of q")
     ln = _lengths(lengths, B)
     dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
-    rc = _load().oracle_sa_backward(_dp(q), _dp(k), _dp(v), _dp(dy), _dp(dq), _dp(dk), _dp(dv),
+    rc = _load().oracle_sa_backward(_dp(q), _dp(k), _dp(v), _dp(dy), _dp(y), _dp(dq), _dp(dk),
+                                    _dp(dv),
                                     B, T, H, d, int(Lb), int(La), _ip(ln),
                                     threads or default_threads())
     _check(rc, "oracle_sa_backward")
@@ -175,11 +187,12 @@ def llsa_forward(q, k, v, alias, out_channels, q_branches, Lb: int, La: int, len
 
 
 def llsa_backward(q, k, v, dy, alias, out_channels, q_branches, Lb: int, La: int, lengths=None,
-                  convention: str = "text", threads: int = 0):
+                  convention: str = "text", threads: int = 0, y=None):
     """Gradient of the LLSA forward (same arguments as :func:`llsa_forward`)
     for the output gradient ``dy [nout][B][T][H][d]``: the exact adjoint of
     the forward's gather. Returns ``(dq, dk, dv)``, each
-    ``[nbranch][B][T][H][d]``."""
+    ``[nbranch][B][T][H][d]``. ``y`` (optional, ``[nout][B][T][H][d]``): a
+    supplied forward output, used as in :func:`sa_backward`."""
     q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
     nb, B, T, H, d = q.shape
     if k.shape != q.shape or v.shape != q.shape:
@@ -194,10 +207,14 @@ def llsa_backward(q, k, v, dy, alias, out_channels, q_branches, Lb: int, La: int
     nout = outc.shape[0]
     if dy.shape != (nout, B, T, H, d):
         raise ValueError("dy must have shape %s" % ((nout, B, T, H, d),))
+    if y is not None:
+        y = _f64(y)
+        if y.shape != dy.shape:
+            raise ValueError("y must have the shape of dy")
     conv = {"text": 0, "eq14": 1}[convention]
     ln = _lengths(lengths, B)
     dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
-    rc = _load().oracle_llsa_backward(_dp(q), _dp(k), _dp(v), _dp(dy), nb, _ip(alias), nout,
+    rc = _load().oracle_llsa_backward(_dp(q), _dp(k), _dp(v), _dp(dy), _dp(y), nb, _ip(alias), nout,
                                       _ip(outc), _ip(qb), conv, _dp(dq), _dp(dk), _dp(dv), B, T,
                                       H, d, int(Lb), int(La), _ip(ln),
                                       threads or default_threads())
@@ -223,13 +240,14 @@ def llsa_two_branch(q, k, v, Lb: int, La: int, lengths=None, threads: int = 0):
                         "text", threads)
 
 
-def llsa_two_branch_backward(q, k, v, dy, Lb: int, La: int, lengths=None, threads: int = 0):
+def llsa_two_branch_backward(q, k, v, dy, Lb: int, La: int, lengths=None, threads: int = 0,
+                             y=None):
     """Gradient of :func:`llsa_two_branch` for ``dy [2][B][T][H][d]``;
     returns ``(dq, dk, dv)``, each ``[2][B][T][H][d]`` (index 0 = causal
     branch, 1 = look-ahead branch)."""
     alias = [CAUSAL] * La + [LOOKAHEAD]
     return llsa_backward(q, k, v, dy, alias, [0, La], [CAUSAL, LOOKAHEAD], Lb, La, lengths,
-                         "text", threads)
+                         "text", threads, y)
 
 
 def llsa_paper(q, k, v, Lb: int, La: int, lengths=None, convention: str = "text",
@@ -241,11 +259,12 @@ def llsa_paper(q, k, v, Lb: int, La: int, lengths=None, convention: str = "text"
 
 
 def llsa_paper_backward(q, k, v, dy, Lb: int, La: int, lengths=None, convention: str = "text",
-                        threads: int = 0):
+                        threads: int = 0, y=None):
     """Gradient of :func:`llsa_paper` for ``dy [La+1][B][T][H][d]``; returns
     ``(dq, dk, dv)``, each ``[La+1][B][T][H][d]``."""
     chans = list(range(La + 1))
-    return llsa_backward(q, k, v, dy, chans, chans, chans, Lb, La, lengths, convention, threads)
+    return llsa_backward(q, k, v, dy, chans, chans, chans, Lb, La, lengths, convention, threads,
+                         y)
 
 
 class StreamOracle:

@@ -151,8 +151,16 @@ int oracle_sa_forward(const double* q, const double* k, const double* v, double*
 /* SA backward (Eq. 7-13)                                                    */
 /* ------------------------------------------------------------------------ */
 
+/*
+ * ysup (nullable, [B][T][H][d]): an output supplied by the caller. NULL gives
+ * the exact gradient (explicit Jacobian, Eq. 9). Otherwise the a a^T part of
+ * the Jacobian, contracted with the incoming gradient, is dl/dy_n . y_n by
+ * Eq. 6, and y_n is taken from ysup: the gradient a backward computes from a
+ * stored (e.g. rounded) forward output.
+ */
+
 int oracle_sa_backward(const double* q, const double* k, const double* v, const double* dy,
-                       double* dq, double* dk, double* dv,
+                       const double* ysup, double* dq, double* dk, double* dv,
                        int B, int T, int H, int d, int Lb, int La, const int32_t* lengths, int threads) {
   if (B < 0 || T < 0 || H < 0 || d <= 0 || Lb < 0 || La < 0) return ORC_ERR_INVALID;
   if (B == 0 || T == 0 || H == 0) return ORC_OK;
@@ -201,15 +209,25 @@ int oracle_sa_backward(const double* q, const double* k, const double* v, const 
           for (int i = 0; i < d; ++i) acc += dyn[i] * vr[j][i];
           g[j] = acc;
         }
-        /* softmax Jacobian J_ij = da_i/dz_j = a_i (delta_ij - a_j) */
-        for (int i = 0; i < W; ++i)
-          for (int j = 0; j < W; ++j) J[(size_t)i * W + j] = an[i] * ((i == j ? 1.0 : 0.0) - an[j]);
-        /* e = g J (Eq. 9 combined with the incoming gradient) */
         double* en = E + (size_t)n * Wmax;
-        for (int j = 0; j < W; ++j) {
-          double acc = 0.0;
-          for (int i = 0; i < W; ++i) acc += g[i] * J[(size_t)i * W + j];
-          en[j] = acc;
+        if (ysup) {
+          /* (g J)_j = a_j g_j - a_j sum_i a_i g_i, and sum_i a_i g_i is
+           * dl/dy_n . y_n (Eq. 6): with a supplied output row y'_n that
+           * term is taken as dl/dy_n . y'_n */
+          const double* yn = ysup + row_off(b, n, h, T, H, d);
+          double dn = 0.0;
+          for (int i = 0; i < d; ++i) dn += dyn[i] * yn[i];
+          for (int j = 0; j < W; ++j) en[j] = an[j] * (g[j] - dn);
+        } else {
+          /* softmax Jacobian J_ij = da_i/dz_j = a_i (delta_ij - a_j) */
+          for (int i = 0; i < W; ++i)
+            for (int j = 0; j < W; ++j) J[(size_t)i * W + j] = an[i] * ((i == j ? 1.0 : 0.0) - an[j]);
+          /* e = g J (Eq. 9 combined with the incoming gradient) */
+          for (int j = 0; j < W; ++j) {
+            double acc = 0.0;
+            for (int i = 0; i < W; ++i) acc += g[i] * J[(size_t)i * W + j];
+            en[j] = acc;
+          }
         }
         /* Eq. 10: dl/dq_n = (1/sqrt d) e [k_{n-B} .. k_{n+A}]^T */
         double* dqn = dq + row_off(b, n, h, T, H, d);
@@ -347,7 +365,9 @@ int oracle_llsa_forward(const double* q, const double* k, const double* v, int n
 
 /*
  * Same arguments as oracle_llsa_forward plus dy ([nout][B][T][H][d], the
- * gradient of the loss with respect to each output); writes dq, dk, dv
+ * gradient of the loss with respect to each output) and ysup (nullable,
+ * [nout][B][T][H][d], a supplied output, used as in oracle_sa_backward);
+ * writes dq, dk, dv
  * ([nbranch][B][T][H][d]). The paper gives the LLSA gradient only in part
  * (Eq. 16, the values); here it is the exact adjoint of the forward, taken
  * per output row exactly as for SA (Eq. 7-13): with a the row's weights over
@@ -359,7 +379,7 @@ int oracle_llsa_forward(const double* q, const double* k, const double* v, int n
  * forward's (the same channel map). Rows past a sequence's end get zero.
  */
 int oracle_llsa_backward(const double* q, const double* k, const double* v, const double* dy,
-                         int nbranch, const int32_t* alias, int nout, const int32_t* out_channel,
+                         const double* ysup, int nbranch, const int32_t* alias, int nout, const int32_t* out_channel,
                          const int32_t* q_branch, int convention, double* dq, double* dk,
                          double* dv, int B, int T, int H, int d, int Lb, int La,
                          const int32_t* lengths, int threads) {
@@ -440,12 +460,21 @@ int oracle_llsa_backward(const double* q, const double* k, const double* v, cons
             for (int i = 0; i < d; ++i) acc += dyt[i] * vr[j][i];
             g[j] = acc;
           }
-          for (int i = 0; i < W; ++i)
-            for (int j = 0; j < W; ++j) J[(size_t)i * W + j] = a[i] * ((i == j ? 1.0 : 0.0) - a[j]);
-          for (int j = 0; j < W; ++j) {
-            double acc = 0.0;
-            for (int i = 0; i < W; ++i) acc += g[i] * J[(size_t)i * W + j];
-            e[j] = acc;
+          if (ysup) {
+            /* as in oracle_sa_backward: the a a^T part of J through the
+             * supplied output row of this output channel */
+            const double* yt = ysup + (size_t)o * bstride + row_off(b, t, h, T, H, d);
+            double dt = 0.0;
+            for (int i = 0; i < d; ++i) dt += dyt[i] * yt[i];
+            for (int j = 0; j < W; ++j) e[j] = a[j] * (g[j] - dt);
+          } else {
+            for (int i = 0; i < W; ++i)
+              for (int j = 0; j < W; ++j) J[(size_t)i * W + j] = a[i] * ((i == j ? 1.0 : 0.0) - a[j]);
+            for (int j = 0; j < W; ++j) {
+              double acc = 0.0;
+              for (int i = 0; i < W; ++i) acc += g[i] * J[(size_t)i * W + j];
+              e[j] = acc;
+            }
           }
           double* dqt = dq + qb + row_off(b, t, h, T, H, d);
           for (int i = 0; i < d; ++i) {

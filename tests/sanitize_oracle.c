@@ -14,12 +14,12 @@
 
 int oracle_sa_forward(const double*, const double*, const double*, double*, double*, int, int, int,
                       int, int, int, const int32_t*, int);
-int oracle_sa_backward(const double*, const double*, const double*, const double*, double*, double*,
-                       double*, int, int, int, int, int, int, const int32_t*, int);
+int oracle_sa_backward(const double*, const double*, const double*, const double*, const double*,
+                       double*, double*, double*, int, int, int, int, int, int, const int32_t*, int);
 int oracle_llsa_forward(const double*, const double*, const double*, int, const int32_t*, int,
                         const int32_t*, const int32_t*, int, double*, double*, int, int, int, int,
                         int, int, const int32_t*, int);
-int oracle_llsa_backward(const double*, const double*, const double*, const double*, int,
+int oracle_llsa_backward(const double*, const double*, const double*, const double*, const double*, int,
                          const int32_t*, int, const int32_t*, const int32_t*, int, double*,
                          double*, double*, int, int, int, int, int, int, const int32_t*, int);
 int oracle_sa_stream_step(const double*, const double*, const double*, double*, double*, double*,
@@ -63,7 +63,9 @@ int main(void) {
     double *y = rnd(n), *lse = rnd((size_t)B * H * T), *dq = rnd(n), *dk = rnd(n), *dv = rnd(n);
     CHECK(oracle_sa_forward(q, k, v, y, lse, B, T, H, d, Lb, La, lengths, 1) == 0);
     CHECK(finite(y, n));
-    CHECK(oracle_sa_backward(q, k, v, dy, dq, dk, dv, B, T, H, d, Lb, La, lengths, 1) == 0);
+    CHECK(oracle_sa_backward(q, k, v, dy, NULL, dq, dk, dv, B, T, H, d, Lb, La, lengths, 1) == 0);
+    CHECK(finite(dq, n) && finite(dk, n) && finite(dv, n));
+    CHECK(oracle_sa_backward(q, k, v, dy, y, dq, dk, dv, B, T, H, d, Lb, La, lengths, 1) == 0);
     CHECK(finite(dq, n) && finite(dk, n) && finite(dv, n));
     free(q); free(k); free(v); free(dy); free(y); free(lse); free(dq); free(dk); free(dv);
     /* LLSA, paper channel form and two-branch form, both conventions */
@@ -83,9 +85,11 @@ int main(void) {
         CHECK(oracle_llsa_forward(lq, lk, lv, nb, alias, nout, outc, qb, conv, ly, ll, B, T, H, d, Lb,
                                   La, lengths, 1) == 0);
         CHECK(finite(ly, mo));
-        CHECK(oracle_llsa_backward(lq, lk, lv, ldy, nb, alias, nout, outc, qb, conv, ldq, ldk, ldv,
-                                   B, T, H, d, Lb, La, lengths, 1) == 0);
-        CHECK(finite(ldq, m) && finite(ldk, m) && finite(ldv, m));
+        for (int sup = 0; sup < 2; ++sup) {
+          CHECK(oracle_llsa_backward(lq, lk, lv, ldy, sup ? ly : NULL, nb, alias, nout, outc, qb, conv,
+                                     ldq, ldk, ldv, B, T, H, d, Lb, La, lengths, 1) == 0);
+          CHECK(finite(ldq, m) && finite(ldk, m) && finite(ldv, m));
+        }
       }
       free(lq); free(lk); free(lv); free(ly); free(ll); free(ldy); free(ldq); free(ldk); free(ldv);
     }

@@ -8,7 +8,7 @@ import torch
 
 from paper_2302_13451_amd import binding as bd
 from paper_2302_13451_amd.inputs import sa_inputs
-from parity import assert_close, assert_lse_close, f64, to_gpu
+from parity import assert_close, assert_lse_close, assert_slices_close, f64, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -61,16 +61,27 @@ VARIANTS = [("bf16", "rsqrt_d", 1.0), ("bf16", "unit", 1.0), ("bf16", "unit", 4.
 @pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", SHAPES)
 def test_forward_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale, peak):
     for seed in (3, 4):
-        out, lse, yr, lr, _ = run_forward(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths,
+        out, lse, yr, lr, x = run_forward(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths,
                                           scale, peak)
-        assert_close(out, yr, dtype, "out")
+        assert_slices_close(out, yr, dtype, x["lengths"], "out")
         assert_lse_close(lse, lr, dtype)
 
 
 def test_config2_full_size(oracle_mod):
     """SA forward bf16, B=8, T=500, H=12, d=64, Lb=32, La=8, N(0,1)/sqrt(d)."""
-    out, lse, yr, lr, _ = run_forward(oracle_mod, 8, 500, 12, 64, 32, 8, "bf16", seed=2)
-    assert_close(out, yr, "bf16", "out")
+    out, lse, yr, lr, x = run_forward(oracle_mod, 8, 500, 12, 64, 32, 8, "bf16", seed=2)
+    assert_slices_close(out, yr, "bf16", x["lengths"], "out")
+    assert_lse_close(lse, lr, "bf16")
+
+
+@pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
+def test_config3_forward_full_size(oracle_mod, scale):
+    """SA forward bf16 at the benchmarked shape, B=16, T=800, H=12, d=64,
+    Lb=64, La=8, lengths U[400, 800] with tail padding: out per (sequence,
+    head) slice and element, lse per row."""
+    out, lse, yr, lr, x = run_forward(oracle_mod, 16, 800, 12, 64, 64, 8, "bf16", 3, (400, 800),
+                                      scale)
+    assert_slices_close(out, yr, "bf16", x["lengths"], "out")
     assert_lse_close(lse, lr, "bf16")
 
 

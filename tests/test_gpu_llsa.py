@@ -8,7 +8,7 @@ import torch
 
 from paper_2302_13451_amd import binding as bd
 from paper_2302_13451_amd.inputs import llsa_inputs
-from parity import assert_close, assert_lse_close, f64, to_gpu
+from parity import assert_lse_close, assert_slices_close, f64, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -23,7 +23,7 @@ def run(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths, scale="rsqrt_d", p
     clean = {n: np.nan_to_num(f64(x[n])) for n in ("q", "k", "v")}
     yr, lr = oracle_mod.llsa_two_branch(clean["q"], clean["k"], clean["v"], Lb, La,
                                         x["lengths"].numpy())
-    return f64(out), lse.cpu().numpy(), yr, lr
+    return f64(out), lse.cpu().numpy(), yr, lr, x["lengths"].numpy()
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -43,24 +43,22 @@ def run(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths, scale="rsqrt_d", p
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):
-    out, lse, yr, lr = run(oracle_mod, B, T, H, d, Lb, La, dtype, 31, lengths, scale)
-    assert_close(out[0], yr[0], dtype, "causal out")
-    assert_close(out[1], yr[1], dtype, "look-ahead out")
+    out, lse, yr, lr, ln = run(oracle_mod, B, T, H, d, Lb, La, dtype, 31, lengths, scale)
+    assert_slices_close(out, yr, dtype, ln, "out (causal, look-ahead)")
     assert_lse_close(lse, lr, dtype)
 
 
 def test_config4_full_size(oracle_mod):
     """LLSA forward bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, lengths U[400, 800]."""
-    out, lse, yr, lr = run(oracle_mod, 16, 800, 12, 64, 64, 8, "bf16", 4, (400, 800))
-    assert_close(out[0], yr[0], "bf16", "causal out")
-    assert_close(out[1], yr[1], "bf16", "look-ahead out")
+    out, lse, yr, lr, ln = run(oracle_mod, 16, 800, 12, 64, 64, 8, "bf16", 4, (400, 800))
+    assert_slices_close(out, yr, "bf16", ln, "out (causal, look-ahead)")
     assert_lse_close(lse, lr, "bf16")
 
 
 def test_llsa_padded_frames_are_never_read(oracle_mod):
-    out, lse, yr, lr = run(oracle_mod, 3, 180, 2, 64, 30, 6, "bf16", 33, (40, 179),
-                           pad=float("nan"))
-    assert_close(out, yr, "bf16", "out")
+    out, lse, yr, lr, ln = run(oracle_mod, 3, 180, 2, 64, 30, 6, "bf16", 33, (40, 179),
+                               pad=float("nan"))
+    assert_slices_close(out, yr, "bf16", ln, "out")
     assert_lse_close(lse, lr, "bf16")
 
 

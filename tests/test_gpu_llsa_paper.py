@@ -9,7 +9,7 @@ import torch
 
 from paper_2302_13451_amd import binding as bd
 from paper_2302_13451_amd.inputs import llsa_inputs
-from parity import assert_close, assert_lse_close, f64, to_gpu
+from parity import assert_close, assert_lse_close, assert_slices_close, f64, round_to, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -28,9 +28,8 @@ def run(oracle_mod, B, T, H, d, Lb, La, dtype, seed, lengths, scale="rsqrt_d", p
     return f64(out), lse.cpu().numpy(), yr, lr, x["lengths"].numpy()
 
 
-def check(out, lse, yr, lr, dtype):
-    for c in range(out.shape[0]):
-        assert_close(out[c], yr[c], dtype, "channel %d out" % c)
+def check(out, lse, yr, lr, lengths, dtype):
+    assert_slices_close(out, yr, dtype, lengths, "out")
     assert_lse_close(lse, lr, dtype)
 
 
@@ -45,22 +44,32 @@ def check(out, lse, yr, lr, dtype):
     (66, 40, 1, 32, 10, 2, (0, 40)),
     (2, 110, 2, 64, 30, 15, (40, 110)),  # the widest look-ahead of the one-tile diagonal pass
     (2, 110, 2, 32, 30, 16, (40, 110)),  # and one past it
+    # bfloat16 look-backs of 80 frames and more take the band passes and the
+    # merge instead of the one-pass kernel: both sides of that switch, and
+    # wide look-backs with short and long look-aheads
+    (2, 200, 2, 64, 79, 8, (60, 200)),
+    (2, 200, 2, 64, 80, 8, (60, 200)),
+    (2, 200, 2, 64, 90, 8, (60, 200)),
+    (2, 220, 2, 32, 100, 4, (1, 220)),
+    (2, 260, 2, 64, 150, 15, (100, 260)),
+    (2, 140, 2, 64, 120, 1, (90, 140)),
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_paper_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale):
-    check(*run(oracle_mod, B, T, H, d, Lb, La, dtype, 41, lengths, scale)[:4], dtype)
+    check(*run(oracle_mod, B, T, H, d, Lb, La, dtype, 41, lengths, scale), dtype)
 
 
 def test_llsa_paper_config4_shape(oracle_mod):
-    """bf16, B=4, T=800, H=12, d=64, Lb=64, La=8 (nine channels), lengths
-    U[400, 800]."""
-    check(*run(oracle_mod, 4, 800, 12, 64, 64, 8, "bf16", 5, (400, 800))[:4], "bf16")
+    """bf16, B=16, T=800, H=12, d=64, Lb=64, La=8 (nine channels), lengths
+    U[400, 800]: the benchmarked shape, every (channel, sequence, head) slice
+    element by element."""
+    check(*run(oracle_mod, 16, 800, 12, 64, 64, 8, "bf16", 5, (400, 800)), "bf16")
 
 
 def test_llsa_paper_padded_frames_are_never_read(oracle_mod):
     out, lse, yr, lr, ln = run(oracle_mod, 3, 160, 2, 64, 24, 5, "bf16", 43, (40, 159),
                                pad=float("nan"))
-    check(out, lse, yr, lr, "bf16")
+    check(out, lse, yr, lr, ln, "bf16")
     for b, L in enumerate(ln):
         assert (out[:, b, L:] == 0).all()
         assert np.isneginf(lse[:, b, :, L:]).all()
@@ -110,28 +119,56 @@ def test_llsa_paper_rejects_bad_arguments():
 # backward
 
 
-def run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
-    print("llsa paper backward case B=%d T=%d H=%d d=%d Lb=%d La=%d seed=%d" % (
-        B, T, H, d, Lb, La, seed), flush=True)
+# Each backward case runs twice, as for the SA backward: with the oracle's
+# forward output (rounded to bfloat16) and log-sum-exp supplied to both sides,
+# per (channel, sequence, head) slice normwise and element by element against
+# the row's scale; and end to end against the exact gradient, per channel
+# tensor normwise (the rounding of `out` to bfloat16 alone moves a slice of dq
+# by about 2e-2 of its maximum).
+def run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0,
+            supplied=False):
+    print("llsa paper backward %s case B=%d T=%d H=%d d=%d Lb=%d La=%d seed=%d" % (
+        "supplied-output" if supplied else "end-to-end", B, T, H, d, Lb, La, seed), flush=True)
     x = llsa_inputs(B, T, H, d, seed, dtype="bf16", scale=scale, lengths=lengths, pad_value=pad,
                     with_dout=True, channels=La + 1)
     q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
     ln = x["lengths"].cuda()
-    out, lse = bd.llsa_paper_forward(q, k, v, Lb, La, ln)
+    clean = {n: np.nan_to_num(f64(x[n])) for n in ("q", "k", "v", "dout")}
+    L = x["lengths"].numpy()
+    y = None
+    if supplied:
+        y, lse = oracle_mod.llsa_paper(clean["q"], clean["k"], clean["v"], Lb, La, L)
+        y = round_to(y, "bf16")
+        out, lse = torch.from_numpy(y).to(torch.bfloat16).cuda(), torch.from_numpy(lse).float().cuda()
+    else:
+        out, lse = bd.llsa_paper_forward(q, k, v, Lb, La, ln)
     dq, dk, dv = bd.llsa_paper_backward(q, k, v, out, lse, do, Lb, La, ln)
     torch.cuda.synchronize()
-    clean = {n: np.nan_to_num(f64(x[n] if n != "dout" else do.cpu())) for n in ("q", "k", "v", "dout")}
     ref = oracle_mod.llsa_paper_backward(clean["q"], clean["k"], clean["v"], clean["dout"], Lb, La,
-                                         x["lengths"].numpy())
+                                         L, y=y)
     return (f64(dq), f64(dk), f64(dv)), ref, x["lengths"].tolist()
 
 
-def check_bwd(got, ref):
+def check_bwd(got, ref, lengths, mode="supplied"):
+    """mode: "supplied" (per slice and element) or "tensors" (per channel
+    tensor)."""
     zero_atol = 1e-5 * float(np.max(np.abs(ref[2])))
     for name, g, r in zip(("dq", "dk", "dv"), got, ref):
-        for c in range(g.shape[0]):
-            assert_close(g[c], r[c], "bf16", "%s channel %d" % (name, c), elementwise=False,
-                         zero_atol=zero_atol)
+        if mode == "tensors":
+            for c in range(g.shape[0]):
+                assert_close(g[c], r[c], "bf16", "%s channel %d" % (name, c), elementwise=False,
+                             zero_atol=zero_atol)
+        else:
+            assert_slices_close(g, r, "bf16", lengths, name, zero_atol=zero_atol,
+                                row_scale=True)
+
+
+def run_check_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
+    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad, supplied=True)
+    check_bwd(got, ref, L, "supplied")
+    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad)
+    check_bwd(got, ref, L, "tensors")
+    return got, L
 
 
 @pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
@@ -151,20 +188,18 @@ def check_bwd(got, ref):
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_paper_backward_parity(oracle_mod, B, T, H, d, Lb, La, lengths, scale):
-    got, ref, _ = run_bwd(oracle_mod, B, T, H, d, Lb, La, 52, lengths, scale)
-    check_bwd(got, ref)
+    run_check_bwd(oracle_mod, B, T, H, d, Lb, La, 52, lengths, scale)
 
 
 def test_llsa_paper_backward_config4_shape(oracle_mod):
-    """bf16, B=4, T=800, H=12, d=64, Lb=64, La=8 (nine channels), lengths
-    U[400, 800]."""
-    got, ref, _ = run_bwd(oracle_mod, 4, 800, 12, 64, 64, 8, 6, (400, 800))
-    check_bwd(got, ref)
+    """bf16, B=16, T=800, H=12, d=64, Lb=64, La=8 (nine channels), lengths
+    U[400, 800]: the benchmarked shape."""
+    run_check_bwd(oracle_mod, 16, 800, 12, 64, 64, 8, 6, (400, 800))
 
 
 def test_llsa_paper_backward_padded_frames_are_never_read(oracle_mod):
-    got, ref, lengths = run_bwd(oracle_mod, 3, 180, 2, 64, 30, 6, 53, (40, 179), pad=float("nan"))
-    check_bwd(got, ref)
+    got, lengths = run_check_bwd(oracle_mod, 3, 180, 2, 64, 30, 6, 53, (40, 179),
+                                 pad=float("nan"))
     for g in got:
         for b, L in enumerate(lengths):
             assert (g[:, b, L:] == 0).all()

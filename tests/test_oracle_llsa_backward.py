@@ -111,3 +111,56 @@ def test_padding_rows_zero_and_padded_inputs_unread(oracle_mod):
     for g in (dq, dk, dv):
         assert np.all(np.isfinite(g))
         assert np.all(g[:, 1, 6:] == 0.0)
+
+
+def _fd_check_lse(fwd, bwd, q, k, v, dy, c, h=1e-6, tol=2e-7):
+    """Finite differences of L = sum_o dy_o . y_o - sum_(o,t) c_(o,t) lse_(o,t)."""
+    dq, dk, dv = bwd(q, k, v, dy)
+
+    def loss():
+        y, lse = fwd(q, k, v)
+        fin = np.isfinite(lse)
+        return float(np.sum(y * dy) - np.sum(np.where(fin, c * np.where(fin, lse, 0.0), 0.0)))
+
+    for name, x, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        num = np.zeros_like(x)
+        it = np.nditer(x, flags=["multi_index"])
+        for _ in it:
+            i = it.multi_index
+            old = x[i]
+            x[i] = old + h
+            lp = loss()
+            x[i] = old - h
+            lm = loss()
+            x[i] = old
+            num[i] = (lp - lm) / (2 * h)
+        err = np.max(np.abs(num - g))
+        assert err < tol, "d%s differs from finite differences by %g" % (name, err)
+
+
+@pytest.mark.parametrize("form", ["two-branch", "paper"])
+def test_supplied_output_gradient(oracle_mod, form):
+    """With a supplied output y' = y + delta, the Jacobian product of every row
+    moves by -a_j (dy . delta) = the gradient of -(dy . delta) lse (d lse / d z_j
+    = a_j): the gradient matches finite differences of
+    sum dy . y - sum c lse, c = dy . delta held constant. With delta = 0 it is
+    the exact gradient."""
+    Lb, La, lengths = 3, 2, [9, 6]
+    rng = np.random.default_rng(17 if form == "paper" else 18)
+    nb = La + 1 if form == "paper" else 2
+    shape = (nb, 2, 9, 1, 3)
+    q, k, v, dy = (_rand(rng, shape) for _ in range(4))
+    if form == "paper":
+        fwd = lambda q, k, v: oracle_mod.llsa_paper(q, k, v, Lb, La, lengths, threads=1)
+        bwd = lambda q, k, v, dy, y=None: oracle_mod.llsa_paper_backward(
+            q, k, v, dy, Lb, La, lengths, threads=1, y=y)
+    else:
+        fwd = lambda q, k, v: oracle_mod.llsa_two_branch(q, k, v, Lb, La, lengths, threads=1)
+        bwd = lambda q, k, v, dy, y=None: oracle_mod.llsa_two_branch_backward(
+            q, k, v, dy, Lb, La, lengths, threads=1, y=y)
+    y, _ = fwd(q, k, v)
+    for g, r in zip(bwd(q, k, v, dy, y), bwd(q, k, v, dy)):
+        np.testing.assert_allclose(g, r, rtol=1e-11, atol=1e-13)
+    delta = 0.3 * _rand(rng, y.shape)
+    c = np.transpose((dy * delta).sum(axis=-1), (0, 1, 3, 2))  # [nout][B][H][T], as lse
+    _fd_check_lse(fwd, lambda q, k, v, dy: bwd(q, k, v, dy, y + delta), q, k, v, dy, c)

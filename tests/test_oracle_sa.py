@@ -257,3 +257,53 @@ def test_dv_support_probe(oracle_mod):
         got = set(np.flatnonzero(dv[0, tau, 0]))
         want = set() if tau >= ln[0] else {n % d for n in range(max(0, tau - La), min(ln[0] - 1, tau + Lb) + 1)}
         assert got == want, tau
+
+
+# --------------------------------------------------------------------------- #
+# backward given a supplied forward output
+# --------------------------------------------------------------------------- #
+
+def test_supplied_exact_output_gives_the_exact_gradient(oracle_mod):
+    """With its own forward output supplied, the gradient through
+    dy_n . y_n equals the explicit-Jacobian gradient: sum_i a_i g_i = dy . y
+    (Eq. 6)."""
+    x, ln = np_inputs(2, 30, 2, 8, seed=44, lengths=(13, 30))
+    y, _ = oracle_mod.sa_forward(x["q"], x["k"], x["v"], 5, 3, ln)
+    ref = oracle_mod.sa_backward(x["q"], x["k"], x["v"], x["dout"], 5, 3, ln)
+    got = oracle_mod.sa_backward(x["q"], x["k"], x["v"], x["dout"], 5, 3, ln, y=y)
+    for g, r in zip(got, ref):
+        np.testing.assert_allclose(g, r, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", CASES[:4])
+def test_supplied_output_equals_autograd_with_lse_term(oracle_mod, B, T, H, d, Lb, La, lengths):
+    """A supplied output y' = y + delta shifts the Jacobian product by
+    -a_j (dy_n . delta_n), the gradient of -(dy_n . delta_n) lse_n
+    (d lse / d z_j = a_j). So the gradient equals torch autograd of
+    sum dy . y - sum_n c_n lse_n with c_n = dy_n . delta_n held constant,
+    through brute-force masked attention; dv does not change."""
+    x, ln = np_inputs(B, T, H, d, seed=47 + T, lengths=lengths)
+    y, _ = oracle_mod.sa_forward(x["q"], x["k"], x["v"], Lb, La, ln)
+    rng = np.random.default_rng(T)
+    delta = 0.05 * rng.standard_normal(y.shape)
+    got = oracle_mod.sa_backward(x["q"], x["k"], x["v"], x["dout"], Lb, La, ln, y=y + delta)
+    exact = oracle_mod.sa_backward(x["q"], x["k"], x["v"], x["dout"], Lb, La, ln)
+    np.testing.assert_array_equal(got[2], exact[2])
+    c = torch.from_numpy((x["dout"] * delta).sum(axis=-1))  # [B][T][H]
+    q, k, v = (torch.from_numpy(x[n]).clone().requires_grad_(True) for n in ("q", "k", "v"))
+    total = 0.0
+    for b in range(B):
+        m = torch.from_numpy(band_mask(T, Lb, La, ln[b]))
+        z = torch.matmul(q[b].transpose(0, 1), k[b].transpose(0, 1).transpose(1, 2)) / math.sqrt(d)
+        z = z.masked_fill(~m, float("-inf"))  # [H][T][T]
+        rows = torch.arange(T) < ln[b]
+        a = torch.zeros_like(z)
+        a[:, rows] = torch.softmax(z[:, rows], dim=-1)
+        yb = torch.matmul(a, v[b].transpose(0, 1)).transpose(0, 1)  # [T][H][d]
+        lse = torch.logsumexp(z[:, rows], dim=-1)  # [H][n_valid]
+        total = total + (yb * torch.from_numpy(x["dout"][b])).sum() \
+            - (c[b, rows].transpose(0, 1) * lse).sum()
+    total.backward()
+    np.testing.assert_allclose(got[0], q.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(got[1], k.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(got[2], v.grad.numpy(), rtol=1e-10, atol=1e-12)
