@@ -270,6 +270,20 @@ int llsa_stream_step(const void* qc, const void* kc, const void* vc,
                      int S, int H, int d, int Lb, int La,
                      const int32_t* lengths, int dtype, void* stream);
 
+/*
+ * Device-copy reference for measurement; not part of the method. Copies
+ * `bytes` bytes from src to dst on `stream`, so that its duration and its
+ * hardware-counter readings give the practical bandwidth ceiling and the
+ * counter calibration the band kernels are measured against:
+ *   mode 0: 16-byte vector loads into registers and 16-byte vector stores;
+ *   mode 1: 16-byte direct global-to-LDS copies (the staging path of the
+ *           band kernels), LDS reads and 16-byte vector stores.
+ * src, dst : device pointers, 16-byte aligned, not overlapping
+ * bytes    : a multiple of 16 in [0, 2^40]; 0 is a no-op
+ * Returns SA_ERR_NULL / SA_ERR_INVALID for bad arguments before any HIP call.
+ */
+int sa_copy_reference(const void* src, void* dst, long long bytes, int mode, void* stream);
+
 /* Message for the last non-zero status returned to the calling thread. */
 const char* sa_last_error(void);
 

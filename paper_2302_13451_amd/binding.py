@@ -46,6 +46,7 @@ _SIGNATURES = {
                        _i, _vp],
     "llsa_stream_step": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _vp,
                          _vp, _vp, _i, _i, _i, _i, _i, _vp, _i, _vp],
+    "sa_copy_reference": [_vp, _vp, ctypes.c_longlong, _i, _vp],
     "sa_last_error": [],
     "sa_abi_version": [],
 }
@@ -334,3 +335,17 @@ def llsa_stream_step(state: LlsaStreamState, qc, kc, vc, ql, kl, vl, out_c=None,
         _ptr(state.emitted_l), S, H, d, state.Lb, state.La, _ptr(state.lengths), code,
         _stream(dev, stream)))
     return out_c, state.emitted_c, out_l, state.emitted_l
+
+
+def copy_reference(src: torch.Tensor, dst: torch.Tensor, mode: int = 0, *, stream=None):
+    """Device-copy reference for measurement (not part of the method): copies
+    src into dst (same size in bytes, contiguous, GPU) with 16-byte vector
+    loads (mode 0) or direct global->LDS copies (mode 1)."""
+    if not (src.is_cuda and dst.is_cuda and src.is_contiguous() and dst.is_contiguous()):
+        raise SAError(SA_ERR_INVALID, "src and dst must be contiguous GPU tensors")
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise SAError(SA_ERR_INVALID, "src and dst differ in size")
+    _check(load_library().sa_copy_reference(_ptr(src), _ptr(dst), n, int(mode),
+                                            _stream(src.device, stream)))
+    return dst

@@ -388,4 +388,17 @@ int llsa_stream_step(const void* qc, const void* kc, const void* vc, const void*
       sa::launch_llsa_stream_step(a, elem(dtype), static_cast<hipStream_t>(stream)), fn);
 }
 
+int sa_copy_reference(const void* src, void* dst, long long bytes, int mode, void* stream) {
+  const char* fn = "sa_copy_reference";
+  if (bytes < 0 || (bytes & 15) != 0 || bytes > (1LL << 40))
+    return fail(SA_ERR_INVALID, "%s: bytes = %lld must be a multiple of 16 in [0, 2^40]", fn, bytes);
+  if (mode != 0 && mode != 1) return fail(SA_ERR_INVALID, "%s: mode %d is not 0 or 1", fn, mode);
+  if (bytes == 0) return SA_OK;
+  if (int rc = check_ptrs(fn, {src, dst}, {}, {})) return rc;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  const uintptr_t n = static_cast<uintptr_t>(bytes);
+  if (s0 < d0 + n && d0 < s0 + n) return fail(SA_ERR_INVALID, "%s: src and dst overlap", fn);
+  return check_launch(sa::launch_copy_reference(src, dst, bytes, mode, static_cast<hipStream_t>(stream)), fn);
+}
+
 }  // extern "C"

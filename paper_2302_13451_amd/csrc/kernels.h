@@ -123,4 +123,8 @@ struct LlsaStreamStepArgs {
 
 hipError_t launch_llsa_stream_step(const LlsaStreamStepArgs& a, ElemType et, hipStream_t stream);
 
+// Device-copy reference (copy_reference.hip): bytes a multiple of 16, mode 0
+// through registers, mode 1 through direct global->LDS copies.
+hipError_t launch_copy_reference(const void* src, void* dst, long long bytes, int mode, hipStream_t stream);
+
 }  // namespace sa

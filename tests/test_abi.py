@@ -167,3 +167,14 @@ def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(bd, "_LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(bd.SAError):
         bd.load_library()
+
+
+def test_copy_reference_validation(lib):
+    cp = lib.sa_copy_reference
+    assert cp(FAKE, ctypes.c_void_p(0x20000), 0, 0, None) == bd.SA_OK
+    assert cp(FAKE, ctypes.c_void_p(0x20000), 24, 0, None) == bd.SA_ERR_INVALID    # not 16-byte pieces
+    assert cp(FAKE, ctypes.c_void_p(0x20000), -16, 0, None) == bd.SA_ERR_INVALID
+    assert cp(FAKE, ctypes.c_void_p(0x20000), 64, 2, None) == bd.SA_ERR_INVALID    # no mode 2
+    assert cp(None, ctypes.c_void_p(0x20000), 64, 0, None) == bd.SA_ERR_NULL
+    assert cp(FAKE_ODD, ctypes.c_void_p(0x20000), 64, 1, None) == bd.SA_ERR_INVALID
+    assert cp(FAKE, ctypes.c_void_p(0x10010), 64, 0, None) == bd.SA_ERR_INVALID   # overlap
