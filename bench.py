@@ -8,7 +8,12 @@ value is valid frames per second over the whole step. Inputs are resident in
 HBM before timing; four copies of the batch are rotated so that no step finds
 its inputs in the 256 MB Infinity Cache.
 
-The same run also times, on their own workloads:
+The same run also measures:
+  * the device-copy reference of the library at the backward's traffic size,
+    the practical bandwidth ceiling (row "copy_ceiling"; the roofline object
+    carries it and the achieved fraction of it);
+  * sa_forward at the paper's l32_r8 window, B=8, T=500 (row
+    "sa_forward_l32_r8");
   * llsa_forward and llsa_backward, two-branch, same shapes (rows "llsa",
     "llsa_backward");
   * llsa_paper_forward and llsa_paper_backward, the paper's channel form with
@@ -16,12 +21,16 @@ The same run also times, on their own workloads:
     "llsa_paper_backward");
   * sa_stream_step, 64 streams x 1000 steps, ring of 64 + 8 + 1 frames, eager
     and replayed from a HIP graph (row "stream"), and llsa_stream_step on the
-    same shapes (row "llsa_stream");
+    same shapes (row "llsa_stream"), each against the launch floor (an empty
+    launch, eager and from a graph), which bounds them;
   * the algorithmic latency of a 12-layer streaming stack, SA against LLSA
     (row "stream_latency");
   * masked full attention in PyTorch (dense T x T scores, band mask) as the
-    GPU baseline the paper argues against (row "masked_attention_torch");
-  * the CPU oracle on the host cores (``cpu_baseline``).
+    GPU baseline the paper argues against, and torch's
+    scaled_dot_product_attention with a boolean band mask (row
+    "masked_attention_torch");
+  * the CPU oracle on every host core the process may use, on one core, and
+    on the other configurations (``cpu_baseline``).
 
 Prints one JSON line. ``--gpus N`` with N > 1 is not supported (one GPU).
 """
@@ -65,6 +74,21 @@ def source_sha(*names):
         with open(os.path.join(ROOT, "paper_2302_13451_amd", "csrc", n), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def load_mfma(profile_name, sha):
+    """MFMA rate of the kernel from the committed rocprofv3 SQ-counter summary
+    (bf16 MFMA operations per launch over the kernel's duration, against the
+    dense bf16 peak), if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", profile_name)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha") != sha:
+        return None
+    return {k: rec.get(k) for k in ("mfma_tflops", "mfma_frac_of_bf16_peak", "valu_busy",
+                                    "lds_bank_conflict_frac", "mfma_busy")}
 
 
 def load_traffic(profile_name, sha):
@@ -174,10 +198,74 @@ def launch_ms(fn, sets, n):
     torch.cuda.synchronize()
     s0.record()
     for i in range(n):
-        fn(sets[i % N_SETS])
+        fn(sets[i % len(sets)])
     s1.record()
     torch.cuda.synchronize()
     return s0.elapsed_time(s1) / n
+
+
+def copy_ceiling(mib=64, reps=24):
+    """Bandwidth of the library's device-copy reference (sa_copy_reference) at
+    the band kernels' traffic size: mib MiB copied (read + written), four
+    buffer pairs rotated so no copy finds its source in the Infinity Cache,
+    back-to-back launches between HIP events, both access paths."""
+    n = mib << 20
+    pairs = [(torch.empty(n // 4, dtype=torch.int32, device="cuda"),
+              torch.empty(n // 4, dtype=torch.int32, device="cuda")) for _ in range(4)]
+    res = {"bytes_copied": n, "bytes_moved": 2 * n}
+    for mode, name in ((0, "registers"), (1, "direct_to_lds")):
+        for i in range(8):
+            bd.copy_reference(*pairs[i % 4], mode)
+        ms = launch_ms(lambda p: bd.copy_reference(p[0], p[1], mode), pairs, reps)
+        res[name + "_gbs"] = 2 * n / (ms * 1e-3) / 1e9
+    res["gbs"] = max(res["registers_gbs"], res["direct_to_lds_gbs"])
+    del pairs
+    return res
+
+
+C2 = dict(B=8, T=500, H=12, d=64, Lb=32, La=8, lengths="full", seed=2)
+
+
+def bench_c2(steps, warmup):
+    """SA forward bf16 at the paper's l32_r8 window: B=8, T=500 (10 s of 20 ms
+    frames), H=12, d=64, Lb=32, La=8, no padding. Twelve copies of the inputs
+    rotate (about 300 MB), so no call finds them in the Infinity Cache."""
+    c = C2
+    x = sa_inputs(c["B"], c["T"], c["H"], c["d"], c["seed"], dtype="bf16", lengths=c["lengths"],
+                  with_dout=False)
+    base = {n: x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v")}
+    lengths = x["lengths"].cuda()
+    sets = []
+    for i in range(12):
+        s = {n: (t if i == 0 else t.clone()) for n, t in base.items()}
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty(c["B"], c["H"], c["T"], dtype=torch.float32, device="cuda")
+        sets.append(s)
+
+    def fwd(s):
+        bd.sa_forward(s["q"], s["k"], s["v"], c["Lb"], c["La"], lengths, out=s["out"],
+                      lse=s["lse"])
+
+    for i in range(max(warmup, 12)):
+        fwd(sets[i % 12])
+    torch.cuda.synchronize()
+    ms = launch_ms(fwd, sets, max(steps, 48))
+    L = x["lengths"].tolist()
+    byts = acc.sa_forward_bytes(L, c["H"], c["d"])
+    flops = acc.sa_forward_flops(L, c["H"], c["d"], c["Lb"], c["La"])
+    gbs = byts / (ms * 1e-3) / 1e9
+    return {
+        "workload": "SA forward bf16, B=8, T=500, H=12, d=64, Lb=32, La=8, no padding (the paper's "
+                    "l32_r8 window)",
+        "ms_per_call": ms,
+        "frames_per_s": sum(L) / (ms * 1e-3),
+        "useful_tflops": flops / (ms * 1e-3) / 1e12,
+        "algorithmic_gbs": gbs,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None},
+        "algorithmic_bytes": byts,
+        "useful_flops": flops,
+    }
 
 
 def bench_llsa(steps, warmup):
@@ -305,16 +393,51 @@ def bench_llsa_paper(steps, warmup):
     return rows["forward"], rows["backward"]
 
 
-def stream_roofline(byts, step_ms):
-    """Algorithmic bytes of one streaming step over its median duration,
-    against HBM (the step's working set is cache resident and a launch costs
-    about 2.5 us, so this fraction stays small)."""
-    gbs = byts / (step_ms * 1e-3) / 1e9
-    return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "per": "step (one launch)"}
+def launch_floor(steps=1000, n_cap=100):
+    """What one launch costs by itself: the device-copy reference moving 16
+    bytes (one workgroup), launched eagerly with an event pair per launch
+    (median) and replayed from a HIP graph of n_cap launches (mean)."""
+    src = torch.zeros(4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(20):
+        bd.copy_reference(src, dst)
+    torch.cuda.synchronize()
+    t = EventTimer()
+    for _ in range(steps):
+        e = t.start()
+        bd.copy_reference(src, dst)
+        t.stop(e)
+    torch.cuda.synchronize()
+    lat = sorted(t.all_ms())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(n_cap):
+            bd.copy_reference(src, dst)
+    torch.cuda.synchronize()
+    g_ms = 0.0
+    for _ in range(steps // n_cap):
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record()
+        graph.replay()
+        s1.record()
+        torch.cuda.synchronize()
+        g_ms += s0.elapsed_time(s1)
+    return {"eager_launch_ms_p50": lat[len(lat) // 2],
+            "graph_launch_ms": g_ms / (steps // n_cap * n_cap)}
 
 
-def bench_stream():
+def stream_roofline(graph_steps_per_s, floor):
+    """A streaming step is one launch over a cache-resident working set: its
+    bound is the cost of a launch, not HBM. Graph-replayed steps per second
+    against the graph-replayed rate of an empty launch."""
+    peak = 1.0 / (floor["graph_launch_ms"] * 1e-3)
+    return {"bound": "launch", "achieved": graph_steps_per_s, "peak": peak, "unit": "steps/s",
+            "frac": graph_steps_per_s / peak, "traffic": None,
+            "per": "step (one launch, replayed from a HIP graph)"}
+
+
+def bench_stream(floor):
     c = STREAM
     S, H, d, Lb, La, steps = c["S"], c["H"], c["d"], c["Lb"], c["La"], c["steps"]
     R = Lb + La + 1
@@ -386,12 +509,14 @@ def bench_stream():
         "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
         "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
         "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
-        "roofline": stream_roofline(byts, mean_step),
+        "roofline": stream_roofline(steps / (g_ms * 1e-3), floor),
+        "hbm_frac_algorithmic": byts / (mean_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "launch_floor": floor,
         "note": "ring is L2/MALL resident; the step is launch-bound",
     }
 
 
-def bench_llsa_stream():
+def bench_llsa_stream(floor):
     """llsa_stream_step on the streaming shapes: 64 streams, H=12, d=64, Lb=64,
     La=8, open-ended, every stream emitting both outputs every step after the
     first La steps."""
@@ -457,7 +582,9 @@ def bench_llsa_stream():
         "step_latency_ms_p99": lat[min(len(lat) - 1, int(0.99 * len(lat)))],
         "kernel_gbs_algorithmic": byts / (mean_step * 1e-3) / 1e9,
         "kernel_tflops": flops / (mean_step * 1e-3) / 1e12,
-        "roofline": stream_roofline(byts, mean_step),
+        "roofline": stream_roofline((steps // n_cap * n_cap) / (g_ms * 1e-3), floor),
+        "hbm_frac_algorithmic": byts / (mean_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "launch_floor": floor,
         "note": "two outputs per stream and step; the rings are L2/MALL resident; launch-bound",
     }
 
@@ -539,9 +666,37 @@ def bench_masked_attention(steps=5):
     s1.record()
     torch.cuda.synchronize()
     ms = s0.elapsed_time(s1) / steps
-    return {"workload": "masked full attention fwd+bwd in PyTorch (float32 math on bf16 inputs), "
-                        "same batch", "ms_per_step": ms,
-            "frames_per_s": sum(x["lengths"].tolist()) / (ms * 1e-3)}
+    frames = sum(x["lengths"].tolist())
+    res = {"workload": "masked full attention fwd+bwd in PyTorch (float32 math on bf16 inputs), "
+                       "same batch", "ms_per_step": ms, "frames_per_s": frames / (ms * 1e-3)}
+    # torch's scaled_dot_product_attention with the boolean band mask (padded
+    # query rows keep their own frame so no row is empty; their output is
+    # zeroed). float32 operands: its bfloat16 paths are not used here.
+    sdpa_mask = mask | (t[None, :] == t[:, None])[None, None]
+
+    def sdpa_step():
+        qq, kk, vv = (a.float().detach().requires_grad_(True) for a in (q, k, v))
+        o = torch.nn.functional.scaled_dot_product_attention(qq, kk, vv, attn_mask=sdpa_mask)
+        o = torch.where(rows, o, torch.zeros_like(o))
+        o.backward(do.float())
+        return o
+
+    try:
+        for _ in range(2):
+            sdpa_step()
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(steps):
+            sdpa_step()
+        s1.record()
+        torch.cuda.synchronize()
+        sms = s0.elapsed_time(s1) / steps
+        res["sdpa_bool_mask"] = {"workload": "torch scaled_dot_product_attention fwd+bwd with a "
+                                             "boolean band attn_mask, float32, same batch",
+                                 "ms_per_step": sms, "frames_per_s": frames / (sms * 1e-3)}
+    except RuntimeError as e:
+        res["sdpa_bool_mask"] = {"error": str(e)[:200]}
+    return res
 
 
 MEMORY_EXPERIMENT = {"B": 4, "T": 1000, "d": 64, "heads": (8, 16), "La": 8,
@@ -631,30 +786,89 @@ def memory_experiment():
                           "B=%d, T=%d, d=%d, bf16 tensors" % (B, T, d), "rows": rows}
 
 
-def cpu_baseline(min_seconds=10.0):
-    """The fp64 oracle on the host cores: repeated passes of forward+backward
-    over the first sequences of the workload until ~10 s have elapsed."""
-    import oracle
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
-    w = WORKLOAD
-    x = sa_inputs(w["B"], w["T"], w["H"], w["d"], w["seed"], dtype="bf16", lengths=w["lengths"])
-    nseq = 4
-    q, k, v, do = (x[n][:nseq].double().numpy() for n in ("q", "k", "v", "dout"))
-    ln = x["lengths"][:nseq].numpy()
-    threads = min(os.cpu_count() or 1, 16)
-    oracle._load()
+
+def _timed_passes(fn, min_seconds):
     passes, t0 = 0, time.perf_counter()
     while True:
-        oracle.sa_forward(q, k, v, w["Lb"], w["La"], ln, threads=threads)
-        oracle.sa_backward(q, k, v, do, w["Lb"], w["La"], ln, threads=threads)
+        fn()
         passes += 1
         el = time.perf_counter() - t0
         if el >= min_seconds:
-            break
+            return passes, el
+
+
+def cpu_baseline(min_seconds=10.0):
+    """The fp64 oracle (plain C, OpenMP over (sequence, head)) on the host:
+    repeated forward+backward passes over the workload's sequences with every
+    core the process may run on, then on one core, then the other configs'
+    passes (short samples)."""
+    import oracle
+
+    oracle._load()
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    w = WORKLOAD
+    x = sa_inputs(w["B"], w["T"], w["H"], w["d"], w["seed"], dtype="bf16", lengths=w["lengths"])
+    q, k, v, do = (x[n].double().numpy() for n in ("q", "k", "v", "dout"))
+    ln = x["lengths"].numpy()
+
+    def step(nseq, threads):
+        oracle.sa_forward(q[:nseq], k[:nseq], v[:nseq], w["Lb"], w["La"], ln[:nseq],
+                          threads=threads)
+        oracle.sa_backward(q[:nseq], k[:nseq], v[:nseq], do[:nseq], w["Lb"], w["La"], ln[:nseq],
+                           threads=threads)
+
+    passes, el = _timed_passes(lambda: step(w["B"], cores), min_seconds)
     frames = int(ln.sum()) * passes
-    return {"value": frames / el, "unit": "frames/s", "cores": threads, "kind": "oracle",
-            "sample": "%d passes of forward+backward over the first %d sequences (%d frames, all "
-                      "12 heads) of the workload, %.1f s" % (passes, nseq, int(ln.sum()), el)}
+    res = {"value": frames / el, "unit": "frames/s", "cores": cores, "kind": "oracle",
+           "sample": "%d passes of forward+backward over the whole workload batch (16 sequences, "
+                     "%d frames, 12 heads), %.1f s" % (passes, int(ln.sum()), el),
+           "cpu_model": _cpu_model(), "host_cpus": os.cpu_count()}
+    p1, el1 = _timed_passes(lambda: step(1, 1), min_seconds / 4)
+    res["one_core"] = {"value": int(ln[0]) * p1 / el1, "unit": "frames/s", "cores": 1,
+                       "sample": "%d passes over the first sequence (%d frames), %.1f s"
+                                 % (p1, int(ln[0]), el1)}
+    # the other configurations, all cores, short samples
+    c = C2
+    y = sa_inputs(c["B"], c["T"], c["H"], c["d"], c["seed"], dtype="bf16", lengths=c["lengths"],
+                  with_dout=False)
+    yq, yk, yv = (y[n].double().numpy() for n in ("q", "k", "v"))
+    pc, elc = _timed_passes(lambda: oracle.sa_forward(yq, yk, yv, c["Lb"], c["La"], None,
+                                                      threads=cores), min_seconds / 4)
+    res["sa_forward_l32_r8"] = {"value": c["B"] * c["T"] * pc / elc, "unit": "frames/s",
+                                "cores": cores, "sample": "%d forward passes, B=8, T=500, %.1f s"
+                                                          % (pc, elc)}
+    z = llsa_inputs(w["B"], w["T"], w["H"], w["d"], 4, dtype="bf16", lengths=w["lengths"])
+    zq, zk, zv = (z[n].double().numpy() for n in ("q", "k", "v"))
+    zl = z["lengths"].numpy()
+    pl, ell = _timed_passes(lambda: oracle.llsa_two_branch(zq, zk, zv, w["Lb"], w["La"], zl,
+                                                           threads=cores), min_seconds / 4)
+    res["llsa_forward"] = {"value": int(zl.sum()) * pl / ell, "unit": "frames/s", "cores": cores,
+                           "sample": "%d passes of the two-branch forward over the LLSA batch, "
+                                     "%.1f s" % (pl, ell)}
+    st = STREAM
+    S, H, d, Lb, La = st["S"], st["H"], st["d"], st["Lb"], st["La"]
+    sx = stream_inputs(200, S, H, d, st["seed"], dtype="bf16")
+    so = oracle.StreamOracle(S, H, d, Lb, La, Lb + La + 1)
+    sq, sk, sv = (sx[n].double().numpy() for n in ("q", "k", "v"))
+    n_st, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < min_seconds / 4 and n_st < 200:
+        so.step(sq[n_st], sk[n_st], sv[n_st])
+        n_st += 1
+    els = time.perf_counter() - t0
+    res["stream_step"] = {"value": n_st / els, "unit": "steps/s", "cores": 1,
+                          "sample": "%d streaming steps of 64 streams (the oracle's ring "
+                                    "simulation runs on one core), %.1f s" % (n_st, els)}
+    return res
 
 
 def main():
@@ -675,17 +889,20 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: --gpus %d is not supported (the band kernels shard "
-              "over batch and heads with no communication; see the design notes)" % args.gpus,
-              file=sys.stderr)
+              "over batch and heads with no communication)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
+        # the library's device-copy reference, 512 MiB, five launches through
+        # registers, then five through direct global->LDS copies
+        bd.load_library()
         n = 512 << 20
-        src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
         dst = torch.empty_like(src)
-        for _ in range(5):
-            torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n}))
+        for mode in (0, 1):
+            for _ in range(5):
+                bd.copy_reference(src, dst, mode)
+            torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches_per_mode": 5}))
         return
     bd.load_library()
     if args.memory_experiment:
@@ -707,6 +924,7 @@ def main():
     dom_gbs = bwd_gbs if dominant == "sa_backward" else fwd_gbs
     dom_sha = source_sha("band_bwd.hip") if dominant == "sa_backward" else source_sha("band_fwd.hip")
     traffic_file = ("sa_bwd_traffic.json" if dominant == "sa_backward" else "sa_fwd_traffic.json")
+    sq_file = ("sa_bwd_sq_counters.json" if dominant == "sa_backward" else "sa_fwd_sq_counters.json")
     line = {
         "metric": "band-attention frames/s + TFLOP/s & HBM GB/s vs roofline (fwd+bwd)",
         "value": frames / step_s,
@@ -726,7 +944,8 @@ def main():
                    "La": w["La"], "valid_frames": frames, "input_sets_rotated": N_SETS},
         "roofline": {"bound": "hbm", "achieved": dom_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dom_gbs / HBM_PEAK_GBS, "kernel": dominant,
-                     "traffic": load_traffic(traffic_file, dom_sha)},
+                     "traffic": load_traffic(traffic_file, dom_sha),
+                     "mfma": load_mfma(sq_file, dom_sha)},
         "kernels": {
             "sa_forward": {"ms": r["fwd_ms"], "algorithmic_bytes": fwd_b, "gbs": fwd_gbs,
                            "hbm_frac": fwd_gbs / HBM_PEAK_GBS, "useful_flops": fwd_f,
@@ -738,15 +957,24 @@ def main():
         "useful_tflops_step": (fwd_f + bwd_f) / step_s / 1e12,
         "algorithmic_gbs_step": (fwd_b + bwd_b) / step_s / 1e9,
     }
+    log("device-copy reference (practical bandwidth ceiling)")
+    ceiling = copy_ceiling()
+    line["copy_ceiling"] = ceiling
+    line["roofline"]["copy_ceiling_gbs"] = ceiling["gbs"]
+    line["roofline"]["practical_frac"] = dom_gbs / ceiling["gbs"]
     if not args.no_extras:
+        log("SA forward at the l32_r8 window (B=8, T=500)")
+        line["sa_forward_l32_r8"] = bench_c2(args.steps, args.warmup)
         log("LLSA forward and backward")
         line["llsa_backward"], line["llsa"] = bench_llsa(max(20, args.steps // 2), 5)
         log("LLSA in the paper's channel form, forward and backward")
         line["llsa_paper"], line["llsa_paper_backward"] = bench_llsa_paper(20, 3)
+        log("launch floor")
+        floor = launch_floor()
         log("streaming step")
-        line["stream"] = bench_stream()
+        line["stream"] = bench_stream(floor)
         log("LLSA streaming step")
-        line["llsa_stream"] = bench_llsa_stream()
+        line["llsa_stream"] = bench_llsa_stream(floor)
         if not args.no_stack:
             log("12-layer streaming stack latency")
             line["stream_latency"] = bench_stream_latency()
