@@ -133,10 +133,14 @@ int llsa_forward(const void* q, const void* k, const void* v, void* out, float* 
  *
  * q, k, v : [La+1][B][T][H][d] inputs (channel-major)
  * out     : [La+1][B][T][H][d] outputs (padding frames written as 0)
- * lse     : float [La+1][B][H][T] (required; it holds the band part's
- *           log-sum-exp between the two passes; -inf on padding frames)
+ * lse     : float [La+1][B][H][T], natural-log log-sum-exp of every row
+ *           (required: llsa_paper_backward needs it; where the call runs as
+ *           a band pass and a merge, it also carries the band part's
+ *           log-sum-exp between them; -inf on padding frames)
  * La must not exceed SA_LLSA_PAPER_MAX_LA. Lb is clipped to T; La is not
- * (it fixes the channel count).
+ * (it fixes the channel count). bfloat16 with 1 <= La <= 15 and Lb < 80 runs
+ * in one pass; float32, La > 15 or Lb >= 80 run a band pass per channel and
+ * a merge.
  */
 int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, float* lse,
                        int B, int T, int H, int d, int Lb, int La,
@@ -155,10 +159,11 @@ int llsa_paper_forward(const void* q, const void* k, const void* v, void* out, f
  * q, k, v, out, dout : [La+1][B][T][H][d] inputs; out is llsa_paper_forward's
  * lse                : float [La+1][B][H][T] from llsa_paper_forward (required)
  * dq, dk, dv         : [La+1][B][T][H][d] outputs (padding frames written as 0)
- * Supported: dtype SA_BF16, La <= SA_LLSA_PAPER_MAX_LA, and Lb + La <= 64
- * (208 at d = 32), or Lb + La <= 80 when La <= 15 at d = 64; other windows
- * return SA_ERR_UNSUPPORTED. La = 0 is the SA backward with the window
- * t-Lb .. t.
+ * Every window with La <= SA_LLSA_PAPER_MAX_LA and both element types. With
+ * SA_BF16 and a window whose band fits one staged segment (Lb + La <= 64, or
+ * <= 208 at d = 32, or Lb + La <= 80 when La <= 15 at d = 64) it runs an MFMA
+ * band pass and diagonal pass; otherwise one vector-ALU pass. La = 0 is the
+ * SA backward with the window t-Lb .. t.
  */
 int llsa_paper_backward(const void* q, const void* k, const void* v, const void* out,
                         const float* lse, const void* dout, void* dq, void* dk, void* dv,
@@ -180,9 +185,12 @@ int llsa_paper_backward(const void* q, const void* k, const void* v, const void*
  * q, k, v, out, dout : [2][B][T][H][d] inputs; out is llsa_forward's output
  * lse                : float [2][B][H][T] from llsa_forward (required)
  * dq, dk, dv         : [2][B][T][H][d] outputs (padding frames written as 0)
- * Supported: dtype SA_BF16, and windows whose bands fit one staged segment:
- * every Lb + La <= 40 (104 at d = 32), and Lb + La <= 80 (208 at d = 32)
- * when La <= 15. Other cases return SA_ERR_UNSUPPORTED.
+ * Every window and both element types. With SA_BF16 and windows whose bands
+ * fit one staged segment it runs on MFMA (one workgroup per 64-frame tile);
+ * other windows and SA_F32 run one vector-ALU pass. The staged windows are
+ * those where every (output, branch) segment's sweep fits 144 rows at d = 64
+ * (288 at d = 32): for example Lb + La <= 40 for any La, Lb = 32 with
+ * La = 16, and Lb + La <= 80 with La <= 15; Lb = 64 with La = 16 is not.
  */
 int llsa_backward(const void* q, const void* k, const void* v, const void* out,
                   const float* lse, const void* dout, void* dq, void* dk, void* dv,

@@ -1661,9 +1661,10 @@ bool llsa_backward_fits(int d, int Lb, int La) {
 }
 
 hipError_t launch_llsa_backward(const LlsaBackwardArgs& x, ElemType et, hipStream_t stream) {
-  if (et != kBF16) return hipErrorNotSupported;
   LlsaBwdDev a{};
-  if (!llsa_bwd_geometry(x.d, x.Lb, x.La, a)) return hipErrorNotSupported;
+  // bfloat16 windows whose bands fit one staged segment run on MFMA, the rest
+  // on the vector ALUs
+  if (et != kBF16 || !llsa_bwd_geometry(x.d, x.Lb, x.La, a)) return launch_llsa_backward_general(x, et, stream);
   const size_t branch = static_cast<size_t>(x.B) * x.T * x.H * x.d;
   for (int j = 0; j < 2; ++j) {
     a.q[j] = static_cast<const uint16_t*>(x.q) + j * branch;

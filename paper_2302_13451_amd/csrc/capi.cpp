@@ -232,15 +232,12 @@ int llsa_paper_backward(const void* q, const void* k, const void* v, const void*
   if (int rc = check_shape(fn, B, T, H, d, Lb, La, dtype)) return rc;
   if (La > SA_LLSA_PAPER_MAX_LA)
     return fail(SA_ERR_INVALID, "%s: La = %d exceeds %d", fn, La, SA_LLSA_PAPER_MAX_LA);
-  if (dtype != SA_BF16) return fail(SA_ERR_UNSUPPORTED, "%s: only bfloat16 is supported", fn);
   if (B == 0 || T == 0 || H == 0) return SA_OK;
   if (!lse) return fail(SA_ERR_NULL, "%s: lse (from llsa_paper_forward) is required", fn);
   if (int rc = check_ptrs(fn, {q, k, v, out, dout, dq, dk, dv}, {lse}, {lengths})) return rc;
   if (static_cast<long long>(2 * La + 1) * B * (T + La) * H > (1LL << 31) - 1)
     return fail(SA_ERR_INVALID, "%s: (2La+1)*B*(T+La)*H exceeds 2^31-1", fn);
   Lb = Lb < T ? Lb : T;
-  if (La > 0 && !sa::llsa_paper_backward_fits(d, Lb, La))
-    return fail(SA_ERR_UNSUPPORTED, "%s: window Lb = %d, La = %d too wide for d = %d", fn, Lb, La, d);
   sa::LlsaPaperBwdArgs a{};
   a.q = q;
   a.k = k;
@@ -267,14 +264,11 @@ int llsa_backward(const void* q, const void* k, const void* v, const void* out, 
                   int La, const int32_t* lengths, int dtype, void* stream) {
   const char* fn = "llsa_backward";
   if (int rc = check_shape(fn, B, T, H, d, Lb, La, dtype)) return rc;
-  if (dtype != SA_BF16) return fail(SA_ERR_UNSUPPORTED, "%s: only bfloat16 is supported", fn);
   if (B == 0 || T == 0 || H == 0) return SA_OK;
   if (!lse) return fail(SA_ERR_NULL, "%s: lse (from llsa_forward) is required", fn);
   if (int rc = check_ptrs(fn, {q, k, v, out, dout, dq, dk, dv}, {lse}, {lengths})) return rc;
   Lb = Lb < T ? Lb : T;
   La = La < T ? La : T;
-  if (!sa::llsa_backward_fits(d, Lb, La))
-    return fail(SA_ERR_UNSUPPORTED, "%s: window Lb = %d, La = %d too wide for d = %d", fn, Lb, La, d);
   sa::LlsaBackwardArgs a{};
   a.q = q;
   a.k = k;

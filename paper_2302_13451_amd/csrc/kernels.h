@@ -70,6 +70,8 @@ hipError_t launch_llsa_paper_backward_band(const LlsaPaperBwdArgs& a, hipStream_
 bool llsa_paper_backward_fits(int d, int Lb, int La);
 // The whole backward: the band part, then the diagonal frames' part.
 hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& a, ElemType et, hipStream_t stream);
+// Any window and either element type, on the vector ALUs (llsa_bwd_general.hip).
+hipError_t launch_llsa_paper_backward_general(const LlsaPaperBwdArgs& a, ElemType et, hipStream_t stream);
 
 struct SaBackwardArgs {
   const void *q, *k, *v, *out, *dout;
@@ -92,6 +94,8 @@ struct LlsaBackwardArgs {
 };
 
 hipError_t launch_llsa_backward(const LlsaBackwardArgs& a, ElemType et, hipStream_t stream);
+// Any window and either element type, on the vector ALUs (llsa_bwd_general.hip).
+hipError_t launch_llsa_backward_general(const LlsaBackwardArgs& a, ElemType et, hipStream_t stream);
 
 // Whether launch_llsa_backward supports the window (its bands must fit the
 // staged segment).

@@ -2,11 +2,17 @@
 // of Fig. 4): output channel c of frame t reads the window t+c-La-Lb .. t+c,
 // frame tau coming from channel min(La, t+c-tau). The window splits into
 //   * a band from channel La: tau in t+c-La-Lb .. t+c-La, an SA-type window
-//     segment, computed by the band forward (with its log-sum-exp);
+//     segment;
 //   * La single frames tau = t+c-c' from channels c' = 0 .. La-1 (one per
-//     channel, on a diagonal), computed here on the vector ALUs and merged
-//     with the band's normalised output through the two log-sum-exps.
-// Rows t >= len are the band forward's (zero output, lse = -inf).
+//     channel, on a diagonal).
+// bfloat16 with 1 <= La <= 15 and Lb < 80 runs one pass
+// (llsa_paper_fwd_fused_kernel): the queries (c, s - c) of an anti-diagonal
+// group s share one band, so a group is one dense block under one softmax,
+// and the final lse is written directly. Otherwise (float32, La > 15 or
+// Lb >= 80) the band forward computes each channel's band part with its
+// log-sum-exp, and a merge pass adds the diagonal frames (on MFMA for
+// La <= 15, on the vector ALUs beyond) and joins the two parts through their
+// log-sum-exps. Rows t >= len get zero output and lse = -inf.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -672,12 +678,15 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kern
 }  // namespace
 
 hipError_t launch_llsa_paper_backward(const LlsaPaperBwdArgs& x, ElemType et, hipStream_t stream) {
-  if (et != kBF16) return hipErrorNotSupported;
   if (x.La == 0) {  // one channel: SA with the window t - Lb .. t
     const SaBackwardArgs s{x.q, x.k, x.v, x.out, x.dout, x.lse, x.dq, x.dk, x.dv,
                            x.B, x.T, x.H, x.d, x.Lb, 0, x.lengths};
     return launch_sa_backward(s, et, stream);
   }
+  // bfloat16 windows that the band pass stages in one segment: band pass and
+  // diagonal pass on MFMA; the rest on the vector ALUs
+  if (et != kBF16 || !llsa_paper_backward_fits(x.d, x.Lb, x.La))
+    return launch_llsa_paper_backward_general(x, et, stream);
   hipError_t e = launch_llsa_paper_backward_band(x, stream);
   if (e != hipSuccess) return e;
   PaperDiagDev m{};

@@ -102,8 +102,8 @@ int main() {
          SA_ERR_INVALID);
   expect("paper fwd NULL lse", llsa_paper_forward(F, F, F, F, nullptr, 2, 8, 2, 64, 2, 3, nullptr, SA_BF16, nullptr),
          SA_ERR_NULL);
-  expect("paper bwd f32",
-         llsa_paper_backward(F, F, F, F, L, F, F, F, F, 2, 8, 2, 64, 2, 3, nullptr, SA_F32, nullptr),
+  expect("paper bwd dtype 5",
+         llsa_paper_backward(F, F, F, F, L, F, F, F, F, 2, 8, 2, 64, 2, 3, nullptr, 5, nullptr),
          SA_ERR_UNSUPPORTED);
   expect("paper bwd NULL dk",
          llsa_paper_backward(F, F, F, F, L, F, F, nullptr, F, 2, 8, 2, 64, 2, 3, nullptr, SA_BF16, nullptr),
@@ -163,10 +163,15 @@ int main() {
                                                SA_BF16, nullptr),
              SA_ERR_HIP);
     }
-    expect("llsa bwd dispatch",
-           llsa_backward(F, F, F, F, L, F, F, F, F, 3, 300, 2, 64, 30, 8, W, SA_BF16, nullptr), SA_ERR_HIP);
-    expect("paper bwd dispatch",
-           llsa_paper_backward(F, F, F, F, L, F, F, F, F, 3, 300, 2, 64, 30, 8, W, SA_BF16, nullptr), SA_ERR_HIP);
+    for (const auto& c : wd) {
+      for (int dt : {SA_BF16, SA_F32}) {
+        expect("llsa bwd dispatch",
+               llsa_backward(F, F, F, F, L, F, F, F, F, 3, 300, 2, c[0], c[1], c[2], W, dt, nullptr), SA_ERR_HIP);
+        expect("paper bwd dispatch",
+               llsa_paper_backward(F, F, F, F, L, F, F, F, F, 3, 300, 2, c[0], c[1], c[2], W, dt, nullptr),
+               c[2] > SA_LLSA_PAPER_MAX_LA ? SA_ERR_INVALID : SA_ERR_HIP);
+      }
+    }
     expect("copy dispatch", sa_copy_reference(F, G, 4096, 1, nullptr), SA_ERR_HIP);
   }
 

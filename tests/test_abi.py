@@ -95,10 +95,9 @@ def test_llsa_backward_validation(lib):
     assert lb(dv=FAKE_ODD) == bd.SA_ERR_INVALID
     assert lb(La=-1) == bd.SA_ERR_INVALID
     assert lb(d=16) == bd.SA_ERR_UNSUPPORTED
-    assert lb(dtype=bd.SA_F32) == bd.SA_ERR_UNSUPPORTED       # bfloat16 only
-    assert lib.llsa_backward(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 200, 2, 64,
-                             70, 20, None, bd.SA_BF16, None) == bd.SA_ERR_UNSUPPORTED  # window too wide
-    assert "too wide" in lib.sa_last_error().decode()
+    assert lb(dtype=7) == bd.SA_ERR_UNSUPPORTED
+    # float32 and every window are supported: those calls reach a launch, so
+    # they are exercised by the GPU tests, not here
 
 
 def test_llsa_paper_forward_validation(lib):
@@ -126,9 +125,7 @@ def test_llsa_paper_backward_validation(lib):
     assert lb(dv=FAKE_ODD) == bd.SA_ERR_INVALID
     assert lb(La=65) == bd.SA_ERR_INVALID
     assert lb(d=16) == bd.SA_ERR_UNSUPPORTED
-    assert lb(dtype=bd.SA_F32) == bd.SA_ERR_UNSUPPORTED       # bfloat16 only
-    assert lb(T=200, Lb=70, La=20) == bd.SA_ERR_UNSUPPORTED   # window too wide
-    assert "too wide" in lib.sa_last_error().decode()
+    assert lb(dtype=7) == bd.SA_ERR_UNSUPPORTED
 
 
 def test_stream_validation(lib):

@@ -16,23 +16,23 @@ import torch
 
 from paper_2302_13451_amd import binding as bd
 from paper_2302_13451_amd.inputs import llsa_inputs
-from parity import assert_close, assert_slices_close, f64, round_to, to_gpu
+from parity import TORCH_DTYPE, assert_close, assert_slices_close, f64, round_to, to_gpu
 
 pytestmark = pytest.mark.gpu
 
 
-def _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, tag):
-    print("llsa backward %s case B=%d T=%d H=%d d=%d Lb=%d La=%d seed=%d" % (
-        tag, B, T, H, d, Lb, La, seed), flush=True)
-    x = llsa_inputs(B, T, H, d, seed, dtype="bf16", scale=scale, lengths=lengths, pad_value=pad,
+def _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, tag, dtype="bf16"):
+    print("llsa backward %s case B=%d T=%d H=%d d=%d Lb=%d La=%d %s seed=%d" % (
+        tag, B, T, H, d, Lb, La, dtype, seed), flush=True)
+    x = llsa_inputs(B, T, H, d, seed, dtype=dtype, scale=scale, lengths=lengths, pad_value=pad,
                     with_dout=True)
-    g = {n: to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout")}
+    g = {n: to_gpu(x[n], dtype) for n in ("q", "k", "v", "dout")}
     clean = {n: np.nan_to_num(f64(x[n])) for n in ("q", "k", "v", "dout")}
     return x, g, clean
 
 
-def run(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
-    x, g, clean = _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, "end-to-end")
+def run(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0, dtype="bf16"):
+    x, g, clean = _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, "end-to-end", dtype)
     ln = x["lengths"].cuda()
     out, lse = bd.llsa_forward(g["q"], g["k"], g["v"], Lb, La, ln)
     dq, dk, dv = bd.llsa_backward(g["q"], g["k"], g["v"], out, lse, g["dout"], Lb, La, ln)
@@ -42,12 +42,13 @@ def run(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0)
     return (f64(dq), f64(dk), f64(dv)), ref, x["lengths"].tolist()
 
 
-def run_supplied(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
-    x, g, clean = _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, "supplied-output")
+def run_supplied(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0,
+                 dtype="bf16"):
+    x, g, clean = _inputs(B, T, H, d, Lb, La, seed, lengths, scale, pad, "supplied-output", dtype)
     L = x["lengths"].numpy()
     y, lse = oracle_mod.llsa_two_branch(clean["q"], clean["k"], clean["v"], Lb, La, L)
-    y = round_to(y, "bf16")
-    out = torch.from_numpy(y).to(torch.bfloat16).cuda()
+    y = round_to(y, dtype)
+    out = torch.from_numpy(y).to(TORCH_DTYPE[dtype]).cuda()
     dq, dk, dv = bd.llsa_backward(g["q"], g["k"], g["v"], out, torch.from_numpy(lse).float().cuda(),
                                   g["dout"], Lb, La, x["lengths"].cuda())
     torch.cuda.synchronize()
@@ -60,13 +61,16 @@ def _zero_atol(ref):
     return 1e-5 * float(np.max(np.abs(ref[2])))
 
 
-def check_slices(got, ref, lengths, elementwise=True):
+def check_slices(got, ref, lengths, elementwise=True, dtype="bf16"):
     for name, g, r in zip(("dq", "dk", "dv"), got, ref):
-        assert_slices_close(g, r, "bf16", lengths, name, elementwise=elementwise,
-                            zero_atol=_zero_atol(ref), row_scale=True)
+        assert_slices_close(g, r, dtype, lengths, name, elementwise=elementwise,
+                            zero_atol=_zero_atol(ref), row_scale=dtype == "bf16")
 
 
-def check_end_to_end(got, ref):
+def check_end_to_end(got, ref, lengths=None, dtype="bf16"):
+    if dtype == "f32":
+        check_slices(got, ref, lengths, dtype="f32")
+        return
     for name, g, r in zip(("dq", "dk", "dv"), got, ref):
         for br, bname in ((0, "causal"), (1, "look-ahead")):
             assert_close(g[br], r[br], "bf16", "%s %s" % (name, bname), elementwise=False,
@@ -115,14 +119,26 @@ def test_config4_backward_full_size(oracle_mod):
     check_end_to_end(got, ref)
 
 
-def test_llsa_backward_rejects_unsupported():
-    x = llsa_inputs(1, 64, 1, 64, 53, dtype="bf16", with_dout=True)
-    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
-    out, lse = bd.llsa_forward(q, k, v, 70, 20)
-    with pytest.raises(bd.SAError) as e:
-        bd.llsa_backward(q, k, v, out, lse, do, 70, 20)
-    assert e.value.status == bd.SA_ERR_UNSUPPORTED
-    qf, kf, vf, dof, of = (t.float() for t in (q, k, v, do, out))
-    with pytest.raises(bd.SAError) as e:
-        bd.llsa_backward(qf, kf, vf, of, lse, dof, 8, 2)
-    assert e.value.status == bd.SA_ERR_UNSUPPORTED
+# Windows past one staged segment (the vector-ALU kernel) and float32, and
+# the staged-window boundary from both sides: Lb = 32, La = 16 still stages
+# (MFMA tile kernel); Lb = 64, La = 16 does not.
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
+    (2, 200, 2, 64, 70, 20, (60, 200)),
+    (2, 190, 2, 64, 32, 16, (60, 190)),
+    (2, 190, 2, 64, 64, 16, (60, 190)),
+    (2, 150, 1, 32, 120, 30, (40, 150)),
+    (3, 90, 2, 64, 5, 0, (0, 90, 17)),
+    (66, 40, 1, 64, 8, 3, (0, 40)),
+])
+def test_llsa_backward_every_window(oracle_mod, dtype, B, T, H, d, Lb, La, lengths):
+    got, ref, L = run_supplied(oracle_mod, B, T, H, d, Lb, La, 56, lengths, "unit", dtype=dtype)
+    check_slices(got, ref, L, dtype=dtype)
+    got, ref, L = run(oracle_mod, B, T, H, d, Lb, La, 56, lengths, "unit", dtype=dtype)
+    check_end_to_end(got, ref, L, dtype)
+
+
+def test_llsa_backward_float32_config4_shape(oracle_mod):
+    """float32 at the LLSA workload's window, B=4, T=800, H=12, d=64, Lb=64, La=8."""
+    got, ref, L = run_supplied(oracle_mod, 4, 800, 12, 64, 64, 8, 57, (400, 800), dtype="f32")
+    check_slices(got, ref, L, dtype="f32")

@@ -126,20 +126,21 @@ def test_llsa_paper_rejects_bad_arguments():
 # tensor normwise (the rounding of `out` to bfloat16 alone moves a slice of dq
 # by about 2e-2 of its maximum).
 def run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0,
-            supplied=False):
-    print("llsa paper backward %s case B=%d T=%d H=%d d=%d Lb=%d La=%d seed=%d" % (
-        "supplied-output" if supplied else "end-to-end", B, T, H, d, Lb, La, seed), flush=True)
-    x = llsa_inputs(B, T, H, d, seed, dtype="bf16", scale=scale, lengths=lengths, pad_value=pad,
+            supplied=False, dtype="bf16"):
+    print("llsa paper backward %s case B=%d T=%d H=%d d=%d Lb=%d La=%d %s seed=%d" % (
+        "supplied-output" if supplied else "end-to-end", B, T, H, d, Lb, La, dtype, seed),
+        flush=True)
+    x = llsa_inputs(B, T, H, d, seed, dtype=dtype, scale=scale, lengths=lengths, pad_value=pad,
                     with_dout=True, channels=La + 1)
-    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
+    q, k, v, do = (to_gpu(x[n], dtype) for n in ("q", "k", "v", "dout"))
     ln = x["lengths"].cuda()
     clean = {n: np.nan_to_num(f64(x[n])) for n in ("q", "k", "v", "dout")}
     L = x["lengths"].numpy()
     y = None
     if supplied:
         y, lse = oracle_mod.llsa_paper(clean["q"], clean["k"], clean["v"], Lb, La, L)
-        y = round_to(y, "bf16")
-        out, lse = torch.from_numpy(y).to(torch.bfloat16).cuda(), torch.from_numpy(lse).float().cuda()
+        y = round_to(y, dtype)
+        out, lse = torch.from_numpy(y).to(q.dtype).cuda(), torch.from_numpy(lse).float().cuda()
     else:
         out, lse = bd.llsa_paper_forward(q, k, v, Lb, La, ln)
     dq, dk, dv = bd.llsa_paper_backward(q, k, v, out, lse, do, Lb, La, ln)
@@ -149,25 +150,27 @@ def run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=
     return (f64(dq), f64(dk), f64(dv)), ref, x["lengths"].tolist()
 
 
-def check_bwd(got, ref, lengths, mode="supplied"):
+def check_bwd(got, ref, lengths, mode="supplied", dtype="bf16"):
     """mode: "supplied" (per slice and element) or "tensors" (per channel
-    tensor)."""
+    tensor; float32 end to end is held per slice and element too)."""
     zero_atol = 1e-5 * float(np.max(np.abs(ref[2])))
     for name, g, r in zip(("dq", "dk", "dv"), got, ref):
-        if mode == "tensors":
+        if mode == "tensors" and dtype == "bf16":
             for c in range(g.shape[0]):
                 assert_close(g[c], r[c], "bf16", "%s channel %d" % (name, c), elementwise=False,
                              zero_atol=zero_atol)
         else:
-            assert_slices_close(g, r, "bf16", lengths, name, zero_atol=zero_atol,
-                                row_scale=True)
+            assert_slices_close(g, r, dtype, lengths, name, zero_atol=zero_atol,
+                                row_scale=dtype == "bf16")
 
 
-def run_check_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0):
-    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad, supplied=True)
-    check_bwd(got, ref, L, "supplied")
-    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad)
-    check_bwd(got, ref, L, "tensors")
+def run_check_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d", pad=0.0,
+                  dtype="bf16"):
+    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad, supplied=True,
+                          dtype=dtype)
+    check_bwd(got, ref, L, "supplied", dtype)
+    got, ref, L = run_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale, pad, dtype=dtype)
+    check_bwd(got, ref, L, "tensors", dtype)
     return got, L
 
 
@@ -218,9 +221,15 @@ def test_llsa_paper_backward_one_channel_is_sa_backward():
         assert torch.equal(g[0], r)
 
 
-def test_llsa_paper_backward_rejects_unsupported_windows():
-    x = llsa_inputs(1, 200, 1, 64, 55, dtype="bf16", with_dout=True, channels=21)
-    q, k, v, do = (to_gpu(x[n], "bf16") for n in ("q", "k", "v", "dout"))
-    out, lse = bd.llsa_paper_forward(q, k, v, 70, 20)
-    with pytest.raises(bd.SAError):
-        bd.llsa_paper_backward(q, k, v, out, lse, do, 70, 20)
+# Windows the band pass cannot stage (the vector-ALU kernel), float32, and
+# the staged-window boundary: Lb + La = 64 stages, 65 with La = 16 does not.
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
+    (1, 200, 1, 64, 70, 20, "full"),
+    (2, 130, 2, 64, 48, 16, (40, 130)),
+    (2, 130, 2, 64, 49, 16, (40, 130)),
+    (2, 120, 1, 32, 150, 40, (50, 120)),
+    (2, 100, 2, 64, 20, 3, (0, 100)),
+])
+def test_llsa_paper_backward_every_window(oracle_mod, dtype, B, T, H, d, Lb, La, lengths):
+    run_check_bwd(oracle_mod, B, T, H, d, Lb, La, 58, lengths, "unit", dtype=dtype)
