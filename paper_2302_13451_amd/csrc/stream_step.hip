@@ -4,15 +4,13 @@
 // Lb + La + 1 keys: a matrix-vector shape, so it runs on the vector ALUs. One
 // workgroup serves one stream (the stream's step counter is read by every wave
 // and advanced once, after a workgroup barrier, so no other workgroup can see
-// it half-way); each wave takes one head (more in turn when H > 16). Per head a
+// it half-way); each wave takes one head (more in turn when H > 12). Per head a
 // wave
 //   1. stores the new frame in the rings (slot u mod (La+1) for the query,
 //      u mod R for key and value), one 16-byte chunk per lane;
-//   2. if frame t = u - La is due, scores its window with one key per lane
-//      (whole 16-byte chunks of the key row), reduces max and sum across the
-//      wave, and accumulates the output with each lane owning one 16-byte
-//      chunk of the head dim for every 64/chunks-th key, followed by a short
-//      cross-lane sum.
+//   2. if frame t = u - La is due, attends over its window (attend_rows):
+//      groups of lanes read whole key and value rows, one 16-byte chunk per
+//      lane, so every load is coalesced; the scores stay in registers.
 // The just-arrived frame u is taken from the input rather than from the ring
 // slot written in this same launch, so the kernel never reads its own stores.
 #include "device_common.h"
@@ -23,15 +21,14 @@
 namespace sa {
 namespace {
 
-constexpr int kMaxWaves = 16;
-// waves of the LLSA step (its per-lane state allows three per SIMD)
-constexpr int kLlsaWaves = 12;
-// LDS floats per wave of the LLSA step: one query row, two score slots per
-// window frame, rounded up so every wave's query starts 16-byte aligned
-template <int D>
-__host__ __device__ constexpr int llsa_wave_floats(int wmax) {
-  return D + (2 * wmax + 3) / 4 * 4;
-}
+// waves of the SA and LLSA steps (one head each, more in turn; their state
+// allows three per SIMD)
+constexpr int kMaxWaves = 12;
+// row groups per block of attend_rows: the SA step takes windows of up to 10
+// (80 frames at d = 64 in bfloat16, 160 at d = 32) in one block; the LLSA
+// step, with two queries' scores in registers, blocks of 5
+constexpr int kRowGroups = 10;
+constexpr int kRowGroups2 = 5;
 
 template <typename E>
 __device__ __forceinline__ void unpack16(const uint4& x, float* f);
@@ -69,12 +66,6 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
-
 struct DevStream {
   const void *q, *k, *v;
   void* out;
@@ -83,179 +74,120 @@ struct DevStream {
   int32_t* step;
   int32_t* emitted;
   int S, H, Lb, La;
-  int wmax;  // Lb + La + 1: score slots per wave
   const int32_t* lengths;
   float scale_log2;
 };
 
-// Attention of one query row (one head) over the W frames lo .. lo + W - 1 by
-// one wave: krow(tau) and vrow(tau) give frame tau's key and value rows, wts
-// holds the wave's W score slots, orow receives the output row.
-template <typename E, int D, typename KRow, typename VRow>
-__device__ __forceinline__ void attend_wave(const E* qrow, KRow krow, VRow vrow, int lo, int W, float scale_log2,
-                                            float* wts, E* orow, int lane) {
+// Attention of NQ query rows (one head, NQ = 1 or 2) over the same W frames
+// lo .. lo + W - 1 by one wave, with every memory access coalesced: lane
+// (kg, dc) takes 16-byte chunk dc of key and value rows kg, kg + NKG, ..., so
+// each load instruction reads NKG whole rows. The window is taken in blocks of
+// NV row groups (one block for windows up to NV * NKG frames); per block the
+// key (and, with one query, value) chunks are loaded before any arithmetic,
+// the score of row j is summed over the CH lanes of its group and stays in
+// them, and those lanes weight their value chunks with it: no score goes
+// through LDS. Across blocks the softmax runs online (running maximum, sum and
+// weighted sum rescaled when the maximum grows). qs[n] is query n's row (null
+// when it is not due), o[n] its output row (zero when not due).
+template <typename E, int D, int NV, int NQ, typename KRow, typename VRow>
+__device__ __forceinline__ void attend_rows(const E* const* qs, KRow krow, VRow vrow, int lo, int W,
+                                            float scale_log2, E* const* o, int lane) {
   constexpr int EPC = 16 / sizeof(E);
-  constexpr int CH = D / EPC;
-  constexpr int NKG = 64 / CH;
+  constexpr int CH = D / EPC;     // chunks per row: lanes per row group
+  constexpr int NKG = 64 / CH;    // row groups per wave
   auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
-  float qv[D];
-#pragma unroll
-  for (int c = 0; c < CH; ++c) unpack16<E>(chunk(qrow, c), qv + c * EPC);
-
-  // scores: one key per lane
-  float mloc = kNegInf;
-  for (int j = lane; j < W; j += 64) {
-    const E* kr = krow(lo + j);
-    float z = 0.f;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      float kf[EPC];
-      unpack16<E>(chunk(kr, c), kf);
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) z += qv[c * EPC + e] * kf[e];
-    }
-    z *= scale_log2;
-    wts[j] = z;
-    mloc = fmaxf(mloc, z);
-  }
-  const float m = wave_max(mloc);
-  float lpart = 0.f;
-  for (int j = lane; j < W; j += 64) {
-    const float pw = fast_exp2(wts[j] - m);
-    wts[j] = pw;
-    lpart += pw;
-  }
-  const float inv = 1.f / wave_sum(lpart);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  // weighted sum: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
   const int dc = lane % CH, kg = lane / CH;
-  float acc[EPC];
+  float qf[NQ][EPC];
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-  for (int j = kg; j < W; j += NKG) {
-    float vf[EPC];
-    unpack16<E>(chunk(vrow(lo + j), dc), vf);
-    const float pw = wts[j];
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) acc[e] += pw * vf[e];
-  }
-#pragma unroll
-  for (int o = CH; o < 64; o <<= 1)
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) acc[e] += __shfl_xor(acc[e], o);
-  if (kg == 0) *reinterpret_cast<uint4*>(orow + dc * EPC) = pack16<E>(acc, inv);
-  // the next head reuses wts: finish these reads first
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Two query rows (one head) over the same W frames in one pass: each key and
-// value row is read once for both. on0 / on1 select the queries that are due.
-// Query 0 is held in registers, query 1 in the wave's LDS slots qs (D floats,
-// 16-byte aligned, read as broadcasts); wts holds 2W score slots (the first W
-// for query 0).
-template <typename E, int D, typename KRow, typename VRow>
-__device__ __forceinline__ void attend_wave2(const E* q0, const E* q1, bool on0, bool on1, KRow krow, VRow vrow,
-                                             int lo, int W, float scale_log2, float* qs, float* wts, E* o0, E* o1,
-                                             int lane) {
-  constexpr int EPC = 16 / sizeof(E);
-  constexpr int CH = D / EPC;
-  constexpr int NKG = 64 / CH;
-  auto chunk = [](const E* row, int c) { return *reinterpret_cast<const uint4*>(row + c * EPC); };
-  float qa[D];
-#pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    if (on0) unpack16<E>(chunk(q0, c), qa + c * EPC);
+  for (int n = 0; n < NQ; ++n) {
+    if (qs[n]) unpack16<E>(chunk(qs[n], dc), qf[n]);
     else
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) qa[c * EPC + e] = 0.f;
+      for (int e = 0; e < EPC; ++e) qf[n][e] = 0.f;
   }
-  if (lane < CH) {  // query 1 into LDS, one 16-byte chunk per lane
-    float f[EPC];
-    if (on1) unpack16<E>(chunk(q1, lane), f);
-    else
+  float m[NQ], l[NQ], acc[NQ][EPC];
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) f[e] = 0.f;
+  for (int n = 0; n < NQ; ++n) {
+    m[n] = kNegInf;
+    l[n] = 0.f;
 #pragma unroll
-    for (int e = 0; e < EPC; e += 4)
-      *reinterpret_cast<f32x4*>(qs + lane * EPC + e) = f32x4{f[e], f[e + 1], f[e + 2], f[e + 3]};
+    for (int e = 0; e < EPC; ++e) acc[n][e] = 0.f;
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  // scores: one key per lane, both queries
-  float m0 = kNegInf, m1 = kNegInf;
-  for (int j = lane; j < W; j += 64) {
-    const E* kr = krow(lo + j);
-    float z0 = 0.f, z1 = 0.f;
+  for (int j0 = 0; j0 < W; j0 += NV * NKG) {
+    // key chunks, and with one query the value chunks too, before any
+    // arithmetic (two queries need the registers for their scores: their
+    // value chunks follow the scores)
+    uint4 kc[NV], vc[NV];
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
+    for (int i = 0; i < NV; ++i) {
+      const int j = j0 + kg + NKG * i;
+      const bool in = j < W;
+      kc[i] = in ? chunk(krow(lo + j), dc) : make_uint4(0, 0, 0, 0);
+      if constexpr (NQ == 1) vc[i] = in ? chunk(vrow(lo + j), dc) : make_uint4(0, 0, 0, 0);
+    }
+    float z[NQ][NV], bm[NQ];
+#pragma unroll
+    for (int n = 0; n < NQ; ++n) bm[n] = kNegInf;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
       float kf[EPC];
-      unpack16<E>(chunk(kr, c), kf);
+      unpack16<E>(kc[i], kf);
+      const bool in = j0 + kg + NKG * i < W;
 #pragma unroll
-      for (int e = 0; e < EPC; e += 4) {
-        const f32x4 qb = *reinterpret_cast<const f32x4*>(qs + c * EPC + e);
+      for (int n = 0; n < NQ; ++n) {
+        float p = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          z0 += qa[c * EPC + e + i] * kf[e + i];
-          z1 += qb[i] * kf[e + i];
-        }
+        for (int e = 0; e < EPC; ++e) p += qf[n][e] * kf[e];
+#pragma unroll
+        for (int x = 1; x < CH; x <<= 1) p += __shfl_xor(p, x);  // the row's CH chunks
+        z[n][i] = in ? p * scale_log2 : kNegInf;
+        bm[n] = fmaxf(bm[n], z[n][i]);
       }
     }
-    z0 *= scale_log2;
-    z1 *= scale_log2;
-    wts[j] = z0;
-    wts[W + j] = z1;
-    m0 = fmaxf(m0, z0);
-    m1 = fmaxf(m1, z1);
-  }
-  m0 = wave_max(m0);
-  m1 = wave_max(m1);
-  float l0 = 0.f, l1 = 0.f;
-  for (int j = lane; j < W; j += 64) {
-    const float p0 = fast_exp2(wts[j] - m0), p1 = fast_exp2(wts[W + j] - m1);
-    wts[j] = p0;
-    wts[W + j] = p1;
-    l0 += p0;
-    l1 += p1;
-  }
-  const float inv0 = 1.f / wave_sum(l0), inv1 = 1.f / wave_sum(l1);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  // weighted sums: lane (key group kg, chunk dc) covers keys kg, kg + NKG, ...
-  const int dc = lane % CH, kg = lane / CH;
-  float a0[EPC], a1[EPC];
+    if constexpr (NQ > 1) {
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) a0[e] = a1[e] = 0.f;
-  for (int j = kg; j < W; j += NKG) {
-    float vf[EPC];
-    unpack16<E>(chunk(vrow(lo + j), dc), vf);
-    const float p0 = wts[j], p1 = wts[W + j];
+      for (int i = 0; i < NV; ++i) {
+        const int j = j0 + kg + NKG * i;
+        vc[i] = j < W ? chunk(vrow(lo + j), dc) : make_uint4(0, 0, 0, 0);
+      }
+    }
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-      a0[e] += p0 * vf[e];
-      a1[e] += p1 * vf[e];
+    for (int n = 0; n < NQ; ++n) {
+      const float mn = fmaxf(m[n], wave_max(bm[n]));  // finite: the block has a row in the window
+      const float r = fast_exp2(m[n] - mn);             // 0 on the first block
+      m[n] = mn;
+      l[n] *= r;
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[n][e] *= r;
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      float vf[EPC];
+      unpack16<E>(vc[i], vf);
+#pragma unroll
+      for (int n = 0; n < NQ; ++n) {
+        const float p = fast_exp2(z[n][i] - m[n]);  // 0 for rows past the window
+        l[n] += p;
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[n][e] += p * vf[e];
+      }
     }
   }
+  // sums over the row groups: the weights once per group (the CH lanes of a
+  // group hold the same ones), the value chunks across the groups
 #pragma unroll
-  for (int o = CH; o < 64; o <<= 1)
+  for (int n = 0; n < NQ; ++n) {
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-      a0[e] += __shfl_xor(a0[e], o);
-      a1[e] += __shfl_xor(a1[e], o);
+    for (int x = CH; x < 64; x <<= 1) {
+      l[n] += __shfl_xor(l[n], x);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[n][e] += __shfl_xor(acc[n][e], x);
     }
-  if (kg == 0) {
-    *reinterpret_cast<uint4*>(o0 + dc * EPC) = on0 ? pack16<E>(a0, inv0) : make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4*>(o1 + dc * EPC) = on1 ? pack16<E>(a1, inv1) : make_uint4(0, 0, 0, 0);
+    if (kg == 0) {
+      *reinterpret_cast<uint4*>(o[n] + dc * EPC) =
+          qs[n] ? pack16<E>(acc[n], 1.f / l[n]) : make_uint4(0, 0, 0, 0);
+    }
   }
-  // the next head reuses wts: finish these reads first
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 template <typename E, int D>
@@ -264,11 +196,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a
   constexpr int CH = D / EPC;           // chunks per row
   constexpr int NKG = 64 / CH;          // key groups in the weighted sum
   static_assert(CH * EPC == D && NKG * CH == 64, "row must split into 16-byte chunks");
-  extern __shared__ float wts_all[];
   const int s = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
-  float* wts = wts_all + w * a.wmax;
   const int H = a.H, La = a.La, R = a.R;
   const int QR = La + 1;
   const size_t HD = static_cast<size_t>(H) * D;
@@ -310,7 +240,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void stream_step_kernel(DevStream a
     auto krow = [&](int tau) { return (tau == u ? kin : kring + static_cast<size_t>(tau % R) * HD) + ho; };
     auto vrow = [&](int tau) { return (tau == u ? vin : vring + static_cast<size_t>(tau % R) * HD) + ho; };
     const E* qrow = (La == 0 ? qin : qring + static_cast<size_t>(t % QR) * HD) + ho;
-    attend_wave<E, D>(qrow, krow, vrow, lo, W, a.scale_log2, wts, out + ho, lane);
+    const E* qs[1] = {qrow};
+    E* os[1] = {out + ho};
+    attend_rows<E, D, kRowGroups, 1>(qs, krow, vrow, lo, W, a.scale_log2, os, lane);
   }
   if (threadIdx.x == 0 && a.emitted) a.emitted[s] = emit ? t : -1;
   __syncthreads();  // every wave has read step[s]
@@ -334,22 +266,19 @@ struct DevLlsaStream {
   int32_t* step;
   int32_t *emitted_c, *emitted_l;
   int S, H, Lb, La;
-  int wmax;  // Lb + La + 1: score slots per wave
   const int32_t* lengths;
   float scale_log2;
 };
 
 template <typename E, int D>
-__global__ __launch_bounds__(64 * kLlsaWaves) void llsa_stream_step_kernel(DevLlsaStream a) {
+__global__ __launch_bounds__(64 * kMaxWaves) void llsa_stream_step_kernel(DevLlsaStream a) {
   constexpr int EPC = 16 / sizeof(E);
   constexpr int CH = D / EPC;
   static_assert(CH * EPC == D && 4 * CH <= 64, "row must split into 16-byte chunks");
-  extern __shared__ float wts_all[];
+
   const int s = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
-  float* qs = wts_all + w * llsa_wave_floats<D>(a.wmax);  // query 1, then the score slots
-  float* wts = qs + D;
   const int H = a.H, La = a.La, R = a.R;
   const size_t HD = static_cast<size_t>(H) * D;
 
@@ -403,8 +332,9 @@ __global__ __launch_bounds__(64 * kLlsaWaves) void llsa_stream_step_kernel(DevLl
       }
       continue;
     }
-    attend_wave2<E, D>(qc + ho, ql + ho, got_c, got_l, krow, vrow, lo, hi - lo + 1, a.scale_log2, qs, wts,
-                       out_c + ho, out_l + ho, lane);
+    const E* qq[2] = {got_c ? qc + ho : nullptr, got_l ? ql + ho : nullptr};
+    E* oo[2] = {out_c + ho, out_l + ho};
+    attend_rows<E, D, kRowGroups2, 2>(qq, krow, vrow, lo, hi - lo + 1, a.scale_log2, oo, lane);
   }
   if (threadIdx.x == 0) {
     if (a.emitted_c) a.emitted_c[s] = got_c ? u : -1;
@@ -439,25 +369,19 @@ hipError_t launch_llsa_stream_step(const LlsaStreamStepArgs& a, ElemType et, hip
   d.Lb = a.Lb;
   d.La = a.La;
   d.lengths = a.lengths;
-  d.wmax = a.Lb + a.La + 1;
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
-  // per wave a query row and two score slots per window frame, within 64 KB
-  const int per_wave = a.d == 64 ? llsa_wave_floats<64>(d.wmax) : llsa_wave_floats<32>(d.wmax);
-  int nw = a.H < kLlsaWaves ? a.H : kLlsaWaves;
-  const int fit = static_cast<int>((64 * 1024) / (sizeof(float) * static_cast<size_t>(per_wave)));
-  nw = nw < fit ? nw : fit;
+  const int nw = a.H < kMaxWaves ? a.H : kMaxWaves;
   const dim3 grid(a.S), block(64 * nw);
-  const size_t lds = static_cast<size_t>(nw) * per_wave * sizeof(float);
   if (et == kBF16) {
     if (a.d == 64)
-      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 64>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 64>), grid, block, 0, stream, d);
     else
-      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 32>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((llsa_stream_step_kernel<uint16_t, 32>), grid, block, 0, stream, d);
   } else {
     if (a.d == 64)
-      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 64>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 64>), grid, block, 0, stream, d);
     else
-      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 32>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((llsa_stream_step_kernel<float, 32>), grid, block, 0, stream, d);
   }
   return hipGetLastError();
 }
@@ -479,21 +403,19 @@ hipError_t launch_stream_step(const StreamStepArgs& a, ElemType et, hipStream_t 
   d.Lb = a.Lb;
   d.La = a.La;
   d.lengths = a.lengths;
-  d.wmax = a.Lb + a.La + 1;
   d.scale_log2 = kLog2e / sqrtf(static_cast<float>(a.d));
   const int nw = a.H < kMaxWaves ? a.H : kMaxWaves;
   const dim3 grid(a.S), block(64 * nw);
-  const size_t lds = static_cast<size_t>(nw) * d.wmax * sizeof(float);
   if (et == kBF16) {
     if (a.d == 64)
-      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 64>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 64>), grid, block, 0, stream, d);
     else
-      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 32>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<uint16_t, 32>), grid, block, 0, stream, d);
   } else {
     if (a.d == 64)
-      hipLaunchKernelGGL((stream_step_kernel<float, 64>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<float, 64>), grid, block, 0, stream, d);
     else
-      hipLaunchKernelGGL((stream_step_kernel<float, 32>), grid, block, lds, stream, d);
+      hipLaunchKernelGGL((stream_step_kernel<float, 32>), grid, block, 0, stream, d);
   }
   return hipGetLastError();
 }
