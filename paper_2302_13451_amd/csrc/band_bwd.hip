@@ -845,9 +845,9 @@ void sa_bwd_tile_kernel(BwdDev a) {
 // window test.
 constexpr int kPersistMaxB = 64;
 
-template <int D, int SEG>
+template <int D, int ROWS>
 struct RingRegs {
-  static constexpr int NS = D / 32, BPL = (SEG / 16 + 3) / 4;
+  static constexpr int NS = D / 32, BPL = (ROWS / 16 + 3) / 4;
   bf16x8 of[BPL][NS], df[BPL][NS];  // out and dout rows of the loader's new 16-row blocks
   float lse[BPL];
 };
@@ -883,11 +883,12 @@ __device__ __forceinline__ void ring_copy(const BwdDev& a, const TileCursor<1>& 
   }
 }
 
-// out and dout rows and lse values of loader lw's blocks of the same rows.
-template <int D, int SEG>
+// out and dout rows and lse values of loader lw's blocks of the same rows
+// (bl - rlo <= ROWS).
+template <int D, int ROWS>
 __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor<1>& cur, int rlo, int bl, int lw,
-                                               int lane, RingRegs<D, SEG>& rg) {
-  using R = RingRegs<D, SEG>;
+                                               int lane, RingRegs<D, ROWS>& rg) {
+  using R = RingRegs<D, ROWS>;
   const int col = lane & 15, g = lane >> 4;
   const int fs = a.H * D;
   const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
@@ -912,10 +913,10 @@ __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor
 // -D and lse log2(e) of those rows into the statistics rings (+inf for rows
 // outside the sequence). Lane (g, col) holds features 32 s + 8 g .. + 7 of row
 // col: a bfloat16 dot product per lane, summed over the four lanes of the row.
-template <int D, int SEG>
-__device__ __forceinline__ void ring_stats(const RingRegs<D, SEG>& rg, float* ndn, float* lse2, int slot, int qbase,
+template <int D, int SEG, int ROWS>
+__device__ __forceinline__ void ring_stats(const RingRegs<D, ROWS>& rg, float* ndn, float* lse2, int slot, int qbase,
                                            int len, int rlo, int bl, int lw, int lane) {
-  using R = RingRegs<D, SEG>;
+  using R = RingRegs<D, ROWS>;
   constexpr int RR = 2 * SEG;
   const int col = lane & 15, g = lane >> 4;
 #pragma unroll
@@ -990,29 +991,68 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
       zero_padding_tiles<D, 256>(a, st, G, tid - 512);
       return;
     }
-    RingRegs<D, SEG> rg;
-    TileCursor<1> cur;  // tile t
-    cur.seek(st, g0);
-    int slot = 0, rlo = 0;  // its ring slot and first new band row
-    ring_load_regs<D, SEG>(a, cur, 0, bl, lw, lane, rg);
-    ring_copy<D, SEG>(a, cur, s_ring, slot, 0, bl, lw, lane);
+    // A tile that continues its predecessor needs only its last 64 band rows;
+    // one that starts a (sequence, head) goes behind its predecessor's band
+    // and needs all bl of them. Those are loaded over two steps where the
+    // ring has room: the first bl - 64 one tile early (with the predecessor's
+    // new rows, when the predecessor continues its own predecessor or is the
+    // workgroup's first tile), so that no step loads more than a continuing
+    // tile's 64 rows plus that early part. Tile t's band and its successor's
+    // new rows take rows slot .. slot + bl + 64 of the ring, the early rows of
+    // the tile after at most up to slot + 2 bl <= RR.
+    auto wrap = [&](int x) { return x >= RR ? x - RR : x; };
+    RingRegs<D, SEG> rg;       // rows of tile ca
+    RingRegs<D, SEG - kC> re;  // early rows of tile cb
+    TileCursor<1> ca, cb;      // ca: tile t; cb: tile t + 1 when its early rows are loaded
+    ca.seek(st, g0);
+    int sa = 0, lo_a = 0, sb = 0;  // slots, and the first row of tile t loaded in its step
+    bool eb = false;               // tile t + 1's early rows are loaded
+    ring_load_regs<D, SEG>(a, ca, 0, bl, lw, lane, rg);
+    ring_copy<D, SEG>(a, ca, s_ring, sa, 0, bl, lw, lane);
+    if (g0 + 1 < g1) {
+      cb = ca;
+      cb.next(st, H, a.B);
+      if (cb.tile == 0) {
+        eb = true;
+        sb = wrap(sa + bl);
+        ring_load_regs<D, SEG - kC>(a, cb, 0, bl - kC, lw, lane, re);
+        ring_copy<D, SEG>(a, cb, s_ring, sb, 0, bl - kC, lw, lane);
+      }
+    }
     for (int t = g0; t < g1; ++t) {
-      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): tile t's copies and loads are in
-      ring_stats<D, SEG>(rg, s_ndn, s_lse2, slot, cur.tile * kC - La, cur.len, rlo, bl, lw, lane);
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the step's copies and loads are in
+      ring_stats<D, SEG>(rg, s_ndn, s_lse2, sa, ca.tile * kC - La, ca.len, lo_a, bl, lw, lane);
+      if (eb) ring_stats<D, SEG>(re, s_ndn, s_lse2, sb, cb.tile * kC - La, cb.len, 0, bl - kC, lw, lane);
       // tile t is complete in the rings, and the compute waves are done with
-      // tile t - 1, whose rows the copies of tile t + 1 may reuse
+      // tile t - 1, whose rows the copies of the next step may reuse
       barrier_lgkm();
       if (t + 1 < g1) {
-        cur.next(st, H, a.B);
-        // a tile that continues its predecessor needs only its last 64 band
-        // rows; one that starts a (sequence, head) goes behind tile t's band
-        const int inc = cur.tile > 0 ? kC : bl;
-        slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
-        rlo = cur.tile > 0 ? bl - kC : 0;
+        TileCursor<1> cn = ca;  // tile t + 1
+        cn.next(st, H, a.B);
+        const int sn = wrap(sa + (cn.tile > 0 ? kC : bl));
+        const int lo_n = (cn.tile > 0 || eb) ? bl - kC : 0;
         // register loads first: the compiler orders them after every older
         // load that wrote the same registers
-        ring_load_regs<D, SEG>(a, cur, rlo, bl, lw, lane, rg);
-        ring_copy<D, SEG>(a, cur, s_ring, slot, rlo, bl, lw, lane);
+        ring_load_regs<D, SEG>(a, cn, lo_n, bl, lw, lane, rg);
+        ring_copy<D, SEG>(a, cn, s_ring, sn, lo_n, bl, lw, lane);
+        bool en = false;
+        int snn = 0;
+        TileCursor<1> cnn = cn;  // tile t + 2
+        if (t + 2 < g1 && cn.tile > 0) {
+          cnn.next(st, H, a.B);
+          if (cnn.tile == 0) {
+            en = true;
+            snn = wrap(sn + bl);
+            ring_load_regs<D, SEG - kC>(a, cnn, 0, bl - kC, lw, lane, re);
+            ring_copy<D, SEG>(a, cnn, s_ring, snn, 0, bl - kC, lw, lane);
+          }
+        }
+        ca = cn;
+        sa = sn;
+        lo_a = lo_n;
+        cb = cnn;
+        sb = snn;
+        eb = en;
       }
     }
     // with nothing left to copy, the loaders write this workgroup's share of

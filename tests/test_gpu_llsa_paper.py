@@ -188,6 +188,9 @@ def run_check_bwd(oracle_mod, B, T, H, d, Lb, La, seed, lengths, scale="rsqrt_d"
     (66, 40, 1, 32, 10, 2, (0, 40)),
     (2, 110, 2, 64, 40, 15, (40, 110)),  # the widest look-ahead of the one-tile diagonal pass
     (2, 110, 2, 32, 40, 16, (40, 110)),  # and one past it
+    (2, 200, 2, 64, 80, 8, (60, 200)),   # wide bands at nine channels
+    (2, 200, 2, 64, 81, 8, (60, 200)),
+    (3, 300, 2, 32, 75, 11, (300, 1, 170)),
 ])
 @pytest.mark.parametrize("scale", ["rsqrt_d", "unit"])
 def test_llsa_paper_backward_parity(oracle_mod, B, T, H, d, Lb, La, lengths, scale):
