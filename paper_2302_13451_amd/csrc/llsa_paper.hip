@@ -469,8 +469,10 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
     const size_t achan = static_cast<size_t>(A) * cs;
     __syncthreads();  // every wave is done with the previous item's band
     // every row a block may read is staged (finite values: a masked key's
-    // value still enters the product with weight 0)
-    for (int e = tid; e < kFusedRows * CPR; e += 64 * kFusedWaves) {
+    // value still enters the product with weight 0): a group reads rows
+    // rb0 .. rb0 + 16 nkb - 1 with rb0 < 64
+    const int nstage = (64 + 16 * nkb) * CPR;
+    for (int e = tid; e < nstage; e += 64 * kFusedWaves) {
       const int r = e / CPR, c8 = 8 * (e % CPR), fr = fb0 + r;
       const bool ok = fr >= 0 && fr < len;
       const size_t off = achan + row_index(b, fr, h, T, H, D) + c8;
