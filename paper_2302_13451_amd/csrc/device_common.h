@@ -429,8 +429,7 @@ template <int D>
 __device__ __forceinline__ void store_rows_at(uint16_t* base, int loff, bool in_range, const f32x4* acc, float mul,
                                               bool valid, int lane) {
   constexpr int NB = D / 16;
-  const int g = lane >> 4;
-  const bool even = (g & 1) == 0;
+  (void)lane;
   u32x2 p[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -443,12 +442,12 @@ __device__ __forceinline__ void store_rows_at(uint16_t* base, int loff, bool in_
     u32x4 v;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      // even lanes send piece 2j + 1, odd lanes piece 2j
-      const unsigned send = even ? p[2 * j + 1][h] : p[2 * j][h];
-      const auto r = __builtin_amdgcn_permlane16_swap(send, send, false, false);
-      const unsigned got = even ? r[1] : r[0];
-      v[h] = even ? p[2 * j][h] : got;
-      v[2 + h] = even ? got : p[2 * j + 1][h];
+      // one swap of the odd 16-lane rows of piece 2j with the even rows of
+      // piece 2j + 1: an even lane then holds its own piece 2j and that of
+      // its odd partner, an odd lane its partner's piece 2j + 1 and its own
+      const auto r = __builtin_amdgcn_permlane16_swap(p[2 * j][h], p[2 * j + 1][h], false, false);
+      v[h] = r[0];
+      v[2 + h] = r[1];
     }
     if (in_range) st16(row + 32 * j, v);
   }
