@@ -848,7 +848,7 @@ constexpr int kPersistMaxB = 64;
 template <int D, int ROWS>
 struct RingRegs {
   static constexpr int NS = D / 32, BPL = (ROWS / 16 + 3) / 4;
-  bf16x8 of[BPL][NS], df[BPL][NS];  // out and dout rows of the loader's new 16-row blocks
+  bf16x8 of[BPL][NS];  // out rows of the loader's new 16-row blocks
   float lse[BPL];
 };
 
@@ -883,7 +883,7 @@ __device__ __forceinline__ void ring_copy(const BwdDev& a, const TileCursor<1>& 
   }
 }
 
-// out and dout rows and lse values of loader lw's blocks of the same rows
+// out rows and lse values of loader lw's blocks of the same rows
 // (bl - rlo <= ROWS).
 template <int D, int ROWS>
 __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor<1>& cur, int rlo, int bl, int lw,
@@ -893,7 +893,7 @@ __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor
   const int fs = a.H * D;
   const size_t slice = row_index(cur.b, 0, cur.h, a.T, a.H, D);
   const int qbase = cur.tile * kC - a.La, last = cur.len - 1;
-  const uint16_t *o = a.o + slice, *dout = a.dout + slice;
+  const uint16_t* o = a.o + slice;
   const float* lse = a.lse + (static_cast<size_t>(cur.b) * a.H + cur.h) * a.T;
 #pragma unroll
   for (int jj = 0; jj < R::BPL; ++jj) {
@@ -901,10 +901,7 @@ __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor
     if (r16 < bl) {
       const int fr = min(max(qbase + r16 + col, 0), last);
 #pragma unroll
-      for (int s = 0; s < R::NS; ++s) {
-        rg.of[jj][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
-        rg.df[jj][s] = __builtin_bit_cast(bf16x8, ld16(dout + (fr * fs + 32 * s + 8 * g)));
-      }
+      for (int s = 0; s < R::NS; ++s) rg.of[jj][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
       rg.lse[jj] = lse[fr];
     }
   }
@@ -912,10 +909,13 @@ __device__ __forceinline__ void ring_load_regs(const BwdDev& a, const TileCursor
 
 // -D and lse log2(e) of those rows into the statistics rings (+inf for rows
 // outside the sequence). Lane (g, col) holds features 32 s + 8 g .. + 7 of row
-// col: a bfloat16 dot product per lane, summed over the four lanes of the row.
+// col of out in registers and reads the same features of dout from the ring,
+// where the loader's own copies of these rows have landed (its vmcnt wait):
+// a bfloat16 dot product per lane, summed over the four lanes of the row.
 template <int D, int SEG, int ROWS>
-__device__ __forceinline__ void ring_stats(const RingRegs<D, ROWS>& rg, float* ndn, float* lse2, int slot, int qbase,
-                                           int len, int rlo, int bl, int lw, int lane) {
+__device__ __forceinline__ void ring_stats(const RingRegs<D, ROWS>& rg, const uint16_t* rdout, float* ndn,
+                                           float* lse2, int slot, int qbase, int len, int rlo, int bl, int lw,
+                                           int lane) {
   using R = RingRegs<D, ROWS>;
   constexpr int RR = 2 * SEG;
   const int col = lane & 15, g = lane >> 4;
@@ -923,13 +923,13 @@ __device__ __forceinline__ void ring_stats(const RingRegs<D, ROWS>& rg, float* n
   for (int jj = 0; jj < R::BPL; ++jj) {
     const int r16 = rlo + 16 * (lw + 4 * jj);
     if (r16 < bl) {
+      int lr = slot + r16 + col;
+      lr = lr >= RR ? lr - RR : lr;
       float dp = 0.f;
 #pragma unroll
-      for (int s = 0; s < R::NS; ++s) dp = dot_bf16x8(rg.df[jj][s], rg.of[jj][s], dp);
+      for (int s = 0; s < R::NS; ++s) dp = dot_bf16x8(seg_row8<D>(rdout, lr, 32 * s + 8 * g), rg.of[jj][s], dp);
       const float dg = sum_over_column(dp);
       if (g == 0) {
-        int lr = slot + r16 + col;
-        lr = lr >= RR ? lr - RR : lr;
         const int fr = qbase + r16 + col;
         ndn[lr] = -dg;
         lse2[lr] = (fr >= 0 && fr < len) ? rg.lse[jj] * kLog2e : __builtin_huge_valf();
@@ -1021,8 +1021,9 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
     }
     for (int t = g0; t < g1; ++t) {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the step's copies and loads are in
-      ring_stats<D, SEG>(rg, s_ndn, s_lse2, sa, ca.tile * kC - La, ca.len, lo_a, bl, lw, lane);
-      if (eb) ring_stats<D, SEG>(re, s_ndn, s_lse2, sb, cb.tile * kC - La, cb.len, 0, bl - kC, lw, lane);
+      ring_stats<D, SEG>(rg, s_ring + RR * D, s_ndn, s_lse2, sa, ca.tile * kC - La, ca.len, lo_a, bl, lw, lane);
+      if (eb)
+        ring_stats<D, SEG>(re, s_ring + RR * D, s_ndn, s_lse2, sb, cb.tile * kC - La, cb.len, 0, bl - kC, lw, lane);
       // tile t is complete in the rings, and the compute waves are done with
       // tile t - 1, whose rows the copies of the next step may reuse
       barrier_lgkm();
