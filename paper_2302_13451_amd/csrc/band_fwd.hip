@@ -673,7 +673,7 @@ constexpr int kFwdLoaders = 8;     // loader waves (after the eight compute wave
 // kFwdLoaders-th block. (The copy rate of a compute unit grows with the
 // number of waves that issue the copies, up to about eight.)
 template <int D, int BL2>
-__device__ __forceinline__ void ring_fwd_issue(const PairFwdArgs& a, const TileCursor<2>& cur, uint16_t* rk,
+__device__ __forceinline__ void ring_fwd_issue(const PairFwdArgs& a, const TileCursor<1>& cur, uint16_t* rk,
                                                uint16_t* rv, uint16_t* qbuf, int slot, int rlo, int lw, int lane) {
   constexpr int RR = kFwdRingRows, CPR = D / 8, RPI = 64 / CPR, IPB = 16 / RPI;
   const int rl = lane / CPR, pp = lane % CPR;
@@ -705,7 +705,7 @@ __device__ __forceinline__ void ring_fwd_issue(const PairFwdArgs& a, const TileC
 // This workgroup's share (of G) of the tiles wholly past a sequence's end:
 // zero output rows and -inf lse (64 kFwdLoaders threads, thread i).
 template <int D>
-__device__ __forceinline__ void zero_padding_tiles(const PairFwdArgs& a, const SeqTable<2>& st, int G, int i) {
+__device__ __forceinline__ void zero_padding_tiles(const PairFwdArgs& a, const SeqTable<1>& st, int G, int i) {
   constexpr int NT = 64 * kFwdLoaders, CPR = D / 8;
   const int T = a.T, H = a.H, fs = H * D;
   const PadTable pt(st, a.B, H, a.ntiles, threadIdx.x & 63);
@@ -738,10 +738,25 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int T = a.T, H = a.H, fs = H * D;
-  const SeqTable<2> st(a.lengths, a.B, T, H, lane);
-  const int nsteps = st.total();
-  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * nsteps / G);
-  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
+  // The share is a contiguous range of 64-query tiles [g0, g1) of the tile
+  // list (not of its steps, which would leave some shares a whole step
+  // longer): a step takes the next two tiles of one (sequence, head), or one
+  // at the end of the (sequence, head) or of the share.
+  const SeqTable<1> st(a.lengths, a.B, T, H, lane);
+  const int ntl = st.total();
+  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * ntl / G);
+  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * ntl / G);
+  // tiles of the step at tile gi of cursor c
+  auto step_tiles = [&](const TileCursor<1>& c, int gi) { return min(2, min(c.nt - c.tile, g1 - gi)); };
+  // the cursor moved on by n tiles of its (sequence, head), or to the next one
+  auto advance = [&](TileCursor<1>& c, int n) {
+    if (c.tile + n < c.nt) {
+      c.tile += n;
+    } else {
+      c.tile = c.nt - 1;
+      c.next(st, H, a.B);
+    }
+  };
 
   if (w >= 8) {
     // the loaders share each SIMD with two compute waves: at a higher issue
@@ -752,23 +767,29 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
       zero_padding_tiles<D>(a, st, G, tid - 512);
       return;
     }
-    TileCursor<2> cur;
+    TileCursor<1> cur;
     cur.seek(st, g0);
     int slot = 0;
     ring_fwd_issue<D, BL2>(a, cur, s_k, s_v, s_q, slot, 0, lw, lane);
-    for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
+    for (int gi = g0, s = 0, nst = step_tiles(cur, g0); gi < g1; ++s) {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): step s is in
       // a plain barrier: this wave reads no LDS and its copies are ordered by
       // the wait above (a fence would add nothing but the wait). After it the
       // compute waves are done with step s - 1.
       __builtin_amdgcn_s_barrier();
-      if (gi + 1 < g1) {
-        cur.next(st, H, a.B);
-        const int inc = cur.tile > 0 ? 2 * kTq : BL2;
+      const int gn = gi + nst;
+      if (gn < g1) {
+        // every step copies a band of BL2 rows from 64 n frames past its
+        // predecessor's (n tiles): one that continues the predecessor's
+        // (sequence, head) copies only the rows past the predecessor's band
+        advance(cur, nst);
+        const int inc = cur.tile > 0 ? kTq * nst : BL2;
         slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
         ring_fwd_issue<D, BL2>(a, cur, s_k, s_v, s_q + ((s + 1) & 1) * 2 * kTq * D, slot,
-                               cur.tile > 0 ? BL2 - 2 * kTq : 0, lw, lane);
+                               cur.tile > 0 ? BL2 - kTq * nst : 0, lw, lane);
       }
+      gi = gn;
+      nst = gn < g1 ? step_tiles(cur, gn) : 0;
     }
     // with nothing left to copy, the loaders write this workgroup's share of
     // the tiles wholly past a sequence's end while the compute waves finish
@@ -781,11 +802,11 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
   const int grp = w >> 2, wq = w & 3;  // tile of the step, wave within the tile
   const float c2 = a.scale_log2;
   const int nblk = (16 + a.hi - a.lo + kSub - 1) / kSub;
-  TileCursor<2> cur;
+  TileCursor<1> cur;
   cur.seek(st, g0);
   int slot = 0;
-  for (int gi = g0, s = 0; gi < g1; ++gi, ++s) {
-    const int nst = cur.step_tiles();
+  for (int gi = g0, s = 0, nst = 0; gi < g1; gi += nst, ++s) {
+    nst = step_tiles(cur, gi);
     lds_barrier();  // step s is in the rings and query buffer s % 2
     if (grp < nst) {
       const uint16_t* qbuf = s_q + (s & 1) * 2 * kTq * D;
@@ -814,8 +835,8 @@ __global__ __launch_bounds__(64 * (8 + kFwdLoaders)) void band_fwd_pair_kernel(P
       if (a.lse && g == 0 && t < T)
         a.lse[(static_cast<size_t>(cur.b) * H + cur.h) * T + t] = valid ? (m + log2f(lsum)) * kLn2 : kNegInf;
     }
-    cur.next(st, H, a.B);
-    const int inc = cur.tile > 0 ? 2 * kTq : BL2;
+    advance(cur, nst);
+    const int inc = cur.tile > 0 ? kTq * nst : BL2;
     slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
   }
 }
