@@ -79,6 +79,49 @@ def load_library():
     return lib
 
 
+class _Recorder:
+    """Stands in for the loaded library while one binding call runs, and
+    records the entry points it calls with their marshalled arguments."""
+
+    def __init__(self, lib):
+        self.lib = lib
+        self.calls = []
+
+    def __getattr__(self, name):
+        fn = getattr(self.lib, name)
+
+        def call(*args):
+            self.calls.append((fn, args))
+            return fn(*args)
+        return call
+
+
+def prepared(fn, *args, **kwargs):
+    """Runs ``fn(*args, **kwargs)`` (a binding call, or a function making
+    several) once and returns a function of no arguments that repeats the same
+    calls of the C entry points with the same marshalled arguments: no shape
+    checks, no allocation, the stream of the first call. For timing loops, in
+    which the per-call checks would otherwise cost more host time than a short
+    kernel takes. Outputs must be passed in (not allocated by the call), and
+    every tensor must stay alive while the function is used."""
+    global _lib
+    lib = load_library()
+    rec = _Recorder(lib)
+    _lib = rec
+    try:
+        fn(*args, **kwargs)
+    finally:
+        _lib = lib
+    calls = [(f, a) for f, a in rec.calls if f is not lib.sa_last_error]
+
+    def run():
+        for f, a in calls:
+            rc = f(*a)
+            if rc != SA_OK:
+                _check(rc)
+    return run
+
+
 def _check(rc: int):
     if rc != SA_OK:
         raise SAError(rc, load_library().sa_last_error().decode(errors="replace"))

@@ -177,3 +177,20 @@ def test_deterministic():
     o1, l1 = bd.sa_forward(q, k, v, 50, 7, ln)
     o2, l2 = bd.sa_forward(q, k, v, 50, 7, ln)
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_prepared_call_repeats_the_call():
+    """binding.prepared marshals a call once and repeats it bare: the repeat
+    writes the same outputs, bit for bit, into the same tensors."""
+    x = sa_inputs(2, 150, 3, 64, 7, lengths=(60, 150))
+    q, k, v = (x[n].to(torch.bfloat16).cuda() for n in ("q", "k", "v"))
+    ln = x["lengths"].cuda()
+    out = torch.empty_like(q)
+    lse = torch.empty(2, 3, 150, dtype=torch.float32, device="cuda")
+    run = bd.prepared(bd.sa_forward, q, k, v, 20, 5, ln, out=out, lse=lse)
+    first = (out.clone(), lse.clone())
+    out.fill_(7.0)
+    lse.fill_(7.0)
+    run()
+    torch.cuda.synchronize()
+    assert torch.equal(out, first[0]) and torch.equal(lse, first[1])
