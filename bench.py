@@ -228,6 +228,35 @@ def copy_ceiling(mib=64, reps=24):
     return res
 
 
+def kernel_floor(reps=200):
+    """The per-launch floor of the SA kernels' own launch configuration: the
+    workload's B, H, d and window with one frame per sequence and every
+    length 0, so each persistent workgroup starts, finds no tile to work on
+    and writes one padding row (256 workgroups of 16 (forward) and 12
+    (backward) waves, each holding its full LDS allocation), timed back to
+    back like the kernels themselves."""
+    w = WORKLOAD
+    B, H, d = w["B"], w["H"], w["d"]
+    z = torch.zeros(B, 1, H, d, dtype=torch.bfloat16, device="cuda")
+    t = {n: torch.empty_like(z) for n in ("out", "dq", "dk", "dv")}
+    lse = torch.empty(B, H, 1, dtype=torch.float32, device="cuda")
+    lengths = torch.zeros(B, dtype=torch.int32, device="cuda")
+
+    def fwd(_):
+        bd.sa_forward(z, z, z, w["Lb"], w["La"], lengths, out=t["out"], lse=lse)
+
+    def bwd(_):
+        bd.sa_backward(z, z, z, t["out"], lse, z, w["Lb"], w["La"], lengths, dq=t["dq"], dk=t["dk"],
+                       dv=t["dv"])
+    for f in (fwd, bwd):
+        for _ in range(20):
+            f(None)
+    return {"sa_forward_us": launch_ms(fwd, [None], reps) * 1e3,
+            "sa_backward_us": launch_ms(bwd, [None], reps) * 1e3,
+            "note": "B=16, T=1, H=12, d=64, Lb=64, La=8, all lengths 0: the launch and "
+                    "drain of the persistent grid with no tile to compute"}
+
+
 C2 = dict(B=8, T=500, H=12, d=64, Lb=32, La=8, lengths="full", seed=2)
 
 
@@ -967,6 +996,11 @@ def main():
     line["copy_ceiling"] = ceiling
     line["roofline"]["copy_ceiling_gbs"] = ceiling["gbs"]
     line["roofline"]["practical_frac"] = dom_gbs / ceiling["gbs"]
+    log("launch floor of the SA kernels' configuration")
+    floor_k = kernel_floor()
+    line["kernel_launch_floor"] = floor_k
+    line["roofline"]["launch_floor_us"] = floor_k["sa_backward_us" if dominant == "sa_backward"
+                                                  else "sa_forward_us"]
     if not args.no_extras:
         log("SA forward at the l32_r8 window (B=8, T=500)")
         line["sa_forward_l32_r8"] = bench_c2(args.steps, args.warmup)

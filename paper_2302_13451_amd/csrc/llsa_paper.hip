@@ -306,14 +306,16 @@ __device__ __forceinline__ void stage8(uint16_t* tile, int row, int c, bf16x8 x)
   st8(p + 4, u32x2{u[2], u[3]});
 }
 
-// A operand of a product that contracts over the 16 rows of an LDS tile:
-// lane (f, g) receives X[4g + e][f0 + f] for e < 4 and zeros at e >= 4.
+// A operand of a product that contracts over the 16 rows of an LDS tile (row
+// stride D + 4): lane (f, g) receives X[4g + e][f0 + f] for e < 4 and zeros
+// at e >= 4. One transposing read (ds_read_b64_tr_b16): lane L of 16-lane
+// group g points at row 4g + L / 4, columns f0 + 4 (L % 4) .. + 3, and the
+// read hands lane f element f of each of the group's four rows.
 template <int D>
 __device__ __forceinline__ bf16x8 tile_tr(const uint16_t* tile, int f0, int col, int g) {
-  bf16x8 r{};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = __builtin_bit_cast(__bf16, tile[(4 * g + e) * (D + 4) + f0 + col]);
-  return r;
+  const uint16_t* p = tile + (4 * g + (col >> 2)) * (D + 4) + f0 + 4 * (col & 3);
+  const bf16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+  return __builtin_shufflevector(x, bf16x4{}, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // Four values of a score-shaped tile as the B operand (k = 8g + e, e < 4).
