@@ -318,12 +318,11 @@ __device__ __forceinline__ bf16x8 tile_tr(const uint16_t* tile, int f0, int col,
   return __builtin_shufflevector(x, bf16x4{}, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
-// Four values of a score-shaped tile as the B operand (k = 8g + e, e < 4).
+// Four values of a score-shaped tile as the B operand (k = 8g + e, e < 4),
+// rounded to bfloat16 in pairs.
 __device__ __forceinline__ bf16x8 as_b4(const float* x) {
-  bf16x8 r{};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = static_cast<__bf16>(x[e]);
-  return r;
+  const uint32_t lo = pack_bf16x2(x[0], x[1]), hi = pack_bf16x2(x[2], x[3]);
+  return __builtin_bit_cast(bf16x8, u32x4{lo, hi, 0u, 0u});
 }
 
 __device__ __forceinline__ void wave_sync() {
@@ -455,7 +454,8 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
   const uint16_t* k = static_cast<const uint16_t*>(a.k);
   const uint16_t* v = static_cast<const uint16_t*>(a.v);
   uint16_t* out = static_cast<uint16_t*>(a.out);
-  const float scale = a.scale;
+  const float c2 = a.scale * kLog2e;  // score scale, in the exponent's base 2
+  const size_t coff = col * cs, loff = col * ls;  // the lane's channel
   constexpr int CPR = D / 8;  // 16-byte pieces per row
   for (long long it = blockIdx.x; it < items; it += gridDim.x) {
     const int h = static_cast<int>(it % H);
@@ -473,7 +473,8 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
     // every row a block may read is staged (finite values: a masked key's
     // value still enters the product with weight 0): a group reads rows
     // rb0 .. rb0 + 16 nkb - 1 with rb0 < 64
-    const int nstage = (64 + 16 * nkb) * CPR;
+    // (a chunk whose groups all lie past the sequence's end reads nothing)
+    const int nstage = s0 - A >= len ? 0 : (64 + 16 * nkb) * CPR;
     for (int e = tid; e < nstage; e += 64 * kFusedWaves) {
       const int r = e / CPR, c8 = 8 * (e % CPR), fr = fb0 + r;
       const bool ok = fr >= 0 && fr < len;
@@ -490,12 +491,27 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
       const bool qrow = col <= A && tc >= 0 && tc < T;  // a row this group writes
       const bool qv = qrow && tc < len;
       const bool kv = col < A && tc >= 0 && tc < len;
-      const size_t crow = col * cs + row_index(b, tc, h, T, H, D);
+      const size_t crow = coff + row_index(b, tc, h, T, H, D);
+      float* const lrow = a.lse + loff + (static_cast<size_t>(b) * H + h) * T + tc;
+      if (sd - A >= len) {
+        // every query of the group lies past the sequence's end: zero rows
+        if (qrow) {
+#pragma unroll
+          for (int fb = 0; fb < NF; ++fb) st8(out + crow + 16 * fb + 4 * g, u32x2{0u, 0u});
+          if (g == 0) *lrow = kNegInf;
+        }
+        continue;
+      }
       bf16x8 qa[NS];
 #pragma unroll
       for (int s2 = 0; s2 < NS; ++s2) qa[s2] = ld_row8<D>(q + crow + 32 * s2 + 8 * g, qv);
       const int tb0 = sd - A - Lb;  // frame of band key 0
       const int rb0 = sd - s0;      // its staged row
+      // A group whose band and diagonal frames all lie in the sequence needs
+      // no frame test; the rows of its (valid) queries and the zero rows of
+      // the lanes past the last query (ignored at the end) give finite
+      // scores. Raw scores are kept; the scale goes into the exponent.
+      const bool inner = tb0 >= 0 && sd < len;
       // scores: band blocks 0 .. NKB-1, then the diagonal block NKB
       float sc[NKB + 1][4];
       float m = kNegInf;
@@ -511,9 +527,9 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int j = 16 * kb + 4 * g + e, te = tb0 + j;
-            const bool ok = qv && j <= Lb && te >= 0 && te < len;
-            sc[kb][e] = ok ? st[e] * scale : kNegInf;
-            m = fmaxf(m, sc[kb][e]);
+            const bool ok = inner ? j <= Lb : qv && j <= Lb && te >= 0 && te < len;
+            sc[kb][e] = ok ? st[e] : kNegInf;
+            m = vmax(m, sc[kb][e]);
           }
         } else {
 #pragma unroll
@@ -532,19 +548,21 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int j = 4 * g + e, tj = sd - j;
-          const bool ok = qv && j < A && tj >= 0 && tj < len;
-          sc[NKB][e] = ok ? st[e] * scale : kNegInf;
-          m = fmaxf(m, sc[NKB][e]);
+          const bool ok = inner ? j < A : qv && j < A && tj >= 0 && tj < len;
+          sc[NKB][e] = ok ? st[e] : kNegInf;
+          m = vmax(m, sc[NKB][e]);
         }
       }
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      m = vmax(m, __shfl_xor(m, 16, 64));
+      m = vmax(m, __shfl_xor(m, 32, 64));
+      // (a lane without a valid query may have every score masked)
+      const float mc = m == kNegInf ? 0.f : m * c2;
       float ps = 0.f;
 #pragma unroll
       for (int kb = 0; kb <= NKB; ++kb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          sc[kb][e] = sc[kb][e] == kNegInf ? 0.f : __expf(sc[kb][e] - m);
+          sc[kb][e] = fast_exp2(__builtin_fmaf(sc[kb][e], c2, -mc));
           ps += sc[kb][e];
         }
       ps += __shfl_xor(ps, 16, 64);
@@ -573,7 +591,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
         for (int fb = 0; fb < NF; ++fb)
           st8(out + crow + 16 * fb + 4 * g,
               u32x2{pack_bf16x2(acc[fb][0] * inv, acc[fb][1] * inv), pack_bf16x2(acc[fb][2] * inv, acc[fb][3] * inv)});
-        if (g == 0) a.lse[col * ls + (static_cast<size_t>(b) * H + h) * T + tc] = qv ? m + __logf(ps) : kNegInf;
+        if (g == 0) *lrow = qv ? (mc + log2f(ps)) * kLn2 : kNegInf;
       }
     }
   }
