@@ -625,6 +625,18 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kern
     const bool qv = col <= A && tc >= 0 && tc < len;
     const bool kv = col < A && tc >= 0 && tc < len;
     const size_t row = col * cs + row_index(b, tc, h, T, H, D);
+    if (sd - A >= len) {
+      // every query and key of the group lies past the sequence's end: dq
+      // gets nothing, the key rows are zero
+      if (col < A && tc < T) {
+#pragma unroll
+        for (int fb = 0; fb < NF; ++fb) {
+          st8(a.dk + row + 16 * fb + 4 * g, u32x2{0u, 0u});
+          st8(a.dv + row + 16 * fb + 4 * g, u32x2{0u, 0u});
+        }
+      }
+      continue;
+    }
     bf16x8 qa[NS], da[NS], ka[NS], va[NS];
     float dn = 0.f;
 #pragma unroll
