@@ -410,6 +410,56 @@ __device__ __forceinline__ float sum_over_column(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Lane exchanges on the data-parallel-primitive path (DPP), which move data
+// between lanes without an LDS round trip: quad permutations (lane l reads
+// lane l ^ 1, l ^ 2), the mirror of each 8-lane half and each 16-lane row,
+// and rotations of a row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowMirror = 0x140;  // lane i of a row reads lane 15 - i
+constexpr int kDppHalfMirror = 0x141; // lane i of an 8-lane half reads lane 7 - i
+template <int N>
+constexpr int kDppRowRor = 0x120 + N; // lane i of a row reads lane (i - N) mod 16
+
+// Sum (all lanes get it) over each aligned group of CH lanes (CH = 1, 2, 4,
+// 8 or 16): after each step every lane of a group holds the sum of a
+// sub-group twice the size.
+template <int CH>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(CH == 1 || CH == 2 || CH == 4 || CH == 8 || CH == 16, "groups of up to a row");
+  if constexpr (CH >= 2) x += dpp_f<kDppXor1>(x);
+  if constexpr (CH >= 4) x += dpp_f<kDppXor2>(x);
+  if constexpr (CH >= 8) x += dpp_f<kDppHalfMirror>(x);
+  if constexpr (CH >= 16) x += dpp_f<kDppRowMirror>(x);
+  return x;
+}
+
+// Sum over the 64 / CH groups of CH lanes, lane by lane (lane l gets the sum
+// over the lanes l' = l mod CH): rotations of the row by CH, 2 CH, .. 8, then
+// the swaps of row pairs.
+template <int CH>
+__device__ __forceinline__ float across_groups_sum(float x) {
+  if constexpr (CH <= 4) x += dpp_f<kDppRowRor<4>>(x);
+  if constexpr (CH <= 8) x += dpp_f<kDppRowRor<8>>(x);
+  return sum_over_column(x);
+}
+
+// Maximum over the wave (all lanes get it), NaN ignored as by fmaxf.
+__device__ __forceinline__ float wave_max_dpp(float x) {
+  x = fmaxf(x, dpp_f<kDppXor1>(x));
+  x = fmaxf(x, dpp_f<kDppXor2>(x));
+  x = fmaxf(x, dpp_f<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp_f<kDppRowMirror>(x));
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Writes rows r0 .. r0 + nrows - 1 of dst (row stride fs) from a wave's
 // transposed accumulators, lane (g, col) holding features 16 i + 4 g .. + 3
 // of row col. Lanes g and g ^ 1 swap 4-feature pieces (permlane16 swap), so

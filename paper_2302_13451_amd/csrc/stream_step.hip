@@ -60,12 +60,6 @@ __device__ __forceinline__ uint4 pack16<uint16_t>(const float* f, float mul) {
                     pack_bf16x2(f[4] * mul, f[5] * mul), pack_bf16x2(f[6] * mul, f[7] * mul));
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
-}
-
 struct DevStream {
   const void *q, *k, *v;
   void* out;
@@ -138,8 +132,7 @@ __device__ __forceinline__ void attend_rows(const E* const* qs, KRow krow, VRow 
         float p = 0.f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) p += qf[n][e] * kf[e];
-#pragma unroll
-        for (int x = 1; x < CH; x <<= 1) p += __shfl_xor(p, x);  // the row's CH chunks
+        p = group_sum<CH>(p);  // the row's CH chunks
         z[n][i] = in ? p * scale_log2 : kNegInf;
         bm[n] = fmaxf(bm[n], z[n][i]);
       }
@@ -153,7 +146,7 @@ __device__ __forceinline__ void attend_rows(const E* const* qs, KRow krow, VRow 
     }
 #pragma unroll
     for (int n = 0; n < NQ; ++n) {
-      const float mn = fmaxf(m[n], wave_max(bm[n]));  // finite: the block has a row in the window
+      const float mn = fmaxf(m[n], wave_max_dpp(bm[n]));  // finite: the block has a row in the window
       const float r = fast_exp2(m[n] - mn);             // 0 on the first block
       m[n] = mn;
       l[n] *= r;
@@ -177,12 +170,9 @@ __device__ __forceinline__ void attend_rows(const E* const* qs, KRow krow, VRow 
   // group hold the same ones), the value chunks across the groups
 #pragma unroll
   for (int n = 0; n < NQ; ++n) {
+    l[n] = across_groups_sum<CH>(l[n]);
 #pragma unroll
-    for (int x = CH; x < 64; x <<= 1) {
-      l[n] += __shfl_xor(l[n], x);
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[n][e] += __shfl_xor(acc[n][e], x);
-    }
+    for (int e = 0; e < EPC; ++e) acc[n][e] = across_groups_sum<CH>(acc[n][e]);
     if (kg == 0) {
       *reinterpret_cast<uint4*>(o[n] + dc * EPC) =
           qs[n] ? pack16<E>(acc[n], 1.f / l[n]) : make_uint4(0, 0, 0, 0);
