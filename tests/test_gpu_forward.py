@@ -67,6 +67,27 @@ def test_forward_parity(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale, p
         assert_lse_close(lse, lr, dtype)
 
 
+# The persistent kernel (bfloat16, at most 64 sequences) at shapes with
+# several tiles per compute unit, so that shares span (sequence, head)
+# boundaries and every workgroup runs several steps: ragged lengths, empty
+# sequences, one-sided windows and d = 32.
+PERSISTENT_SHAPES = [
+    (12, 600, 12, 64, 37, 5, (50, 600)),
+    (10, 700, 12, 32, 64, 8, (1, 700)),
+    (16, 520, 10, 64, 70, 0, (0, 520)),
+    (14, 650, 12, 64, 0, 9, (100, 650)),
+]
+
+
+@pytest.mark.parametrize("dtype,scale,peak", [v for v in VARIANTS if v[0] == "bf16"])
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", PERSISTENT_SHAPES)
+def test_forward_parity_persistent(oracle_mod, dtype, B, T, H, d, Lb, La, lengths, scale, peak):
+    out, lse, yr, lr, x = run_forward(oracle_mod, B, T, H, d, Lb, La, dtype, 6, lengths, scale,
+                                      peak)
+    assert_slices_close(out, yr, dtype, x["lengths"], "out")
+    assert_lse_close(lse, lr, dtype)
+
+
 def test_config2_full_size(oracle_mod):
     """SA forward bf16, B=8, T=500, H=12, d=64, Lb=32, La=8, N(0,1)/sqrt(d)."""
     out, lse, yr, lr, x = run_forward(oracle_mod, 8, 500, 12, 64, 32, 8, "bf16", seed=2)
