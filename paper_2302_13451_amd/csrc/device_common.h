@@ -502,6 +502,22 @@ __device__ __forceinline__ void store_rows_at(uint16_t* base, int loff, bool in_
     if (in_range) st16(row + 32 * j, v);
   }
 }
+// The same regrouping on the float values: lane (col, g) receives, for
+// j < D / 32, the 8 features 32 j + row_piece_offset(g) .. + 7 of row col
+// (in MFMA output order it holds features 16 i + 4 g .. + 3 in acc[i]).
+__device__ __forceinline__ int row_piece_offset(int g) { return 8 * (g >> 1) + ((g & 1) == 0 ? 0 : 16); }
+template <int D>
+__device__ __forceinline__ void rows_to_pieces(const f32x4* acc, f32x8* piece) {
+#pragma unroll
+  for (int j = 0; j < D / 32; ++j)
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[2 * j][h]),
+                                                      __float_as_uint(acc[2 * j + 1][h]), false, false);
+      piece[j][h] = __uint_as_float(r[0]);
+      piece[j][4 + h] = __uint_as_float(r[1]);
+    }
+}
 template <int D>
 __device__ __forceinline__ void store_rows_direct(uint16_t* dst, int fs, int r0, int nrows, const f32x4* acc,
                                                   float mul, bool valid, int lane) {

@@ -370,6 +370,11 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_merge_mfma_kernel(
     }
     float* lp = a.lse + col * ls + (static_cast<size_t>(b) * H + h) * T + tc;
     const float lb = qv ? *lp : kNegInf;
+    // the band part of the output row, 16-byte pieces 32 j + po
+    const int po = row_piece_offset(g);
+    u32x4 yb[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) yb[j] = qv ? ld16(out + qrow + 32 * j + po) : kZero16;
 #pragma unroll
     for (int s2 = 0; s2 < NS; ++s2) stage8<D>(sv, col, 32 * s2 + 8 * g, va[s2]);
     f32x4 st = {0.f, 0.f, 0.f, 0.f};
@@ -398,20 +403,29 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_merge_mfma_kernel(
     const float den = wb + ps;
     const bf16x8 pb = as_b4(p);
     wave_sync();
+    // lane (i, g) holds features 16 fb + 4g .. + 3 of query i in y[fb]; the
+    // row goes out as 16-byte pieces (lanes g, g ^ 1 swap their halves)
+    f32x4 y[NF];
 #pragma unroll
-    for (int fb = 0; fb < NF; ++fb) {
-      const f32x4 y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sv, 16 * fb, col, g), pb,
-                                                             f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-      if (qv) {  // lane (i, g) holds features 16 fb + 4g .. + 3 of query i
-        uint16_t* o = out + qrow + 16 * fb + 4 * g;
-        const u32x2 yb = *reinterpret_cast<const u32x2*>(o);
-        const float inv = 1.f / den;
-        float r[4];
-        const float bv[4] = {__uint_as_float(yb[0] << 16), __uint_as_float(yb[0] & 0xffff0000u),
-                             __uint_as_float(yb[1] << 16), __uint_as_float(yb[1] & 0xffff0000u)};
+    for (int fb = 0; fb < NF; ++fb)
+      y[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sv, 16 * fb, col, g), pb, f32x4{0.f, 0.f, 0.f, 0.f},
+                                                      0, 0, 0);
+    f32x8 yp[NS];
+    rows_to_pieces<D>(y, yp);
+    if (qv) {
+      const float inv = 1.f / den;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) r[e] = (wb == 0.f ? y[e] : wb * bv[e] + y[e]) * inv;  // bv is NaN for an empty band
-        st8(o, u32x2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])});
+      for (int j = 0; j < NS; ++j) {
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          // the band part is NaN for an empty band, whose weight wb is 0
+          const float b0 = __uint_as_float(yb[j][e] << 16), b1 = __uint_as_float(yb[j][e] & 0xffff0000u);
+          const float r0 = (wb == 0.f ? yp[j][2 * e] : wb * b0 + yp[j][2 * e]) * inv;
+          const float r1 = (wb == 0.f ? yp[j][2 * e + 1] : wb * b1 + yp[j][2 * e + 1]) * inv;
+          o[e] = pack_bf16x2(r0, r1);
+        }
+        st16(out + qrow + 32 * j + po, o);
       }
     }
     if (qv && g == 0) *lp = m + __logf(den);
@@ -497,7 +511,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
         // every query of the group lies past the sequence's end: zero rows
         if (qrow) {
 #pragma unroll
-          for (int fb = 0; fb < NF; ++fb) st8(out + crow + 16 * fb + 4 * g, u32x2{0u, 0u});
+          for (int j = 0; j < NS; ++j) st16(out + crow + 32 * j + row_piece_offset(g), kZero16);
           if (g == 0) *lrow = kNegInf;
         }
         continue;
@@ -585,20 +599,16 @@ __global__ __launch_bounds__(64 * kFusedWaves) void llsa_paper_fwd_fused_kernel(
           acc[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(tile, 16 * fb, col, g), pb, acc[fb], 0, 0, 0);
       }
       wave_sync();  // the tile is rewritten by the next group
-      if (qrow) {  // lane (i, g) holds features 16 fb + 4g .. + 3 of query i
-        const float inv = qv ? 1.f / ps : 0.f;
-#pragma unroll
-        for (int fb = 0; fb < NF; ++fb)
-          st8(out + crow + 16 * fb + 4 * g,
-              u32x2{pack_bf16x2(acc[fb][0] * inv, acc[fb][1] * inv), pack_bf16x2(acc[fb][2] * inv, acc[fb][3] * inv)});
-        if (g == 0) *lrow = qv ? (mc + log2f(ps)) * kLn2 : kNegInf;
-      }
+      // lane (i, g) holds features 16 fb + 4g .. + 3 of query i; the row goes
+      // out as 16-byte pieces (lanes g, g ^ 1 swap their halves)
+      store_rows_at<D>(out + crow, row_piece_offset(g), qrow, acc, qv ? 1.f / ps : 0.f, qv, lane);
+      if (qrow && g == 0) *lrow = qv ? (mc + log2f(ps)) * kLn2 : kNegInf;
     }
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kernel(PaperDiagDev a) {
+__global__ __launch_bounds__(64 * kDiagWaves) __attribute__((amdgpu_waves_per_eu(5))) void llsa_paper_bwd_diag_mfma_kernel(PaperDiagDev a) {
   constexpr int NS = D / 32, NF = D / 16, TS = 16 * (D + 4);
   __shared__ __attribute__((aligned(16))) uint16_t s_tile[kDiagWaves][3 * TS];  // q, k, dout rows
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -630,9 +640,9 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kern
       // gets nothing, the key rows are zero
       if (col < A && tc < T) {
 #pragma unroll
-        for (int fb = 0; fb < NF; ++fb) {
-          st8(a.dk + row + 16 * fb + 4 * g, u32x2{0u, 0u});
-          st8(a.dv + row + 16 * fb + 4 * g, u32x2{0u, 0u});
+        for (int j = 0; j < NS; ++j) {
+          st16(a.dk + row + 32 * j + row_piece_offset(g), kZero16);
+          st16(a.dv + row + 32 * j + row_piece_offset(g), kZero16);
         }
       }
       continue;
@@ -648,6 +658,13 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kern
       va[s2] = ld_row8<D>(a.v + row + c0, kv);
       dn = dot_bf16x8(da[s2], ld_row8<D>(a.o + row + c0, qv), dn);
     }
+    // the band pass's part of dq of query col, loaded with the operands so
+    // that its latency overlaps theirs (every query row belongs to exactly
+    // one group, so no other wave writes it): 16-byte pieces 32 j + po
+    const int po = row_piece_offset(g);
+    u32x4 dq0[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) dq0[j] = qv ? ld16(a.dq + row + 32 * j + po) : u32x4{0u, 0u, 0u, 0u};
     dn += __shfl_xor(dn, 16, 64);
     dn += __shfl_xor(dn, 32, 64);  // D of query col
     const float lse = qv ? a.lse[col * ls + (static_cast<size_t>(b) * H + h) * T + tc] : 0.f;
@@ -682,27 +699,32 @@ __global__ __launch_bounds__(64 * kDiagWaves) void llsa_paper_bwd_diag_mfma_kern
     const bf16x8 bdst = as_b4(dst), bds = as_b4(ds), bp = as_b4(pw);
     wave_sync();
     const bool kout = col < A && tc >= 0 && tc < T;  // a key row of this group (zeros past the length)
+    // dk, dv and dq in turn (rows written as 16-byte pieces: lanes g, g ^ 1
+    // swap their halves)
+    f32x4 gx[NF];
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int fb = 0; fb < NF; ++fb) {
-      const int f0 = 16 * fb;
-      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-      const f32x4 gq = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sk, f0, col, g), bdst, z, 0, 0, 0);
-      const f32x4 gk = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sq, f0, col, g), bds, z, 0, 0, 0);
-      const f32x4 gv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sdo, f0, col, g), bp, z, 0, 0, 0);
-      const size_t off = row + f0 + 4 * g;  // features f0 + 4g .. + 3 of row col
-      if (qv) {
-        uint16_t* p = a.dq + off;
-        const u32x2 o = *reinterpret_cast<const u32x2*>(p);
-        const float r0 = __uint_as_float(o[0] << 16) + scale * gq[0];
-        const float r1 = __uint_as_float(o[0] & 0xffff0000u) + scale * gq[1];
-        const float r2 = __uint_as_float(o[1] << 16) + scale * gq[2];
-        const float r3 = __uint_as_float(o[1] & 0xffff0000u) + scale * gq[3];
-        st8(p, u32x2{pack_bf16x2(r0, r1), pack_bf16x2(r2, r3)});
-      }
-      if (kout) {
-        st8(a.dk + off, kv ? u32x2{pack_bf16x2(scale * gk[0], scale * gk[1]), pack_bf16x2(scale * gk[2], scale * gk[3])}
-                           : u32x2{0u, 0u});
-        st8(a.dv + off, kv ? u32x2{pack_bf16x2(gv[0], gv[1]), pack_bf16x2(gv[2], gv[3])} : u32x2{0u, 0u});
+    for (int fb = 0; fb < NF; ++fb)
+      gx[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sq, 16 * fb, col, g), bds, z, 0, 0, 0);
+    store_rows_at<D>(a.dk + row, po, kout, gx, scale, kv, lane);
+#pragma unroll
+    for (int fb = 0; fb < NF; ++fb)
+      gx[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sdo, 16 * fb, col, g), bp, z, 0, 0, 0);
+    store_rows_at<D>(a.dv + row, po, kout, gx, 1.f, kv, lane);
+#pragma unroll
+    for (int fb = 0; fb < NF; ++fb)
+      gx[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tile_tr<D>(sk, 16 * fb, col, g), bdst, z, 0, 0, 0);
+    f32x8 pq[NS];
+    rows_to_pieces<D>(gx, pq);
+    if (qv) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) {
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          o[e] = pack_bf16x2(__uint_as_float(dq0[j][e] << 16) + scale * pq[j][2 * e],
+                             __uint_as_float(dq0[j][e] & 0xffff0000u) + scale * pq[j][2 * e + 1]);
+        st16(a.dq + row + 32 * j + po, o);
       }
     }
     wave_sync();  // the tiles are rewritten by the next group
