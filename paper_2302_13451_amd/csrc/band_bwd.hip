@@ -1461,28 +1461,32 @@ struct PaperBwdDev {
   float scale, scale_log2, log2_scale;
 };
 
-// One workgroup of 16 waves per (sequence, head, 64-frame tile). LDS holds the
-// key and value bands of channel A (origin f0 - A - Lb, staged once) and the
-// query and dout bands (origin f0) of two output channels at a time, with -D
-// and lse log2(e) of both. The outputs are taken in pairs (2p, 2p + 1): waves
-// 0-3 / 4-7 take the query role of the pair's first / second output, waves
-// 8-11 / 12-15 the key role, accumulating over the pairs; at the end waves
-// 12-15 hand their sums to waves 8-11, which store dk[A] and dv[A].
+// The band pass pipelined over the output channels: one workgroup of 12 waves
+// per (sequence, head, 64-frame tile). LDS holds the key and value bands of
+// channel A (origin f0 - A - Lb, staged once) and the query and dout bands
+// (origin f0) of two channels, a double buffer, each with -D and lse log2(e)
+// of its rows. While waves 0-3 take the query role of channel c (dq[c], band
+// part) and waves 4-7 its key role (accumulating dk[A] and dv[A] over the
+// channels in registers), waves 8-11 copy the bands of channel c + 1 into the
+// other buffer and form its statistics from the out rows they load alongside
+// (each loader the 16-row blocks it copied itself, after its own vmcnt wait);
+// one barrier per channel. Band rows outside the sequence hold copies of its
+// first or last frame (finite data): key rows are masked by the window
+// tests, query rows by lse = +inf. Three waves per SIMD leave the roles the
+// registers to issue every operand read of a sub-block first.
 template <int D>
-__global__ __launch_bounds__(1024) void llsa_paper_bwd_band_kernel(PaperBwdDev a) {
-  constexpr int NT = 1024;
+__global__ __launch_bounds__(768) void llsa_paper_bwd_band_pipe_kernel(PaperBwdDev a) {
+  constexpr int NT = 768;
   constexpr int SEG = Seg<D>::kRows;
   constexpr int NS = D / 32, NB = D / 16;
-  constexpr int NB16 = SEG / 16;
-  constexpr int BPW = (2 * NB16 + 15) / 16;
-  static_assert(SEG % 16 == 0, "the D product covers the band in 16-row blocks");
-  static_assert(4 * 64 * 2 * NB * 4 * 2 <= 6 * SEG * D, "the key-role hand-over fits the bands");
+  constexpr int NB16 = SEG / 16;              // 16-row blocks of a band
+  constexpr int BPL = (NB16 + 3) / 4;         // ... per loader wave
+  constexpr int CPR = D / 8, RPI = 64 / CPR;  // 16-byte pieces per row, rows per copy instruction
+  static_assert(SEG % 16 == 0 && 16 % RPI == 0, "bands are copied in 16-row blocks");
   __shared__ __attribute__((aligned(128))) uint16_t s_band[6 * SEG * D];
-  __shared__ __attribute__((aligned(16))) float s_stat[4 * SEG];
-  // bands: q, dout of slot 0; q, dout of slot 1; k, v of channel A
+  __shared__ __attribute__((aligned(16))) float s_stat[4 * SEG];  // -D and lse log2(e) of buffers 0, 1
+  // bands: q, dout of buffer 0; q, dout of buffer 1; k, v of channel A
   auto band = [&](int x) { return s_band + x * SEG * D; };
-  auto s_qb = [&](int j) { return band(2 * j); };
-  auto s_db = [&](int j) { return band(2 * j + 1); };
 
   int bh, tile;
   if (!xcd_slice_item(blockIdx.x, a.B * a.H, a.ntiles, bh, tile)) return;
@@ -1503,109 +1507,113 @@ __global__ __launch_bounds__(1024) void llsa_paper_bwd_band_kernel(PaperBwdDev a
   }
   const size_t slice = row_index(b, 0, h, T, H, D);
   const int fs = H * D;
-  const int koff = -(A + a.Lb);  // key band origin relative to f0 (the query bands start at f0)
+  const int koff = -(A + a.Lb);  // key band origin relative to f0
   const int kbase = f0 + koff;
-  const int kblo = max(0, -kbase), kbhi = min(SEG, len - kbase);
-  const int qbhi = min(SEG, len - f0);
-  seg_issue_rows<D, 16>(band(4), a.k + A * cs + slice, fs, kbase, kblo, kbhi, w, lane);
-  seg_issue_rows<D, 16>(band(5), a.v + A * cs + slice, fs, kbase, kblo, kbhi, w, lane);
+  const int last = len - 1;
 
-  const int wq = w & 3, role = w >> 2;  // 0, 1: query role of slot role; 2, 3: key role of slot role - 2
+  if (w >= 8) {
+    // the loaders share each SIMD with two compute waves: at a higher issue
+    // priority their few instructions go out as soon as they are ready
+    __builtin_amdgcn_s_setprio(3);
+    const int lw = w - 8;
+    // band rows of the 16-row blocks lw, lw + 4, ...: frame base + r (clamped
+    // into the sequence) into row r of X
+    auto copy_band = [&](uint16_t* X, const uint16_t* src, int base) {
+      const int rl = lane / CPR, pp = lane % CPR;
+      for (int rb = lw; rb < NB16; rb += 4)
+#pragma unroll
+        for (int u = 0; u < 16 / RPI; ++u) {
+          const int r = 16 * rb + RPI * u + rl;
+          const int fr = min(max(base + r, 0), last);
+          const int off = fr * fs + 8 * (pp ^ seg_swizzle<D>(r));
+          __builtin_amdgcn_global_load_lds(src + off, X + (16 * rb + RPI * u) * D, 16, 0, 0);
+        }
+    };
+    // out rows (lane (g, col): features 32 s + 8 g .. + 7 of row 16 rb + col)
+    // and lse of the same blocks of channel c's query band
+    bf16x8 of[BPL][NS];
+    float lsev[BPL];
+    auto load_regs = [&](int c) {
+      const uint16_t* o = a.o + c * cs + slice;
+      const float* lp = a.lse + c * a.lstride + (static_cast<size_t>(b) * H + h) * T;
+#pragma unroll
+      for (int jj = 0; jj < BPL; ++jj) {
+        const int rb = lw + 4 * jj;
+        if (rb < NB16) {
+          const int fr = min(f0 + 16 * rb + col, last);
+#pragma unroll
+          for (int s = 0; s < NS; ++s) of[jj][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
+          lsev[jj] = lp[fr];
+        }
+      }
+    };
+    // -D = -(dout . out) and lse log2(e) (+inf past the sequence's end) of the
+    // loader's rows of buffer j, whose dout rows its own copies put there
+    auto stats = [&](int j) {
+      const uint16_t* db = band(2 * j + 1);
+      float* ndn = s_stat + 2 * SEG * j;
+#pragma unroll
+      for (int jj = 0; jj < BPL; ++jj) {
+        const int rb = lw + 4 * jj;
+        if (rb < NB16) {
+          const int r = 16 * rb + col;
+          float dp = 0.f;
+#pragma unroll
+          for (int s = 0; s < NS; ++s) dp = dot_bf16x8(seg_row8<D>(db, r, 32 * s + 8 * g), of[jj][s], dp);
+          const float dg = sum_over_column(dp);
+          if (g == 0) {
+            ndn[r] = -dg;
+            ndn[SEG + r] = f0 + r < len ? lsev[jj] * kLog2e : __builtin_huge_valf();
+          }
+        }
+      }
+    };
+    copy_band(band(4), a.k + A * cs + slice, kbase);
+    copy_band(band(5), a.v + A * cs + slice, kbase);
+    load_regs(0);
+    copy_band(band(0), a.q + slice, f0);
+    copy_band(band(1), a.dout + slice, f0);
+    for (int c = 0; c <= A; ++c) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): channel c's copies and loads are in
+      stats(c & 1);
+      // channel c is complete, and the compute waves are done with channel
+      // c - 1, whose buffer the copies of channel c + 1 reuse
+      barrier_lgkm();
+      if (c + 1 <= A) {
+        const int j = (c + 1) & 1;
+        load_regs(c + 1);
+        copy_band(band(2 * j), a.q + (c + 1) * cs + slice, f0);
+        copy_band(band(2 * j + 1), a.dout + (c + 1) * cs + slice, f0);
+      }
+    }
+    return;
+  }
+
+  const int wq = w & 3;
   const int r0 = f0 + 16 * wq;
   const bool valid = r0 + col < len;
   const int nrows = min(16, T - r0);
-  const int npairs = A / 2 + 1;
-  // stages the query bands and statistics of pair p; every wave runs it, with
-  // the same barriers, in either role's loop
-  auto stage_pair = [&](int p) {
-    const int c0 = 2 * p;
-    const bool two = c0 + 1 <= A;
-    if (p > 0) __syncthreads();  // every wave is done with the previous pair's bands
-    for (int j = 0; j < (two ? 2 : 1); ++j) {
-      seg_issue_rows<D, 16>(s_qb(j), a.q + (c0 + j) * cs + slice, fs, f0, 0, qbhi, w, lane);
-      seg_issue_rows<D, 16>(s_db(j), a.dout + (c0 + j) * cs + slice, fs, f0, 0, qbhi, w, lane);
-    }
-    // out rows of both query bands as the B operand of the D products (zero
-    // outside the sequence): wave w takes the 16-row blocks w, w + 16, ...
-    bf16x8 of[BPW][NS];
-#pragma unroll
-    for (int i = 0; i < BPW; ++i) {
-      const int blk = w + 16 * i;
-      const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
-      const int fr = f0 + 16 * rb + col;
-      const bool in = blk < 2 * NB16 && (jb == 0 || two) && fr < len;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        of[i][s] = bf16x8{};
-        if (in) of[i][s] = __builtin_bit_cast(bf16x8, ld16(a.o + (c0 + jb) * cs + slice + (fr * fs + 32 * s + 8 * g)));
-      }
-    }
-    float lsev = 0.f;
-    const int lj = tid >= SEG ? 1 : 0, lr = tid - lj * SEG;
-    const int lfr = f0 + lr;
-    const bool lin = tid < 2 * SEG && (lj == 0 || two) && lfr < len;
-    if (lin) lsev = a.lse[(c0 + lj) * a.lstride + (static_cast<size_t>(b) * H + h) * T + lfr];
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (p == 0) {  // rows outside the sequence stay zero: no later load writes them
-      if (kblo > 0) {
-        seg_zero_rows<D, NT>(band(4), 0, min(kblo, SEG), tid);
-        seg_zero_rows<D, NT>(band(5), 0, min(kblo, SEG), tid);
-      }
-      if (kbhi < SEG) {
-        seg_zero_rows<D, NT>(band(4), max(kbhi, 0), SEG, tid);
-        seg_zero_rows<D, NT>(band(5), max(kbhi, 0), SEG, tid);
-      }
-      if (qbhi < SEG)
-        for (int x = 0; x < 4; ++x) seg_zero_rows<D, NT>(band(x), qbhi, SEG, tid);
-      __syncthreads();
-    }
-    if (tid < 2 * SEG) s_stat[2 * SEG * lj + SEG + lr] = lin ? lsev * kLog2e : __builtin_huge_valf();
-#pragma unroll
-    for (int i = 0; i < BPW; ++i) {
-      const int blk = w + 16 * i;
-      if (blk < 2 * NB16) {
-        const int jb = blk >= NB16 ? 1 : 0, rb = blk - jb * NB16;
-        f32x4 dd = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(seg_row8<D>(s_db(jb), 16 * rb + col, 32 * s + 8 * g), of[i][s],
-                                                       dd, 0, 0, 0);
-        const int e = col & 3;
-        const float dg = e == 0 ? dd[0] : e == 1 ? dd[1] : e == 2 ? dd[2] : dd[3];
-        if ((col >> 2) == g) s_stat[2 * SEG * jb + 16 * rb + col] = -dg;
-      }
-    }
-    __syncthreads();
-  };
-  const int j = role & 1;
-  auto bands_of = [&]() {
-    return BwdBands<D, SEG>{s_qb(j), s_db(j), band(4), band(5), s_stat + 2 * SEG * j, s_stat + 2 * SEG * j + SEG,
-                            f0, kbase, 0};
-  };
   // segment c: window t + lo .. t + hi with lo = c - A - Lb, hi = c - A (the
-  // role functions' Lb = -lo, La = hi); an odd channel count leaves the last
-  // pair's second slot empty
-  f32x4* s_red = reinterpret_cast<f32x4*>(s_band);
-  const int ri = wq * 64 + lane;
-  if (role < 2) {
+  // role functions' Lb = -lo, La = hi)
+  auto bands_of = [&](int c) {
+    const int j = c & 1;
+    return BwdBands<D, SEG>{band(2 * j), band(2 * j + 1), band(4), band(5), s_stat + 2 * SEG * j,
+                            s_stat + 2 * SEG * j + SEG, f0, kbase, 0};
+  };
+  if (w < 4) {
     const int c_own = 16 * wq + col;  // query band row of frame r0 + col
     const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
-    for (int p = 0; p < npairs; ++p) {
-      stage_pair(p);
-      const int c = 2 * p + j;
-      if (c > A) continue;
+    for (int c = 0; c <= A; ++c) {
+      lds_barrier();  // channel c is in buffer c % 2
       const int lo = c - A - a.Lb, hi = c - A;
-      f32x4 aq[NB];
       const int rel = lo - koff;  // key band row of the first key of query f0 (= c)
       const int sbs = rel & ~15;
       const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
-      bwd_query_role<D, SEG, false, false>(bands_of(), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own, c_own, r0, wq,
-                                           len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
+      f32x4 aq[NB];
+      bwd_query_role<D, SEG, true, false>(bands_of(c), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own, c_own, r0,
+                                          wq, len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
       store_rows_direct<D>(a.dq + c * cs + slice, fs, r0, nrows, aq, 1.f, valid, lane);
     }
-    __syncthreads();  // the key roles' hand-over (two barriers)
-    __syncthreads();
   } else {
     const int c_own = 16 * wq + col - koff;  // key band row of frame r0 + col
     const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
@@ -1615,36 +1623,17 @@ __global__ __launch_bounds__(1024) void llsa_paper_bwd_band_kernel(PaperBwdDev a
       const int rel = -hi;  // query band row of the first query that sees key f0 (= A - c)
       const int sbs = rel & ~15;
       const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
-      bwd_key_role<D, SEG, false, decltype(acc)::value>(bands_of(), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own,
-                                                        r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk, sbs);
+      bwd_key_role<D, SEG, true, decltype(acc)::value>(bands_of(c), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own,
+                                                       r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk, sbs);
     };
-    stage_pair(0);  // the first pair's slots both hold an output (A >= 1)
-    key_role(j, std::false_type{});
-    for (int p = 1; p < npairs; ++p) {
-      stage_pair(p);
-      const int c = 2 * p + j;
-      if (c <= A) key_role(c, std::true_type{});
+    lds_barrier();  // channel 0
+    key_role(0, std::false_type{});
+    for (int c = 1; c <= A; ++c) {
+      lds_barrier();
+      key_role(c, std::true_type{});
     }
-    // waves 12-15 hand their sums to waves 8-11 (A >= 1: both slots of the
-    // first pair hold an output, so both sets are initialised)
-    __syncthreads();
-    if (role == 3) {
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        s_red[(2 * i) * 256 + ri] = adv[i];
-        s_red[(2 * i + 1) * 256 + ri] = adk[i];
-      }
-    }
-    __syncthreads();
-    if (role == 2) {
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        adv[i] += s_red[(2 * i) * 256 + ri];
-        adk[i] += s_red[(2 * i + 1) * 256 + ri];
-      }
-      store_rows_direct<D>(a.dv + A * cs + slice, fs, r0, nrows, adv, 1.f, valid, lane);
-      store_rows_direct<D>(a.dk + A * cs + slice, fs, r0, nrows, adk, a.scale, valid, lane);
-    }
+    store_rows_direct<D>(a.dv + A * cs + slice, fs, r0, nrows, adv, 1.f, valid, lane);
+    store_rows_direct<D>(a.dk + A * cs + slice, fs, r0, nrows, adk, a.scale, valid, lane);
   }
 }
 
@@ -1690,9 +1679,9 @@ hipError_t launch_llsa_paper_backward_band(const LlsaPaperBwdArgs& x, hipStream_
   a.log2_scale = -0.5f * log2f(static_cast<float>(x.d));
   const int grid = xcd_slice_grid(x.B * x.H, a.ntiles);
   if (x.d == 64)
-    hipLaunchKernelGGL(llsa_paper_bwd_band_kernel<64>, dim3(grid), dim3(1024), 0, stream, a);
+    hipLaunchKernelGGL(llsa_paper_bwd_band_pipe_kernel<64>, dim3(grid), dim3(768), 0, stream, a);
   else
-    hipLaunchKernelGGL(llsa_paper_bwd_band_kernel<32>, dim3(grid), dim3(1024), 0, stream, a);
+    hipLaunchKernelGGL(llsa_paper_bwd_band_pipe_kernel<32>, dim3(grid), dim3(768), 0, stream, a);
   return hipGetLastError();
 }
 
