@@ -979,8 +979,17 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   const int bl = 48 + kSub * nblk;                     // band rows of a tile (<= SEG)
   const SeqTable<1> st(a.lengths, a.B, T, H, lane);
   const int nsteps = st.total();
-  const int g0 = static_cast<int>(static_cast<long long>(blockIdx.x) * nsteps / G);
-  const int g1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * nsteps / G);
+  // Shares in XCD-major order (block bid runs on XCD bid % 8), so that
+  // neighbouring shares run on one XCD, and every other share walked
+  // backwards: the two workgroups of a boundary read the band rows around it
+  // (the halo of each one's first or last tile) at the same time, at the
+  // start or at the end of the launch, and the second read hits that XCD's
+  // L2.
+  const int sid = G % 8 == 0 ? static_cast<int>(blockIdx.x % 8) * (G / 8) + static_cast<int>(blockIdx.x / 8)
+                             : static_cast<int>(blockIdx.x);
+  const bool rev = (sid & 1) == 0;
+  const int g0 = static_cast<int>(static_cast<long long>(sid) * nsteps / G);
+  const int g1 = static_cast<int>(static_cast<long long>(sid + 1) * nsteps / G);
 
   if (w >= 8) {
     // the loaders share each SIMD with two compute waves: at a higher issue
@@ -991,66 +1000,80 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
       zero_padding_tiles<D, 256>(a, st, G, tid - 512);
       return;
     }
-    // A tile that continues its predecessor needs only its last 64 band rows;
-    // one that starts a (sequence, head) goes behind its predecessor's band
-    // and needs all bl of them. Those are loaded over two steps where the
-    // ring has room: the first bl - 64 one tile early (with the predecessor's
-    // new rows, when the predecessor continues its own predecessor or is the
-    // workgroup's first tile), so that no step loads more than a continuing
-    // tile's 64 rows plus that early part. Tile t's band and its successor's
-    // new rows take rows slot .. slot + bl + 64 of the ring, the early rows of
-    // the tile after at most up to slot + 2 bl <= RR.
-    auto wrap = [&](int x) { return x >= RR ? x - RR : x; };
+    // A tile that continues its predecessor needs only the 64 band rows past
+    // the predecessor's band (its last 64 walking forwards, its first 64
+    // walking backwards: band row r of a tile is band row r + 64 of the next
+    // tile back); one that starts a (sequence, head) goes behind (ahead of)
+    // its predecessor's band and needs all bl of them. Those are loaded over
+    // two steps where the ring has room: the other bl - 64 one tile early
+    // (with the predecessor's new rows, when the predecessor continues its
+    // own predecessor or is the workgroup's first tile), so that no step
+    // loads more than a continuing tile's 64 rows plus that early part. Tile
+    // t's band, its successor's new rows and the early rows of the tile after
+    // span 2 bl <= RR rows of the ring.
+    auto wrap = [&](int x) { return x >= RR ? x - RR : (x < 0 ? x + RR : x); };
+    auto step = [&](TileCursor<1>& c) {
+      if (rev)
+        c.prev(st, H);
+      else
+        c.next(st, H, a.B);
+    };
+    // the 64 rows a continuing tile adds, and the early part of a restart
+    const int tlo = rev ? 0 : bl - kC, thi = rev ? kC : bl;
+    const int elo = rev ? kC : 0, ehi = rev ? bl : bl - kC;
     RingRegs<D, SEG> rg;       // rows of tile ca
     RingRegs<D, SEG - kC> re;  // early rows of tile cb
     TileCursor<1> ca, cb;      // ca: tile t; cb: tile t + 1 when its early rows are loaded
-    ca.seek(st, g0);
-    int sa = 0, lo_a = 0, sb = 0;  // slots, and the first row of tile t loaded in its step
-    bool eb = false;               // tile t + 1's early rows are loaded
+    ca.seek(st, rev ? g1 - 1 : g0);
+    int sa = 0, lo_a = 0, hi_a = bl, sb = 0;  // slots, and the rows of tile t loaded in its step
+    bool eb = false;                          // tile t + 1's early rows are loaded
     ring_load_regs<D, SEG>(a, ca, 0, bl, lw, lane, rg);
     ring_copy<D, SEG>(a, ca, s_ring, sa, 0, bl, lw, lane);
     if (g0 + 1 < g1) {
       cb = ca;
-      cb.next(st, H, a.B);
-      if (cb.tile == 0) {
+      step(cb);
+      if (rev ? ca.tile == 0 : cb.tile == 0) {
         eb = true;
-        sb = wrap(sa + bl);
-        ring_load_regs<D, SEG - kC>(a, cb, 0, bl - kC, lw, lane, re);
-        ring_copy<D, SEG>(a, cb, s_ring, sb, 0, bl - kC, lw, lane);
+        sb = wrap(rev ? sa - bl : sa + bl);
+        ring_load_regs<D, SEG - kC>(a, cb, elo, ehi, lw, lane, re);
+        ring_copy<D, SEG>(a, cb, s_ring, sb, elo, ehi, lw, lane);
       }
     }
     for (int t = g0; t < g1; ++t) {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the step's copies and loads are in
-      ring_stats<D, SEG>(rg, s_ring + RR * D, s_ndn, s_lse2, sa, ca.tile * kC - La, ca.len, lo_a, bl, lw, lane);
+      ring_stats<D, SEG>(rg, s_ring + RR * D, s_ndn, s_lse2, sa, ca.tile * kC - La, ca.len, lo_a, hi_a, lw, lane);
       if (eb)
-        ring_stats<D, SEG>(re, s_ring + RR * D, s_ndn, s_lse2, sb, cb.tile * kC - La, cb.len, 0, bl - kC, lw, lane);
+        ring_stats<D, SEG>(re, s_ring + RR * D, s_ndn, s_lse2, sb, cb.tile * kC - La, cb.len, elo, ehi, lw, lane);
       // tile t is complete in the rings, and the compute waves are done with
       // tile t - 1, whose rows the copies of the next step may reuse
       barrier_lgkm();
       if (t + 1 < g1) {
         TileCursor<1> cn = ca;  // tile t + 1
-        cn.next(st, H, a.B);
-        const int sn = wrap(sa + (cn.tile > 0 ? kC : bl));
-        const int lo_n = (cn.tile > 0 || eb) ? bl - kC : 0;
+        step(cn);
+        const bool cont = rev ? ca.tile > 0 : cn.tile > 0;
+        const int sn = wrap(rev ? sa - (cont ? kC : bl) : sa + (cont ? kC : bl));
+        const bool part = cont || eb;
+        const int lo_n = part ? tlo : 0, hi_n = part ? thi : bl;
         // register loads first: the compiler orders them after every older
         // load that wrote the same registers
-        ring_load_regs<D, SEG>(a, cn, lo_n, bl, lw, lane, rg);
-        ring_copy<D, SEG>(a, cn, s_ring, sn, lo_n, bl, lw, lane);
+        ring_load_regs<D, SEG>(a, cn, lo_n, hi_n, lw, lane, rg);
+        ring_copy<D, SEG>(a, cn, s_ring, sn, lo_n, hi_n, lw, lane);
         bool en = false;
         int snn = 0;
         TileCursor<1> cnn = cn;  // tile t + 2
-        if (t + 2 < g1 && cn.tile > 0) {
-          cnn.next(st, H, a.B);
-          if (cnn.tile == 0) {
+        if (t + 2 < g1 && cont) {
+          step(cnn);
+          if (rev ? cn.tile == 0 : cnn.tile == 0) {
             en = true;
-            snn = wrap(sn + bl);
-            ring_load_regs<D, SEG - kC>(a, cnn, 0, bl - kC, lw, lane, re);
-            ring_copy<D, SEG>(a, cnn, s_ring, snn, 0, bl - kC, lw, lane);
+            snn = wrap(rev ? sn - bl : sn + bl);
+            ring_load_regs<D, SEG - kC>(a, cnn, elo, ehi, lw, lane, re);
+            ring_copy<D, SEG>(a, cnn, s_ring, snn, elo, ehi, lw, lane);
           }
         }
         ca = cn;
         sa = sn;
         lo_a = lo_n;
+        hi_a = hi_n;
         cb = cnn;
         sb = snn;
         eb = en;
@@ -1070,7 +1093,7 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
   const RingLaneBase<D, RR> rb(lane, (w < 4 ? Lb : La) + 16 * wq + col);
   const int sloff = store_lane_offset<D>(fs, lane);
   TileCursor<1> cur;
-  cur.seek(st, g0);
+  cur.seek(st, rev ? g1 - 1 : g0);
   int slot = 0;
   for (int t = g0; t < g1; ++t) {
     lds_barrier();  // tile t is in the rings; the loaders then copy tile t + 1
@@ -1097,9 +1120,15 @@ __global__ __launch_bounds__(768) void sa_bwd_persist_kernel(BwdDev a) {
                                   a.log2_scale, lane, aq);
       store_rows_at<D>(a.dq + first, sloff, in_range, aq, 1.f, valid, lane);
     }
-    cur.next(st, H, a.B);
-    const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;
-    slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+    if (rev) {
+      const int dec = cur.tile > 0 ? kC : 48 + kSub * nblk;
+      cur.prev(st, H);
+      slot = slot - dec < 0 ? slot - dec + RR : slot - dec;
+    } else {
+      cur.next(st, H, a.B);
+      const int inc = cur.tile > 0 ? kC : 48 + kSub * nblk;
+      slot = slot + inc >= RR ? slot + inc - RR : slot + inc;
+    }
   }
 }
 

@@ -623,6 +623,27 @@ struct TileCursor {
     } while (nt == 0);
     len = b < B ? st.len(b) : 1;
   }
+  // the step before (one tile per step only): the previous tile of the
+  // (sequence, head), or the last tile of the one before
+  __device__ __forceinline__ void prev(const SeqTable<TPS>& st, int H) {
+    static_assert(TPS == 1, "a cursor walks back one tile at a time");
+    if (tile > 0) {
+      --tile;
+      return;
+    }
+    if (h > 0) {
+      --h;
+      tile = nt - 1;
+      return;
+    }
+    h = H - 1;
+    do {
+      --b;
+      nt = b >= 0 ? st.nt(b) : 1;
+    } while (nt == 0);
+    len = b >= 0 ? st.len(b) : 1;
+    tile = nt - 1;
+  }
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
