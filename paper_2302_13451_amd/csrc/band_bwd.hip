@@ -1218,6 +1218,7 @@ struct LlsaBwdDev {
   int lo[2][2], hi[2][2];  // segment (output j, branch i); lo > hi: empty
   int qoff[2];             // frame of query band j's row 0, relative to the tile's first frame
   int koff[2];             // frame of key band i's row 0, relative to the tile's first frame
+  int krows[2];            // rows of key band i that some wave reads (<= the band's SEG rows)
 };
 
 // One workgroup of 16 waves per (sequence, head, 64-frame tile). LDS holds
@@ -1274,7 +1275,7 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
     blo[j] = max(0, -qbase[j]);
     bhi[j] = min(SEG, len - qbase[j]);
     blo[2 + j] = max(0, -kbase[j]);
-    bhi[2 + j] = min(SEG, len - kbase[j]);
+    bhi[2 + j] = min(a.krows[j], len - kbase[j]);
   }
   for (int j = 0; j < 2; ++j) {
     seg_issue_rows<D, 16>(s_qb(j), a.q[j] + slice, fs, qbase[j], blo[j], bhi[j], w, lane);
@@ -1309,8 +1310,9 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
 #pragma unroll
   for (int x = 0; x < 8; ++x) {
     const int bi = x < 4 ? x / 2 : 2 + (x - 4) / 2;  // its row range: query band j or key band 2 + i
-    if (blo[bi] > 0) seg_zero_rows<D, NT>(band(x), 0, min(blo[bi], SEG), tid);
-    if (bhi[bi] < SEG) seg_zero_rows<D, NT>(band(x), max(bhi[bi], 0), SEG, tid);
+    const int rows = x < 4 ? SEG : a.krows[bi - 2];  // the rows any wave reads
+    if (blo[bi] > 0) seg_zero_rows<D, NT>(band(x), 0, min(blo[bi], rows), tid);
+    if (bhi[bi] < rows) seg_zero_rows<D, NT>(band(x), max(bhi[bi], 0), rows, tid);
   }
   __syncthreads();
   if (tid < 2 * SEG) s_stat[2 * SEG * lj + SEG + lr] = lin ? lsev * kLog2e : __builtin_huge_valf();
@@ -1369,30 +1371,41 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
     __syncthreads();  // the key roles' hand-over (two barriers)
     __syncthreads();
   } else {
-    // branch L's key role is split by output: waves 8-11 take branch C (both
-    // outputs, stored) and then branch L's output-0 segment, waves 12-15 its
-    // output-1 segment, and hand their sum to waves 8-11 at the end
+    // branch L's key role is split between the two groups of waves so that
+    // each takes about the same number of sub-blocks: waves 8-11 take branch
+    // C (both outputs, stored) and then the first two sub-blocks of branch
+    // L's output-0 segment, waves 12-15 the rest of that segment and the
+    // output-1 segment, and hand their sum to waves 8-11 at the end (with no
+    // branch C, waves 8-11 take the whole output-0 segment)
     f32x4 adv[NB], adk[NB];
-    auto key_role = [&](int j, int i, auto acc) {
+    // sub-blocks m0 .. m0 + cnt - 1 of segment (j, i) (cnt < 0: to the last)
+    auto key_role = [&](int j, int i, int m0, int cnt, auto acc) {
       const int c_own = 16 * wq + col - a.koff[i];  // key band row of frame r0 + col
       const uint32_t own = 2u * static_cast<uint32_t>(seg_row_off<D>(c_own, g));
       const int lo = a.lo[j][i], hi = a.hi[j][i];
       const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f0
-      const int sbs = rel & ~15;
-      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+      const int sbs = (rel & ~15) + kSub * m0;
+      const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub - m0;
+      const int n = cnt < 0 || cnt > nblk ? nblk : cnt;
       bwd_key_role<D, SEG, false, decltype(acc)::value>(bands_of(j, i), SubBlockAddr<D, SEG>(lane, 16 * wq + sbs), own,
-                                                        r0, wq, len, -lo, hi, nblk, a.scale_log2, lane, adv, adk, sbs);
+                                                        r0, wq, len, -lo, hi, n, a.scale_log2, lane, adv, adk, sbs);
     };
+    const int lo01 = a.lo[0][1], hi01 = a.hi[0][1], rel01 = -hi01 - a.qoff[0];
+    const int nblk01 = (16 + hi01 - lo01 + (rel01 & 15) + kSub - 1) / kSub;
+    const int split = has_c && nblk01 > 2 ? 2 : nblk01;  // output-0 sub-blocks of waves 8-11
     if (role == 2) {
       if (has_c) {
-        key_role(0, 0, std::false_type{});
-        key_role(1, 0, std::true_type{});
+        key_role(0, 0, 0, -1, std::false_type{});
+        key_role(1, 0, 0, -1, std::true_type{});
       }
       store_rows_direct<D>(a.dv[0] + slice, fs, r0, nrows, adv, 1.f, valid && has_c, lane);
       store_rows_direct<D>(a.dk[0] + slice, fs, r0, nrows, adk, a.scale, valid && has_c, lane);
-      key_role(0, 1, std::false_type{});
+      key_role(0, 1, 0, split, std::false_type{});
+    } else if (split < nblk01) {
+      key_role(0, 1, split, -1, std::false_type{});
+      key_role(1, 1, 0, -1, std::true_type{});
     } else {
-      key_role(1, 1, std::false_type{});
+      key_role(1, 1, 0, -1, std::false_type{});
     }
     __syncthreads();  // every wave is done with the bands: their space takes the hand-over
     f32x4* s_red = reinterpret_cast<f32x4*>(s_band);
@@ -1463,6 +1476,20 @@ bool llsa_bwd_geometry(int d, int Lb, int La, LlsaBwdDev& a) {
     }
   for (int i = 0; i < 2; ++i)
     if (64 - a.koff[i] > seg_rows || 64 - a.qoff[i] > seg_rows) return false;
+  // the rows of each key band that some wave reads: its own 64 and the
+  // query roles' sub-blocks (branch C's short segments need about half the
+  // band, so only those rows are staged)
+  for (int i = 0; i < 2; ++i) {
+    int rows = 64 - a.koff[i];
+    for (int j = 0; j < 2; ++j) {
+      if (a.lo[j][i] > a.hi[j][i]) continue;
+      const int rel = a.lo[j][i] - a.koff[i];
+      const int nb = (16 + a.hi[j][i] - a.lo[j][i] + (rel & 15) + kSub - 1) / kSub;
+      const int r = 48 + (rel & ~15) + kSub * nb;
+      rows = rows > r ? rows : r;
+    }
+    a.krows[i] = rows;
+  }
   return true;
 }
 
