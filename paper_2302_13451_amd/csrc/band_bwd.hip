@@ -1219,6 +1219,7 @@ struct LlsaBwdDev {
   int qoff[2];             // frame of query band j's row 0, relative to the tile's first frame
   int koff[2];             // frame of key band i's row 0, relative to the tile's first frame
   int krows[2];            // rows of key band i that some wave reads (<= the band's SEG rows)
+  int bq[2], bk[2];        // persistent kernel: rows of query band j and key band i per 32-frame step
 };
 
 // One workgroup of 16 waves per (sequence, head, 64-frame tile). LDS holds
@@ -1427,6 +1428,342 @@ __global__ __launch_bounds__(1024) void llsa_bwd_tile_kernel(LlsaBwdDev a) {
       store_rows_direct<D>(a.dv[1] + slice, fs, r0, nrows, adv, 1.f, valid, lane);
       store_rows_direct<D>(a.dk[1] + slice, fs, r0, nrows, adk, a.scale, valid, lane);
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent two-branch LLSA backward for up to 64 sequences (d = 64). The
+// eight bands of the tile kernel above live in LDS rings that advance by 32
+// frames per step: the query and dout bands of both outputs and branch L's key
+// and value band in rings of kLlsaRingL rows, branch C's in rings of
+// kLlsaRingC rows. A step that continues its predecessor in the same
+// (sequence, head) copies only the 32 rows past the predecessor's bands, while
+// the predecessor is computed; a step that starts a (sequence, head) copies its
+// whole bands once the predecessor's roles are done with the rings. One
+// workgroup per compute unit walks a contiguous share of the 64-frame tiles,
+// two steps per tile:
+//   * waves 8-11 (the loaders) issue the direct copies, and form -D and
+//     lse log2(e) of the new query-band rows of both outputs (the dout rows
+//     they copied themselves, out rows and lse loaded into registers);
+//   * waves 0-1 / 2-3 take the query roles of output 0 / 1 (branch L's
+//     segment, then branch C's), 16 queries each;
+//   * waves 4-5 take branch C's key role (both outputs, stored) and the first
+//     two sub-blocks of branch L's output-0 segment, waves 6-7 the rest of that
+//     segment and branch L's output-1 segment, 16 keys each; waves 6-7 hand
+//     their sums to waves 4-5 through LDS, rounded to bfloat16.
+// Two barriers per step: the step's rows are in (and the previous step's
+// roles are done), and the roles are done with the rings (the hand-over).
+constexpr int kLlsaRingL = 160, kLlsaRingC = 96;
+constexpr int kLlsaStep = 32;  // frames per step of the persistent kernel
+
+// Band rows [rlo, bl) of one array (frame base + r, clamped into the
+// sequence) to ring rows (slot + r) mod RR in 16-row blocks; loader lw of 4
+// takes blocks lw, lw + 4, ...
+template <int D, int RR>
+__device__ __forceinline__ void lring_copy(uint16_t* ring, const uint16_t* src, int fs, int base, int last, int slot,
+                                           int rlo, int bl, int lw, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, IPB = 16 / RPI;
+  const int rl = lane / CPR, pp = lane % CPR;
+  for (int r16 = rlo + 16 * lw; r16 < bl; r16 += 64) {
+    int lr0 = slot + r16;
+    lr0 = lr0 >= RR ? lr0 - RR : lr0;
+#pragma unroll
+    for (int u = 0; u < IPB; ++u) {
+      const int r = r16 + u * RPI + rl;
+      const int off = min(max(base + r, 0), last) * fs + 8 * (pp ^ seg_swizzle<D>(lr0 + u * RPI + rl));
+      __builtin_amdgcn_global_load_lds(src + off, ring + (lr0 + u * RPI) * D, 16, 0, 0);
+    }
+  }
+}
+
+// out rows and lse values of loader lw's blocks of query-band rows [rlo, bl)
+template <int D, int ROWS>
+__device__ __forceinline__ void lring_load_regs(const uint16_t* o, const float* lse, int fs, int base, int last,
+                                                int rlo, int bl, int lw, int lane, RingRegs<D, ROWS>& rg) {
+  using R = RingRegs<D, ROWS>;
+  const int col = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int jj = 0; jj < R::BPL; ++jj) {
+    const int r16 = rlo + 16 * (lw + 4 * jj);
+    if (r16 < bl) {
+      const int fr = min(max(base + r16 + col, 0), last);
+#pragma unroll
+      for (int s = 0; s < R::NS; ++s) rg.of[jj][s] = __builtin_bit_cast(bf16x8, ld16(o + (fr * fs + 32 * s + 8 * g)));
+      rg.lse[jj] = lse[fr];
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void llsa_bwd_zero_padding(const LlsaBwdDev& a, const SeqTable<1>& st, int G, int i) {
+  const PadTable pt(st, a.B, a.H, a.ntiles, threadIdx.x & 63);
+  const int np = pt.total();
+  const int p1 = static_cast<int>(static_cast<long long>(blockIdx.x + 1) * np / G);
+  for (int p = static_cast<int>(static_cast<long long>(blockIdx.x) * np / G); p < p1; ++p) {
+    int b, h, tile;
+    pt.item(p, a.ntiles, b, h, tile);
+    const int f0 = tile * kC, f1 = min(f0 + kC, a.T);
+    for (int j = 0; j < 2; ++j) {
+      zero_rows<D, 256>(a.dk[j], a.dv[j], b, h, a.T, a.H, f0, f1, i);
+      zero_rows<D, 256>(a.dq[j], nullptr, b, h, a.T, a.H, f0, f1, i);
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
+  constexpr int NB = D / 16, RL = kLlsaRingL, RC = kLlsaRingC, ST = kLlsaStep;
+  constexpr int ROWS = RL - ST;  // most query-band rows one step copies
+  static_assert(RL % 32 == 0 && RC % 32 == 0, "the swizzle pattern must survive the wrap of a ring");
+  // q, dout of output 0; q, dout of output 1; k, v of branch L (RL rows
+  // each); k, v of branch C (RC rows each)
+  __shared__ __attribute__((aligned(128))) uint16_t s_ring[(6 * RL + 2 * RC) * D];
+  __shared__ __attribute__((aligned(16))) float s_stat[4 * RL];  // -D, lse log2(e) of query bands 0, 1
+  __shared__ __attribute__((aligned(16))) uint32_t s_hand[2 * 16 * 64];  // waves 6-7's sums, bfloat16 pairs
+  auto rq = [&](int j) { return s_ring + 2 * j * RL * D; };
+  auto rd = [&](int j) { return s_ring + (2 * j + 1) * RL * D; };
+  // key and value rings of branch i (0: C, 1: L)
+  auto rk = [&](int i) { return i ? s_ring + 4 * RL * D : s_ring + 6 * RL * D; };
+  auto rv = [&](int i) { return i ? s_ring + 5 * RL * D : s_ring + (6 * RL + RC) * D; };
+  auto ndn = [&](int j) { return s_stat + 2 * j * RL; };
+  auto lse2 = [&](int j) { return s_stat + (2 * j + 1) * RL; };
+
+  const int G = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.T, H = a.H, fs = H * D;
+  const SeqTable<1> st(a.lengths, a.B, T, H, lane);
+  const int ntl = st.total();
+  // shares in XCD-major order (block bid runs on XCD bid % 8): neighbouring
+  // shares, which share the band rows around their boundary, on one XCD
+  const int sid = G % 8 == 0 ? static_cast<int>(blockIdx.x % 8) * (G / 8) + static_cast<int>(blockIdx.x / 8)
+                             : static_cast<int>(blockIdx.x);
+  const int g0 = static_cast<int>(static_cast<long long>(sid) * ntl / G);
+  const int g1 = static_cast<int>(static_cast<long long>(sid + 1) * ntl / G);
+  const int nhs = 2 * (g1 - g0);  // steps of this workgroup
+  // the step after (c, hh): the second half of the tile, or the next tile
+  auto advance = [&](TileCursor<1>& c, int& hh) {
+    if (hh == 0) {
+      hh = 1;
+    } else {
+      hh = 0;
+      c.next(st, H, a.B);
+    }
+  };
+
+  if (w >= 8) {
+    __builtin_amdgcn_s_setprio(3);  // as in the SA kernel
+    const int lw = w - 8;
+    if (g0 < g1) {
+      RingRegs<D, ROWS> rg[2];
+      // the copies of step (c, hh) into slots sl (query and branch-L rings)
+      // and sc (branch-C rings): all band rows, or the 32 past its
+      // predecessor's
+      auto issue = [&](const TileCursor<1>& c, int hh, int sl, int sc, bool cold) {
+        const int f = c.tile * kC + ST * hh, last = c.len - 1;
+        const size_t slice = row_index(c.b, 0, c.h, T, H, D);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          lring_load_regs<D, ROWS>(a.o[j] + slice, a.lse[j] + (static_cast<size_t>(c.b) * H + c.h) * T, fs,
+                                   f + a.qoff[j], last, cold ? 0 : a.bq[j] - ST, a.bq[j], lw, lane, rg[j]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int lo = cold ? 0 : a.bq[j] - ST;
+          lring_copy<D, RL>(rq(j), a.q[j] + slice, fs, f + a.qoff[j], last, sl, lo, a.bq[j], lw, lane);
+          lring_copy<D, RL>(rd(j), a.dout[j] + slice, fs, f + a.qoff[j], last, sl, lo, a.bq[j], lw, lane);
+        }
+        {
+          const int lo = cold ? 0 : a.bk[1] - ST;
+          lring_copy<D, RL>(rk(1), a.k[1] + slice, fs, f + a.koff[1], last, sl, lo, a.bk[1], lw, lane);
+          lring_copy<D, RL>(rv(1), a.v[1] + slice, fs, f + a.koff[1], last, sl, lo, a.bk[1], lw, lane);
+        }
+        {
+          const int lo = cold ? 0 : a.bk[0] - ST;
+          lring_copy<D, RC>(rk(0), a.k[0] + slice, fs, f + a.koff[0], last, sc, lo, a.bk[0], lw, lane);
+          lring_copy<D, RC>(rv(0), a.v[0] + slice, fs, f + a.koff[0], last, sc, lo, a.bk[0], lw, lane);
+        }
+      };
+      TileCursor<1> ca;
+      ca.seek(st, g0);
+      int ha = 0, sl = 0, sc = 0;
+      bool cold = true;
+      issue(ca, ha, sl, sc, true);
+      for (int hs = 0; hs < nhs; ++hs) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): step hs's copies and loads are in
+        {
+          const int f = ca.tile * kC + ST * ha;
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            ring_stats<D, RL / 2, ROWS>(rg[j], rd(j), ndn(j), lse2(j), sl, f + a.qoff[j], ca.len,
+                                        cold ? 0 : a.bq[j] - ST, a.bq[j], lw, lane);
+        }
+        // step hs is complete in the rings, and the roles are done with step
+        // hs - 1, whose rows the copies of a continuing step hs + 1 may reuse
+        barrier_lgkm();
+        TileCursor<1> cn = ca;
+        int hn = ha;
+        advance(cn, hn);
+        const bool more = hs + 1 < nhs;
+        const bool cont = hn == 1 || cn.tile > 0;
+        const int nl = sl + ST >= RL ? sl + ST - RL : sl + ST;
+        const int nc = sc + ST >= RC ? sc + ST - RC : sc + ST;
+        if (more && cont) issue(cn, hn, nl, nc, false);
+        barrier_lgkm();  // the roles are done with the rings (the hand-over)
+        // a step that starts a (sequence, head) overwrites rows step hs used
+        if (more && !cont) issue(cn, hn, nl, nc, true);
+        ca = cn;
+        ha = hn;
+        sl = nl;
+        sc = nc;
+        cold = !cont;
+      }
+    }
+    // with nothing left to copy, the loaders write this workgroup's share of
+    // the tiles wholly past a sequence's end while the compute waves finish
+    llsa_bwd_zero_padding<D>(a, st, G, tid - 512);
+    return;
+  }
+  if (g0 >= g1) return;
+
+  const int col = lane & 15;
+  const int wq = w & 1;  // 16-row group of the step
+  const int sloff = store_lane_offset<D>(fs, lane);
+  const bool has_c = a.lo[0][0] <= a.hi[0][0];
+  const int rel01 = -a.hi[0][1] - a.qoff[0];
+  const int nblk01 = (16 + a.hi[0][1] - a.lo[0][1] + (rel01 & 15) + kSub - 1) / kSub;
+  const int split = has_c && nblk01 > 2 ? 2 : nblk01;  // output-0 branch-L sub-blocks of waves 4-5
+  // lane offsets of the sub-block reads in a ring of each size, and of the
+  // lane's own row: query role (w < 4) in its query band, key role in the key
+  // bands of both branches
+  const int jq = w >> 1;  // output of a query-role wave
+  const RingLaneBase<D, RL> rbl(lane, (w < 4 ? -a.qoff[jq & 1] : -a.koff[1]) + 16 * wq + col);
+  // (the branch-C offsets are formed where they are used: fewer registers
+  // held across the step)
+  auto rbc = [&]() { return RingLaneBase<D, RC>(lane, -a.koff[0] + 16 * wq + col); };
+  // each kind of wave runs its own loop over the steps (two barriers per
+  // step, as the loaders), so that no wave holds another kind's values
+  TileCursor<1> cur;
+  cur.seek(st, g0);
+  int hh = 0, sl = 0, sc = 0;
+  auto ring_row = [](int x, int RR) { return x >= RR ? x - RR : x; };
+  auto next_step = [&]() {
+    advance(cur, hh);
+    sl = sl + ST >= RL ? sl + ST - RL : sl + ST;
+    sc = sc + ST >= RC ? sc + ST - RC : sc + ST;
+  };
+  if (w < 4) {
+    const int j = jq;
+    for (int hs = 0; hs < nhs; ++hs) {
+      lds_barrier();  // step hs is in the rings
+      const int len = cur.len, f = cur.tile * kC + ST * hh;
+      const int r0 = f + 16 * wq;
+      const bool valid = r0 + col < len;
+      const bool in_range = col < T - r0;
+      const size_t first = row_index(cur.b, r0, cur.h, T, H, D);
+      int own_row;
+      uint32_t own;
+      rbl.own_at(sl, own_row, own);
+      f32x4 aq[NB];
+      // segment (j, i); the window of query t is t + lo .. t + hi
+      {
+        const int lo = a.lo[j][1], hi = a.hi[j][1];
+        const int rel = lo - a.koff[1];
+        const int sbs = rel & ~15;
+        const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+        const BwdBands<D, RL> bd{rq(j), rd(j), rk(1), rv(1), ndn(j), lse2(j), f + a.qoff[j], f + a.koff[1], sl};
+        bwd_query_role<D, RL, true, false>(bd, rbl.at(ring_row(sl + 16 * wq + sbs, RL)), own, own_row, r0, wq, len,
+                                            -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
+      }
+      if (has_c) {
+        const int lo = a.lo[j][0], hi = a.hi[j][0];
+        const int rel = lo - a.koff[0];
+        const int sbs = rel & ~15;
+        const int nblk = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+        const BwdBands<D, RC> bd{rq(j), rd(j), rk(0), rv(0), ndn(j), lse2(j), f + a.qoff[j], f + a.koff[0], sc};
+        bwd_query_role<D, RC, true, true>(bd, rbc().at(ring_row(sc + 16 * wq + sbs, RC)), own, own_row, r0, wq,
+                                           len, -lo, hi, nblk, a.scale_log2, a.log2_scale, lane, aq, sbs);
+      }
+      store_rows_at<D>(a.dq[j] + first, sloff, in_range, aq, 1.f, valid, lane);
+      lds_barrier();  // the hand-over
+      next_step();
+    }
+    return;
+  }
+  // key roles: sub-blocks m0 .. m0 + cnt - 1 (cnt < 0: to the last) of
+  // segment (j, i) for keys from f + 16 wq on, accumulating when ACC
+  auto krole = [&](int j, int i, int m0, int cnt, int f, int len, f32x4* adv, f32x4* adk, auto acc) {
+    const int lo = a.lo[j][i], hi = a.hi[j][i];
+    const int rel = -hi - a.qoff[j];  // query band row of the first query that sees key f
+    const int sbs = (rel & ~15) + kSub * m0;
+    const int nb = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub - m0;
+    const int n = cnt < 0 || cnt > nb ? nb : cnt;
+    int own_row;
+    uint32_t own;
+    if (i == 1)
+      rbl.own_at(sl, own_row, own);
+    else
+      rbc().own_at(sc, own_row, own);
+    const BwdBands<D, RL> bd{rq(j), rd(j), rk(i), rv(i), ndn(j), lse2(j), f + a.qoff[j], f + a.koff[i], sl};
+    bwd_key_role<D, RL, true, decltype(acc)::value>(bd, rbl.at(ring_row(sl + 16 * wq + sbs, RL)), own,
+                                                     f + 16 * wq, wq, len, -lo, hi, n, a.scale_log2, lane, adv, adk,
+                                                     sbs);
+  };
+  uint32_t* const hand = s_hand + wq * 16 * 64 + lane;
+  if (w < 6) {
+    for (int hs = 0; hs < nhs; ++hs) {
+      lds_barrier();  // step hs is in the rings
+      const int len = cur.len, f = cur.tile * kC + ST * hh;
+      const int r0 = f + 16 * wq;
+      const bool valid = r0 + col < len;
+      const bool in_range = col < T - r0;
+      const size_t first = row_index(cur.b, r0, cur.h, T, H, D);
+      f32x4 adv[NB], adk[NB];
+      if (has_c) {
+        krole(0, 0, 0, -1, f, len, adv, adk, std::false_type{});
+        krole(1, 0, 0, -1, f, len, adv, adk, std::true_type{});
+      }
+      store_rows_at<D>(a.dv[0] + first, sloff, in_range, adv, 1.f, valid && has_c, lane);
+      store_rows_at<D>(a.dk[0] + first, sloff, in_range, adk, a.scale, valid && has_c, lane);
+      krole(0, 1, 0, split, f, len, adv, adk, std::false_type{});
+      lds_barrier();  // the hand-over
+#pragma unroll
+      for (int x = 0; x < NB; ++x) {
+        const uint32_t pv0 = hand[64 * (4 * x)], pv1 = hand[64 * (4 * x + 1)];
+        const uint32_t pk0 = hand[64 * (4 * x + 2)], pk1 = hand[64 * (4 * x + 3)];
+        adv[x][0] += __uint_as_float(pv0 << 16);
+        adv[x][1] += __uint_as_float(pv0 & 0xffff0000u);
+        adv[x][2] += __uint_as_float(pv1 << 16);
+        adv[x][3] += __uint_as_float(pv1 & 0xffff0000u);
+        adk[x][0] += __uint_as_float(pk0 << 16);
+        adk[x][1] += __uint_as_float(pk0 & 0xffff0000u);
+        adk[x][2] += __uint_as_float(pk1 << 16);
+        adk[x][3] += __uint_as_float(pk1 & 0xffff0000u);
+      }
+      store_rows_at<D>(a.dv[1] + first, sloff, in_range, adv, 1.f, valid, lane);
+      store_rows_at<D>(a.dk[1] + first, sloff, in_range, adk, a.scale, valid, lane);
+      next_step();
+    }
+    return;
+  }
+  for (int hs = 0; hs < nhs; ++hs) {
+    lds_barrier();  // step hs is in the rings
+    const int len = cur.len, f = cur.tile * kC + ST * hh;
+    f32x4 adv[NB], adk[NB];
+    if (split < nblk01) {
+      krole(0, 1, split, -1, f, len, adv, adk, std::false_type{});
+      krole(1, 1, 0, -1, f, len, adv, adk, std::true_type{});
+    } else {
+      krole(1, 1, 0, -1, f, len, adv, adk, std::false_type{});
+    }
+#pragma unroll
+    for (int x = 0; x < NB; ++x) {
+      hand[64 * (4 * x)] = pack_bf16x2(adv[x][0], adv[x][1]);
+      hand[64 * (4 * x + 1)] = pack_bf16x2(adv[x][2], adv[x][3]);
+      hand[64 * (4 * x + 2)] = pack_bf16x2(adk[x][0], adk[x][1]);
+      hand[64 * (4 * x + 3)] = pack_bf16x2(adk[x][2], adk[x][3]);
+    }
+    lds_barrier();  // the hand-over
+    next_step();
   }
 }
 
@@ -1741,6 +2078,37 @@ hipError_t launch_llsa_paper_backward_band(const LlsaPaperBwdArgs& x, hipStream_
   return hipGetLastError();
 }
 
+// Rows of each band per 32-frame step of the persistent kernel (two 16-row
+// groups: 16 + sbs + 32 nblk for each sweep, and the 32 own rows), in whole
+// 16-row blocks; false when a band and the next step's 32 rows do not fit its
+// ring. Needs the segments and origins of llsa_bwd_geometry.
+static bool llsa_bwd_ring_geometry(LlsaBwdDev& a) {
+  auto need = [](int rel, int lo, int hi) {
+    const int nb = (16 + hi - lo + (rel & 15) + kSub - 1) / kSub;
+    return 16 + (rel & ~15) + kSub * nb;
+  };
+  for (int i = 0; i < 2; ++i) {
+    int rows = kLlsaStep - a.koff[i];
+    for (int j = 0; j < 2; ++j)
+      if (a.lo[j][i] <= a.hi[j][i]) {
+        const int r = need(a.lo[j][i] - a.koff[i], a.lo[j][i], a.hi[j][i]);
+        rows = rows > r ? rows : r;
+      }
+    a.bk[i] = (rows + 15) & ~15;
+  }
+  for (int j = 0; j < 2; ++j) {
+    int rows = kLlsaStep - a.qoff[j];
+    for (int i = 0; i < 2; ++i)
+      if (a.lo[j][i] <= a.hi[j][i]) {
+        const int r = need(-a.hi[j][i] - a.qoff[j], a.lo[j][i], a.hi[j][i]);
+        rows = rows > r ? rows : r;
+      }
+    a.bq[j] = (rows + 15) & ~15;
+  }
+  return a.bq[0] + kLlsaStep <= kLlsaRingL && a.bq[1] + kLlsaStep <= kLlsaRingL &&
+         a.bk[1] + kLlsaStep <= kLlsaRingL && a.bk[0] + kLlsaStep <= kLlsaRingC;
+}
+
 bool llsa_backward_fits(int d, int Lb, int La) {
   LlsaBwdDev a{};
   return llsa_bwd_geometry(d, Lb, La, a);
@@ -1771,6 +2139,10 @@ hipError_t launch_llsa_backward(const LlsaBackwardArgs& x, ElemType et, hipStrea
   a.scale = 1.f / sqrtf(static_cast<float>(x.d));
   a.scale_log2 = kLog2e * a.scale;
   a.log2_scale = -0.5f * log2f(static_cast<float>(x.d));
+  if (x.d == 64 && x.B <= kPersistMaxB && llsa_bwd_ring_geometry(a)) {
+    hipLaunchKernelGGL(llsa_bwd_ring_kernel<64>, dim3(compute_units()), dim3(768), 0, stream, a);
+    return hipGetLastError();
+  }
   const int grid = xcd_slice_grid(x.B * x.H, a.ntiles);
   if (x.d == 64)
     hipLaunchKernelGGL(llsa_bwd_tile_kernel<64>, dim3(grid), dim3(1024), 0, stream, a);

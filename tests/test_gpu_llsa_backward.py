@@ -111,6 +111,21 @@ def test_llsa_backward_padded_frames_are_never_read(oracle_mod):
             assert np.all(g[:, b, n:] == 0.0)
 
 
+# More 64-frame tiles than the persistent kernel has workgroups (256), so each
+# walks several (sequence, head) slices: steps that continue their
+# predecessor's bands and steps that start a new slice, with branch C (La > 0)
+# and without (La = 0), and windows on both sides of its ring geometry.
+@pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
+    (16, 640, 8, 64, 37, 5, (1, 640)),
+    (12, 700, 10, 64, 20, 0, (100, 700)),
+    (16, 600, 8, 64, 24, 16, (50, 600)),
+    (20, 520, 12, 64, 64, 8, (0, 520)),
+])
+def test_llsa_backward_persistent(oracle_mod, B, T, H, d, Lb, La, lengths):
+    got, ref, L = run_supplied(oracle_mod, B, T, H, d, Lb, La, 57, lengths)
+    check_slices(got, ref, L)
+
+
 def test_config4_backward_full_size(oracle_mod):
     """LLSA backward bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, lengths U[400, 800]."""
     got, ref, L = run_supplied(oracle_mod, 16, 800, 12, 64, 64, 8, 4, (400, 800))
