@@ -185,12 +185,16 @@ int llsa_paper_backward(const void* q, const void* k, const void* v, const void*
  * q, k, v, out, dout : [2][B][T][H][d] inputs; out is llsa_forward's output
  * lse                : float [2][B][H][T] from llsa_forward (required)
  * dq, dk, dv         : [2][B][T][H][d] outputs (padding frames written as 0)
- * Every window and both element types. With SA_BF16 and windows whose bands
- * fit one staged segment it runs on MFMA (one workgroup per 64-frame tile);
- * other windows and SA_F32 run one vector-ALU pass. The staged windows are
- * those where every (output, branch) segment's sweep fits 144 rows at d = 64
- * (288 at d = 32): for example Lb + La <= 40 for any La, Lb = 32 with
- * La = 16, and Lb + La <= 80 with La <= 15; Lb = 64 with La = 16 is not.
+ * Every window and both element types. With SA_BF16 it runs on MFMA when
+ * the bands fit: for B <= 64 at d = 64, windows whose bands fit the LDS rings
+ * of the persistent kernel (one workgroup per compute unit, 32-frame steps;
+ * e.g. Lb = 64 with La = 8 or 16) run there; other windows whose every
+ * (output, branch) segment's sweep fits 144 staged rows at d = 64 (288 at
+ * d = 32), for example Lb + La <= 40 for any La, Lb = 32 with La = 16, and
+ * Lb + La <= 80 with La <= 15, run one workgroup per 64-frame tile. Other
+ * windows and SA_F32 run one vector-ALU pass. Results do not depend on which
+ * kernel runs beyond rounding: the persistent kernel adds one half of branch
+ * L's dk and dv sums to the other after rounding it to bfloat16.
  */
 int llsa_backward(const void* q, const void* k, const void* v, const void* out,
                   const float* lse, const void* dout, void* dq, void* dk, void* dv,

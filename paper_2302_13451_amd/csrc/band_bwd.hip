@@ -2116,9 +2116,13 @@ bool llsa_backward_fits(int d, int Lb, int La) {
 
 hipError_t launch_llsa_backward(const LlsaBackwardArgs& x, ElemType et, hipStream_t stream) {
   LlsaBwdDev a{};
-  // bfloat16 windows whose bands fit one staged segment run on MFMA, the rest
-  // on the vector ALUs
-  if (et != kBF16 || !llsa_bwd_geometry(x.d, x.Lb, x.La, a)) return launch_llsa_backward_general(x, et, stream);
+  // bfloat16 windows whose bands fit the persistent kernel's rings (up to 64
+  // sequences, d = 64) or one staged segment run on MFMA, the rest on the
+  // vector ALUs (the segments and origins are set whether or not the staged
+  // segment fits)
+  const bool staged = llsa_bwd_geometry(x.d, x.Lb, x.La, a);
+  const bool ring = et == kBF16 && x.d == 64 && x.B <= kPersistMaxB && llsa_bwd_ring_geometry(a);
+  if (!ring && (et != kBF16 || !staged)) return launch_llsa_backward_general(x, et, stream);
   const size_t branch = static_cast<size_t>(x.B) * x.T * x.H * x.d;
   for (int j = 0; j < 2; ++j) {
     a.q[j] = static_cast<const uint16_t*>(x.q) + j * branch;
@@ -2139,7 +2143,7 @@ hipError_t launch_llsa_backward(const LlsaBackwardArgs& x, ElemType et, hipStrea
   a.scale = 1.f / sqrtf(static_cast<float>(x.d));
   a.scale_log2 = kLog2e * a.scale;
   a.log2_scale = -0.5f * log2f(static_cast<float>(x.d));
-  if (x.d == 64 && x.B <= kPersistMaxB && llsa_bwd_ring_geometry(a)) {
+  if (ring) {
     hipLaunchKernelGGL(llsa_bwd_ring_kernel<64>, dim3(compute_units()), dim3(768), 0, stream, a);
     return hipGetLastError();
   }

@@ -120,6 +120,7 @@ def test_llsa_backward_padded_frames_are_never_read(oracle_mod):
     (12, 700, 10, 64, 20, 0, (100, 700)),
     (16, 600, 8, 64, 24, 16, (50, 600)),
     (20, 520, 12, 64, 64, 8, (0, 520)),
+    (16, 600, 8, 64, 64, 16, (50, 600)),
 ])
 def test_llsa_backward_persistent(oracle_mod, B, T, H, d, Lb, La, lengths):
     got, ref, L = run_supplied(oracle_mod, B, T, H, d, Lb, La, 57, lengths)
@@ -134,9 +135,10 @@ def test_config4_backward_full_size(oracle_mod):
     check_end_to_end(got, ref)
 
 
-# Windows past one staged segment (the vector-ALU kernel) and float32, and
-# the staged-window boundary from both sides: Lb = 32, La = 16 still stages
-# (MFMA tile kernel); Lb = 64, La = 16 does not.
+# Windows past one staged segment and float32 (the vector-ALU kernel), and the
+# boundaries from both sides: Lb = 32, La = 16 still stages (MFMA); Lb = 64,
+# La = 16 does not stage but fits the persistent kernel's rings at bfloat16
+# (MFMA for up to 64 sequences at d = 64); Lb = 70, La = 20 fits neither.
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("B,T,H,d,Lb,La,lengths", [
     (2, 200, 2, 64, 70, 20, (60, 200)),
