@@ -6,7 +6,10 @@ workload (B=16, T=800, H=12, d=64, Lb=64, La=8, lengths U[400, 800], bf16,
 synthetic N(0,1)/sqrt(d) inputs and N(0,1) upstream gradient). The headline
 value is valid frames per second over the whole step. Inputs are resident in
 HBM before timing; four copies of the batch are rotated so that no step finds
-its inputs in the 256 MB Infinity Cache.
+its inputs in the 256 MB Infinity Cache. Every timed loop starts after 50 ms
+of the same launches back to back (``clock_ramp_ms``), so that it measures the
+kernels at the GPU's working clocks rather than their ramp from idle; the W
+warmup steps follow the ramp.
 
 The same run also measures:
   * the device-copy reference of the library at the backward's traffic size,
@@ -60,6 +63,12 @@ BF16_DENSE_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, published
 WORKLOAD = dict(B=16, T=800, H=12, d=64, Lb=64, La=8, lengths=(400, 800), seed=3)
 STREAM = dict(S=64, H=12, d=64, Lb=64, La=8, steps=1000, seed=5)
 N_SETS = 4
+# Seconds of back-to-back launches of the same calls before every timed loop:
+# from idle the GPU takes some tens of milliseconds of sustained load to reach
+# its working clocks, and a loop timed before that (the headline step at 5
+# warmup steps reads about 58 us instead of 54 us) measures the ramp, not the
+# kernels. The W warmup steps of the contract follow the ramp.
+RAMP_S = 0.05
 
 
 def log(msg):
@@ -166,14 +175,18 @@ def sa_step(s, lengths, w, tf=None, tb=None, sb=None):
 def bench_sa(steps, warmup):
     w = WORKLOAD
     sets, lengths, host_lengths = sa_sets(w)
-    for i in range(max(warmup, N_SETS)):
-        sa_step(sets[i % N_SETS], lengths, w)
+    # every set's out and lse from its own forward first
+    for i in range(N_SETS):
+        sa_step(sets[i], lengths, w)
     torch.cuda.synchronize()
     # each step marshalled once: the timed loop issues bare C-ABI calls; step
-    # i runs the forward on set i and the backward on set i + 2 (every set's
-    # out and lse are already those of its own forward)
+    # i runs the forward on set i and the backward on set i + 2
     step_calls = [bd.prepared(sa_step, sets[i], lengths, w, sb=sets[(i + 2) % N_SETS])
                   for i in range(N_SETS)]
+    ramp(step_calls)
+    for i in range(warmup):
+        step_calls[i % N_SETS]()
+    torch.cuda.synchronize()
     # the timed steps carry no events of their own: an event between two
     # kernels costs more than the gap it measures
     start = torch.cuda.Event(enable_timing=True)
@@ -201,12 +214,27 @@ def bench_sa(steps, warmup):
                 bwd_ms=launch_ms(bwd, sets, n), lengths=host_lengths)
 
 
+def ramp(calls):
+    """Issues the calls back to back, in rounds of 50, until RAMP_S seconds of
+    wall time have passed with the GPU kept busy."""
+    t0 = time.perf_counter()
+    i = 0
+    while True:
+        for _ in range(50):
+            calls[i % len(calls)]()
+            i += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= RAMP_S:
+            return
+
+
 def launch_ms(fn, sets, n):
     """Average duration of n back-to-back launches, from HIP events recorded on
     the stream the library launches on (the current one). Each set's call is
     marshalled once (binding.prepared), so the loop issues bare C-ABI calls and
     the host keeps ahead of even the shortest kernels."""
     calls = [bd.prepared(fn, s) for s in sets]
+    ramp(calls)
     s0 = torch.cuda.Event(enable_timing=True)
     s1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -975,6 +1003,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "clock_ramp_ms": RAMP_S * 1e3,
         "ms_per_step": r["total_ms"] / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
