@@ -1510,6 +1510,26 @@ __device__ __forceinline__ void llsa_bwd_zero_padding(const LlsaBwdDev& a, const
   }
 }
 
+// The persistent kernel's work list is the steps of all (sequence, head)
+// slices in order, two per 64-frame tile. Shares are cut by cost: a step
+// costs one unit and the first step of a slice kRestartUnits more (its whole
+// bands are copied while no step of its own runs), so that a workgroup whose
+// share starts a slice takes fewer steps. cinc: inclusive prefix over
+// sequences (lane b) of the cost of all their slices. Returns the first step
+// whose cost starts at or after cost point c (nsteps when c is past the end).
+constexpr int kRestartUnits = 1;
+__device__ __forceinline__ int ring_step_at_cost(const SeqTable<1>& st, int cinc, int c, int nsteps) {
+  constexpr int R = kRestartUnits;
+  if (c >= __builtin_amdgcn_readlane(cinc, 63)) return nsteps;
+  const int b = __builtin_popcountll(__ballot(cinc <= c));
+  const int lc = c - (b == 0 ? 0 : __builtin_amdgcn_readlane(cinc, b - 1));
+  const int nt = st.nt(b);
+  const int h = lc / (2 * nt + R);
+  const int u = lc - h * (2 * nt + R);  // units 0 .. R: the first step's; k + R: step k >= 1
+  const int k = u == 0 ? 0 : (u <= R ? 1 : u - R);
+  return 2 * (st.before(b) + h * nt) + k;
+}
+
 template <int D>
 __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
   constexpr int NB = D / 16, RL = kLlsaRingL, RC = kLlsaRingC, ST = kLlsaStep;
@@ -1538,9 +1558,16 @@ __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
   // shares, which share the band rows around their boundary, on one XCD
   const int sid = G % 8 == 0 ? static_cast<int>(blockIdx.x % 8) * (G / 8) + static_cast<int>(blockIdx.x / 8)
                              : static_cast<int>(blockIdx.x);
-  const int g0 = static_cast<int>(static_cast<long long>(sid) * ntl / G);
-  const int g1 = static_cast<int>(static_cast<long long>(sid + 1) * ntl / G);
-  const int nhs = 2 * (g1 - g0);  // steps of this workgroup
+  int cinc = lane < a.B && st.ntv > 0 ? H * (2 * st.ntv + kRestartUnits) : 0;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int x = __shfl_up(cinc, o);
+    if (lane >= o) cinc += x;
+  }
+  const long long cost = __builtin_amdgcn_readlane(cinc, 63);
+  const int q0 = ring_step_at_cost(st, cinc, static_cast<int>(sid * cost / G), 2 * ntl);
+  const int q1 = ring_step_at_cost(st, cinc, static_cast<int>((sid + 1) * cost / G), 2 * ntl);
+  const int nhs = q1 - q0;  // steps of this workgroup
   // the step after (c, hh): the second half of the tile, or the next tile
   auto advance = [&](TileCursor<1>& c, int& hh) {
     if (hh == 0) {
@@ -1554,7 +1581,7 @@ __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
   if (w >= 8) {
     __builtin_amdgcn_s_setprio(3);  // as in the SA kernel
     const int lw = w - 8;
-    if (g0 < g1) {
+    if (nhs > 0) {
       RingRegs<D, ROWS> rg[2];
       // the copies of step (c, hh) into slots sl (query and branch-L rings)
       // and sc (branch-C rings): all band rows, or the 32 past its
@@ -1584,8 +1611,8 @@ __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
         }
       };
       TileCursor<1> ca;
-      ca.seek(st, g0);
-      int ha = 0, sl = 0, sc = 0;
+      ca.seek(st, q0 >> 1);
+      int ha = q0 & 1, sl = 0, sc = 0;
       bool cold = true;
       issue(ca, ha, sl, sc, true);
       for (int hs = 0; hs < nhs; ++hs) {
@@ -1623,7 +1650,7 @@ __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
     llsa_bwd_zero_padding<D>(a, st, G, tid - 512);
     return;
   }
-  if (g0 >= g1) return;
+  if (nhs <= 0) return;
 
   const int col = lane & 15;
   const int wq = w & 1;  // 16-row group of the step
@@ -1643,8 +1670,8 @@ __global__ __launch_bounds__(768) void llsa_bwd_ring_kernel(LlsaBwdDev a) {
   // each kind of wave runs its own loop over the steps (two barriers per
   // step, as the loaders), so that no wave holds another kind's values
   TileCursor<1> cur;
-  cur.seek(st, g0);
-  int hh = 0, sl = 0, sc = 0;
+  cur.seek(st, q0 >> 1);
+  int hh = q0 & 1, sl = 0, sc = 0;
   auto ring_row = [](int x, int RR) { return x >= RR ? x - RR : x; };
   auto next_step = [&]() {
     advance(cur, hh);
