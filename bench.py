@@ -217,6 +217,8 @@ def bench_sa(steps, warmup):
 def ramp(calls):
     """Issues the calls back to back, in rounds of 50, until RAMP_S seconds of
     wall time have passed with the GPU kept busy."""
+    if RAMP_S <= 0:
+        return
     t0 = time.perf_counter()
     i = 0
     while True:
@@ -957,7 +959,12 @@ def main():
                     help="only run a plain device copy of 512 MiB (counter calibration)")
     ap.add_argument("--memory-experiment", action="store_true",
                     help="only measure memory per training vector, SA against masked attention")
+    ap.add_argument("--ramp-ms", type=float, default=RAMP_S * 1e3,
+                    help="milliseconds of back-to-back launches before every timed loop (0 for "
+                         "profiler runs, whose per-dispatch records it would multiply)")
     args = ap.parse_args()
+    global RAMP_S
+    RAMP_S = max(0.0, args.ramp_ms) * 1e-3
     if args.gpus != 1:
         print("bench.py runs on one GPU only: --gpus %d is not supported (the band kernels shard "
               "over batch and heads with no communication)" % args.gpus, file=sys.stderr)
