@@ -945,6 +945,7 @@ def cpu_baseline(min_seconds=10.0):
 
 
 def main():
+    global RAMP_S
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
@@ -963,7 +964,6 @@ def main():
                     help="milliseconds of back-to-back launches before every timed loop (0 for "
                          "profiler runs, whose per-dispatch records it would multiply)")
     args = ap.parse_args()
-    global RAMP_S
     RAMP_S = max(0.0, args.ramp_ms) * 1e-3
     if args.gpus != 1:
         print("bench.py runs on one GPU only: --gpus %d is not supported (the band kernels shard "
