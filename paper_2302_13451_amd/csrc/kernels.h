@@ -97,8 +97,9 @@ hipError_t launch_llsa_backward(const LlsaBackwardArgs& a, ElemType et, hipStrea
 // Any window and either element type, on the vector ALUs (llsa_bwd_general.hip).
 hipError_t launch_llsa_backward_general(const LlsaBackwardArgs& a, ElemType et, hipStream_t stream);
 
-// Whether launch_llsa_backward supports the window (its bands must fit the
-// staged segment).
+// Whether the window's bands fit one staged segment of the tile kernel (the
+// MFMA path of launch_llsa_backward for bfloat16 outside the persistent
+// kernel's rings; every other window runs on the vector ALUs).
 bool llsa_backward_fits(int d, int Lb, int La);
 
 struct StreamStepArgs {
