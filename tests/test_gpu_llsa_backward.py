@@ -127,6 +127,18 @@ def test_llsa_backward_persistent(oracle_mod, B, T, H, d, Lb, La, lengths):
     check_slices(got, ref, L)
 
 
+def test_llsa_backward_persistent_padded_frames_are_never_read(oracle_mod):
+    """NaN in every padding frame, with several slices per workgroup of the
+    persistent kernel (steps that continue and steps that start a slice)."""
+    got, ref, L = run_supplied(oracle_mod, 24, 400, 12, 64, 64, 8, 58, (50, 399), pad=float("nan"))
+    for g in got:
+        assert np.all(np.isfinite(g))
+    check_slices(got, ref, L)
+    for g in got:
+        for b, n in enumerate(L):
+            assert np.all(g[:, b, n:] == 0.0)
+
+
 def test_config4_backward_full_size(oracle_mod):
     """LLSA backward bf16, B=16, T=800, H=12, d=64, Lb=64, La=8, lengths U[400, 800]."""
     got, ref, L = run_supplied(oracle_mod, 16, 800, 12, 64, 64, 8, 4, (400, 800))
